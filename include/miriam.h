@@ -1,0 +1,309 @@
+/*
+ * miriam.h — C ABI of the Miriam elastic-kernel library for AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Miriam: Exploiting Elastic Kernels for Real-time Multi-DNN Inference on
+ * Edge GPU" (Zhao, Ling, Guan, Xing; arXiv 2307.04339).
+ *
+ * Three groups of entry points:
+ *   1. Elastic operators (§6.1 elastic block, §6.2 elastic grid, §6.4 index functions):
+ *      create an operator over caller-owned device buffers, query its logical tile
+ *      space, and launch any contiguous shard [shard_begin, shard_begin+shard_len) of
+ *      that tile space with any grid and any block of 64, 128 or 256 threads.  The
+ *      output is bitwise identical for every shard plan, shard order, grid and block.
+ *   2. Design-space shrinking and shard planning (§6.2 Eq. (1), §6.3 Eq. (2), (4), (5),
+ *      §7 shaded binary tree): host-only functions, usable without a GPU.
+ *   3. The runtime coordinator (§5.2, §7): two task queues (critical and normal),
+ *      critical tasks run unsharded, normal tasks are cut into elastic shards sized to
+ *      the resources the critical kernels leave free.
+ *
+ * Conventions (all entry points):
+ *   - Every function returns an int: MIRIAM_OK (0) or a negative miriam_err.  No C++
+ *     exception and no abort crosses this boundary.  miriam_last_error() returns a
+ *     thread-local text for the last failure on the calling thread.
+ *   - Pointers named "device" are HIP device addresses owned by the caller; the
+ *     library never frees them.  Streams are hipStream_t values passed as void*
+ *     (NULL = the legacy default stream).
+ *   - Element types: activations/weights/outputs use the operator's dtype; per-channel
+ *     parameters (bias, batch-norm, layer-norm gamma/beta) are always float32.
+ *   - Layouts: activations NHWC; convolution weights [Cout][KH][KW][Cin/groups];
+ *     depthwise weights [KH][KW][C]; GEMM computes Y[m][n] = sum_k A[m][k] * B[n][k]
+ *     (B "K-major") or sum_k A[m][k] * B[k][n] (B "N-major").
+ */
+#ifndef MIRIAM_H
+#define MIRIAM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MIRIAM_OK = 0,
+    MIRIAM_EINVAL = -1,    /* malformed argument (null pointer, bad enum, bad shape) */
+    MIRIAM_ERANGE = -2,    /* shard outside [0, T), grid < 1 or unsupported block size */
+    MIRIAM_EHIP = -3,      /* the HIP runtime reported an error (text in miriam_last_error) */
+    MIRIAM_ENOMEM = -4,    /* host or device allocation failed */
+    MIRIAM_EBUSY = -5,     /* object still referenced by work in flight */
+    MIRIAM_ESTATE = -6,    /* call not valid in the current state (e.g. not initialised) */
+    MIRIAM_ENOTFOUND = -7  /* unknown ticket or handle */
+} miriam_err;
+
+typedef enum {
+    MIRIAM_OP_CONV2D = 0,    /* implicit-GEMM convolution (+ fused epilogue) */
+    MIRIAM_OP_GEMM = 1,      /* fully connected / matrix product (+ fused epilogue) */
+    MIRIAM_OP_BGEMM = 2,     /* strided batched matrix product (attention scores, context) */
+    MIRIAM_OP_DWCONV = 3,    /* depthwise convolution (+ fused epilogue) */
+    MIRIAM_OP_POOL_MAX = 4,  /* max pooling, ignored padding */
+    MIRIAM_OP_POOL_AVG = 5,  /* average pooling, divisor = window size */
+    MIRIAM_OP_SOFTMAX = 6,   /* row softmax of scale * x */
+    MIRIAM_OP_LAYERNORM = 7, /* row layer normalisation (+ residual added first) */
+    MIRIAM_OP_BN_ACT = 8     /* elementwise epilogue: act(BN(x + bias) + residual) */
+} miriam_op_kind;
+
+typedef enum { MIRIAM_F32 = 0, MIRIAM_F16 = 1, MIRIAM_BF16 = 2 } miriam_dtype;
+
+typedef enum { MIRIAM_ACT_NONE = 0, MIRIAM_ACT_RELU = 1, MIRIAM_ACT_RELU6 = 2, MIRIAM_ACT_GELU = 3 } miriam_act;
+
+/* Epilogue flags for CONV2D, GEMM, BGEMM, DWCONV and BN_ACT, applied in this order:
+ * v = acc (+ bias[c]); v = BN(v); v = v (+ residual); y = act(v). */
+enum {
+    MIRIAM_EPI_BIAS = 1,      /* bias: float32[Cout] */
+    MIRIAM_EPI_BN = 2,        /* bn: float32[4*Cout] = gamma, beta, running mean, running var */
+    MIRIAM_EPI_RESIDUAL = 4   /* residual: same dtype/layout/strides as y */
+};
+
+/*
+ * Operator descriptor.  Fields not used by a kind are ignored.
+ *   CONV2D / DWCONV / POOL_*: x is N x H x W x C (NHWC, pixel stride C unless ldx > 0),
+ *       y is N x Ho x Wo x K (pixel stride K unless ldy > 0), Ho = (H + 2 pad - kh)/stride + 1.
+ *       CONV2D: wt is [K][kh][kw][C/groups] (groups must be 1).  DWCONV: wt is [kh][kw][C],
+ *       K = C.  POOL: K = C, kh x kw window.
+ *   GEMM:  A = x is m x kk (row stride ldx, default kk), B = wt is nn x kk (row stride ldw,
+ *       default kk), y is m x nn (row stride ldy, default nn).
+ *   BGEMM: batch matrices; batch index bi splits as (bi / batch_div, bi % batch_div) and
+ *       operand X's offset is (bi / batch_div) * sX0 + (bi % batch_div) * sX1 elements.
+ *       b_nmajor = 0: B[n][k] (row stride ldw); 1: B[k][n] (row stride ldw).
+ *   SOFTMAX: x, y are m rows of nn values (row strides ldx, ldy); y = softmax(scale * x).
+ *   LAYERNORM: y = LN(x (+ residual)) * gamma + beta over rows of nn; gamma = wt, beta = bias
+ *       (float32[nn]).
+ *   BN_ACT: x, y are m rows of nn channels; epilogue flags as above.
+ */
+typedef struct miriam_op_desc {
+    int32_t kind;       /* miriam_op_kind */
+    int32_t dtype;      /* miriam_dtype */
+    int32_t act;        /* miriam_act */
+    int32_t flags;      /* MIRIAM_EPI_* */
+    int64_t n, h, w, c; /* input geometry (NHWC) */
+    int64_t k;          /* output channels (CONV2D) */
+    int64_t kh, kw, stride, pad, groups;
+    int64_t m, nn, kk;  /* GEMM-style sizes */
+    int64_t batch, batch_div;
+    int64_t ldx, ldw, ldy;               /* row strides in elements, 0 = dense */
+    int64_t sx0, sx1, sw0, sw1, sy0, sy1; /* BGEMM batch strides in elements */
+    int32_t b_nmajor;
+    int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128 tiles */
+    float eps;          /* BN / LN epsilon */
+    float scale;        /* SOFTMAX scale */
+    const void *x, *wt, *bias, *bn, *residual; /* device pointers (wt = weights) */
+    void *y;                                 /* device pointer */
+} miriam_op_desc;
+
+typedef struct miriam_op miriam_op;     /* opaque; created by miriam_op_create */
+typedef struct miriam_task miriam_task; /* opaque; an ordered list of ops = one request */
+
+typedef struct miriam_op_info {
+    int64_t num_tiles;        /* T: size of the logical tile space */
+    int32_t logical_block;    /* threads of the logical block (256 = 4 logical waves) */
+    int32_t lds_bytes;        /* LDS per workgroup; independent of the physical block */
+    int32_t tile_m, tile_n;   /* contraction tile shape (0 for other kinds) */
+    int32_t max_wg_per_cu[3]; /* resident workgroups per CU for blocks 64, 128, 256 (0 if unknown) */
+    double flops;             /* algorithmic floating-point operations of the whole op */
+    double bytes;             /* algorithmic HBM bytes: inputs and weights read once, outputs written once */
+} miriam_op_info;
+
+/* ------------------------------------------------------------------ device */
+typedef struct miriam_device_desc {
+    int32_t n_cu;              /* compute units (N_SM of Table 1) */
+    int32_t max_threads_per_cu; /* L_threads of Table 1 */
+    int32_t lds_per_cu;        /* bytes */
+    int32_t n_xcd;             /* dies that workgroups are dealt round-robin to */
+    int32_t wave_size;
+    int32_t clock_khz;
+    char arch[64];
+} miriam_device_desc;
+
+/* Query the current HIP device.  Returns MIRIAM_EHIP if no device is present. */
+int miriam_device_query(miriam_device_desc *out);
+
+/* ---------------------------------------------------------- elastic operators */
+
+/* Validate *d and create an operator that borrows the device pointers in *d until
+ * miriam_op_destroy.  Allocates host memory only.  §6.4: the operator's index
+ * function is computation-based (logical ids computed in-kernel). */
+int miriam_op_create(const miriam_op_desc *d, miriam_op **out);
+
+/* Fill *out with the operator's tile space and resource figures. */
+int miriam_op_query(const miriam_op *op, miriam_op_info *out);
+
+/*
+ * §6.1-6.2: launch shard [shard_begin, shard_begin + shard_len) of the operator's
+ * tile space on `stream` with `grid` workgroups of `block` threads (64, 128 or 256).
+ * Workgroup g runs tiles shard_begin + r(g) + i*grid (i = 0, 1, ...) below the shard's
+ * end, where r(g) ranks workgroups so that those on one die take consecutive tiles.
+ * A grid larger than shard_len is legal (the surplus workgroups exit at once).
+ * Asynchronous: no synchronisation and no allocation.  Returns MIRIAM_ERANGE without
+ * launching anything if 0 <= shard_begin, 1 <= shard_len, shard_begin + shard_len <= T,
+ * grid >= 1 or block in {64,128,256} does not hold.
+ */
+int miriam_elastic_launch(const miriam_op *op, int64_t shard_begin, int64_t shard_len,
+                          int grid, int block, void *stream);
+
+/*
+ * Same launch, additionally recording for every tile t of the shard, in caller-owned
+ * device arrays of T int32 entries: owner_wg[t] = physical workgroup, owner_iter[t] =
+ * persistent-loop iteration, and count[t] += 1 (atomic).  Used to check the tile map.
+ */
+int miriam_elastic_launch_traced(const miriam_op *op, int64_t shard_begin, int64_t shard_len,
+                                 int grid, int block, void *stream,
+                                 int32_t *owner_wg, int32_t *owner_iter, int32_t *count);
+
+/* Release the operator.  MIRIAM_EBUSY if a submitted task that uses it is pending. */
+int miriam_op_destroy(miriam_op *op);
+
+/* ------------------------------------------------------ planning (host only) */
+
+/* Eq. (1): dichotomy slice widths of a kernel with M blocks, smallest first.
+ * Returns the number of widths written (n+1), or MIRIAM_EINVAL / MIRIAM_ERANGE (cap). */
+int miriam_plan_dichotomy(int64_t M, int64_t *widths, int cap);
+
+/* Balanced slicing plan of T tiles into n shards: shard j = [floor(jT/n), floor((j+1)T/n)). */
+int miriam_plan_split(int64_t T, int64_t n, int64_t *begin, int64_t *len);
+
+/* Logical rank of physical workgroup g in a launch of G workgroups over n_xcd dies. */
+int64_t miriam_plan_wg_rank(int64_t g, int64_t G, int64_t n_xcd);
+
+/* Eq. (2): largest elastic grid and block next to a critical kernel of n_blk_rt
+ * workgroups of s_blk_rt threads. */
+int64_t miriam_plan_eq2_grid_limit(int64_t n_sm, int64_t n_blk_rt);
+int64_t miriam_plan_eq2_block_limit(int64_t l_threads, int64_t s_blk_rt);
+
+/* Eq. (4) WIScore, second factor read as (S_blk_rt + S_blk_be) / L_threads. */
+double miriam_plan_wiscore(int64_t n_sm, int64_t l_threads, int64_t n_blk_rt, int64_t s_blk_rt,
+                           int64_t n_blk_be, int64_t s_blk_be);
+
+/* Eq. (5) OScore over n shards' launch-overhead terms. */
+int miriam_plan_oscore(int64_t n, const double *lo_blk, const double *lo_pt,
+                       double max_blk, double max_pt);
+
+/* §6.3: keep the best ceil(frac*n) (>= 1) candidates by (score, grid, block), best first.
+ * Returns the number kept. */
+int miriam_plan_top_fraction(int n, const double *score, const int64_t *grid,
+                             const int64_t *block, double frac, int *keep);
+
+/* §7 shaded binary tree: length of the shallowest node that starts at `cursor` and
+ * holds at most max_len tiles; *depth receives its depth.  Negative on bad input. */
+int64_t miriam_plan_tree_head(int64_t T, int64_t cursor, int64_t max_len, int *depth);
+
+/* ------------------------------------------------------------- coordinator */
+
+typedef enum {
+    MIRIAM_POLICY_ELASTIC = 0,     /* Miriam: critical unsharded, normal as elastic shards */
+    MIRIAM_POLICY_SEQUENTIAL = 1,  /* one request at a time, critical first (baseline) */
+    MIRIAM_POLICY_MULTISTREAM = 2  /* every task on its own stream, full kernels (baseline) */
+} miriam_policy;
+
+typedef enum { MIRIAM_BACKEND_HIP = 0, MIRIAM_BACKEND_FAKE = 1 } miriam_backend;
+
+typedef struct miriam_config {
+    int32_t policy;          /* miriam_policy */
+    int32_t backend;         /* miriam_backend; FAKE simulates a device on the host (tests) */
+    int32_t n_be_streams;    /* streams for normal tasks (1..3) */
+    int32_t inflight_depth;  /* max shards in flight per normal stream (>= 1) */
+    double top_frac;         /* §6.3 kept fraction (0.2) */
+    double max_blk_frac;     /* Eq. (5) MAX_blk as a fraction of the unsharded time (0.1) */
+    double max_pt_frac;      /* Eq. (5) MAX_pt as a fraction of the unsharded time (0.1) */
+    double quantum_us;       /* target duration of one normal shard */
+    int32_t log_launches;    /* keep miriam_launch_record entries (diagnostics, tests) */
+    int32_t profile_reps;    /* timed repetitions per op when a task is created (HIP backend) */
+    /* FAKE backend only: simulated compute units, WG slots per CU, ns per tile, launch ns */
+    int32_t fake_n_cu, fake_slots_per_cu;
+    double fake_tile_ns, fake_launch_ns;
+} miriam_config;
+
+typedef struct miriam_completion {
+    uint64_t ticket;
+    int32_t criticality;     /* 1 critical, 0 normal */
+    int32_t status;          /* MIRIAM_OK or the error that failed the task */
+    int64_t t_release_ns;    /* scheduled release (CLOCK_MONOTONIC) */
+    int64_t t_start_ns;      /* first launch of the task */
+    int64_t t_end_ns;        /* completion observed */
+    int64_t deadline_ns;     /* absolute; 0 = none */
+    int32_t deadline_met;    /* 1 if no deadline or t_end <= deadline */
+    int32_t n_shards;        /* launches issued for this request */
+} miriam_completion;
+
+typedef struct miriam_stats {
+    int64_t launches;         /* kernel launches issued */
+    int64_t shards_sized;     /* normal shards sized next to a critical kernel */
+    int64_t eq2_violations;   /* normal shards launched above the Eq. (2) limit (must stay 0) */
+    int64_t decisions;        /* shard decisions taken */
+    double decision_ns_total; /* host time spent deciding */
+    int64_t completed;        /* requests completed */
+} miriam_stats;
+
+/* Start the coordinator (creates its streams and its dispatcher thread). */
+int miriam_init(const miriam_config *cfg);
+
+/* Group ops (run in order) into one inference request template.  The task borrows the ops. */
+int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out);
+
+/* Submit one request of `task`.  criticality 1 = critical queue, 0 = normal queue.
+ * release_ns: absolute CLOCK_MONOTONIC time before which it is held back (0 = now).
+ * deadline_ns: absolute, 0 = none (recorded; ties among pending critical requests are
+ * broken by earliest deadline).  Thread-safe. */
+int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_t deadline_ns,
+                  uint64_t *ticket_out);
+
+/* Non-blocking: move up to max_out completion records into out; returns the count. */
+int miriam_poll(miriam_completion *out, int max_out);
+
+/* Block until every submitted request has completed or timeout_ms passes
+ * (MIRIAM_EBUSY on timeout). */
+int miriam_drain(int64_t timeout_ms);
+
+/* Counters since miriam_init. */
+int miriam_stats_get(miriam_stats *out);
+
+/* One launch issued by the coordinator (kept when cfg.log_launches is set). */
+typedef struct miriam_launch_record {
+    uint64_t ticket;       /* request the launch belongs to */
+    int32_t op_index;      /* position of the op in its task */
+    int32_t stream;        /* 0 = critical stream, 1.. = normal streams */
+    int32_t criticality;
+    int32_t grid, block;
+    int32_t crit_busy;     /* a critical request was in flight when the shard was sized */
+    int64_t shard_begin, shard_len, num_tiles;
+    int64_t eq2_grid_limit; /* Eq. (2) grid limit in force (0 if none) */
+    int64_t t_issue_ns;
+} miriam_launch_record;
+
+/* Copy up to max_out of the oldest unread launch records; returns the count. */
+int miriam_launch_log(miriam_launch_record *out, int max_out);
+
+/* MIRIAM_EBUSY if a submitted request of this task is pending. */
+int miriam_task_destroy(miriam_task *t);
+
+/* Drain, stop the dispatcher, destroy internal streams and events. */
+int miriam_shutdown(void);
+
+/* CLOCK_MONOTONIC in ns (the clock of release, start and end stamps). */
+int64_t miriam_now_ns(void);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char *miriam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MIRIAM_H */

@@ -1,0 +1,900 @@
+// Runtime dynamic kernel coordinator (§5.2, §7).
+//
+// Two queues of inference requests: critical and normal.  One dispatcher thread
+// owns every launch.  Critical requests run unsharded, in order, on the
+// critical stream.  Normal requests run as elastic shards on one stream per
+// normal task; each shard is the head node of the op's shaded binary tree
+// (§7), sized either to the whole GPU (no critical work in flight, greedy
+// policy) or to the resources the running critical kernel leaves free, by the
+// Eq. (2) limiters and the WIScore x OScore ranking with the top fraction kept
+// (§6.3).  A bounded number of shards per normal stream is in flight, so a
+// newly released critical request waits at most for the shards already on the
+// GPU.  All streams keep the default priority: the coordinator, not the
+// hardware queue priority, decides what may occupy the GPU.
+//
+// Baseline policies for comparison (§8.1.3): SEQUENTIAL runs one request at a
+// time on one stream, critical first; MULTISTREAM launches every request's
+// kernels unsharded on its task's stream.
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <cmath>
+#include <condition_variable>
+#include <cstring>
+#include <ctime>
+#include <deque>
+#include <mutex>
+#include <new>
+#include <queue>
+#include <thread>
+#include <vector>
+
+#include "internal.h"
+
+namespace miriam {
+
+static int64_t mono_ns() {
+    timespec ts;
+    clock_gettime(CLOCK_MONOTONIC, &ts);
+    return (int64_t)ts.tv_sec * 1000000000LL + ts.tv_nsec;
+}
+
+// ------------------------------------------------------------------ backends
+struct Backend {
+    virtual ~Backend() {}
+    virtual int start(int n_streams) = 0;
+    virtual int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) = 0;
+    virtual int record(int stream) = 0;       // event id >= 0, or < 0 error
+    virtual int query(int ev) = 0;            // 1 done, 0 pending, < 0 error
+    virtual void release(int ev) = 0;
+    virtual double time_us(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int reps) = 0;
+    virtual double launch_gap_us(const miriam_op *op, int reps) = 0;
+    virtual void stop() = 0;
+};
+
+struct HipBackend : Backend {
+    int dev = 0;
+    std::vector<hipStream_t> streams;
+    std::vector<hipEvent_t> events;
+    std::vector<int> free_ev;
+    hipStream_t prof = nullptr;
+
+    int start(int n) override {
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+        for (int i = 0; i < n; ++i) {
+            hipStream_t s;
+            e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+            streams.push_back(s);
+        }
+        e = hipStreamCreateWithFlags(&prof, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+        return MIRIAM_OK;
+    }
+    int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) override {
+        return op_launch(op, b, l, grid, block, streams[stream], nullptr, nullptr, nullptr);
+    }
+    int record(int stream) override {
+        int id;
+        if (!free_ev.empty()) {
+            id = free_ev.back();
+            free_ev.pop_back();
+        } else {
+            hipEvent_t ev;
+            hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+            events.push_back(ev);
+            id = (int)events.size() - 1;
+        }
+        hipError_t e = hipEventRecord(events[id], streams[stream]);
+        if (e != hipSuccess) {
+            free_ev.push_back(id);
+            return hip_fail(e, "hipEventRecord");
+        }
+        return id;
+    }
+    int query(int ev) override {
+        hipError_t e = hipEventQuery(events[ev]);
+        if (e == hipSuccess) return 1;
+        if (e == hipErrorNotReady) return 0;
+        return hip_fail(e, "hipEventQuery");
+    }
+    void release(int ev) override { free_ev.push_back(ev); }
+    double time_us(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int reps) override {
+        hipEvent_t e0, e1;
+        if (hipEventCreate(&e0) != hipSuccess) return -1.0;
+        if (hipEventCreate(&e1) != hipSuccess) {
+            (void)hipEventDestroy(e0);
+            return -1.0;
+        }
+        double best = -1.0;
+        if (op_launch(op, b, l, grid, block, prof, nullptr, nullptr, nullptr) == MIRIAM_OK &&
+            hipStreamSynchronize(prof) == hipSuccess) {
+            for (int r = 0; r < reps; ++r) {
+                (void)hipEventRecord(e0, prof);
+                if (op_launch(op, b, l, grid, block, prof, nullptr, nullptr, nullptr) != MIRIAM_OK) break;
+                (void)hipEventRecord(e1, prof);
+                if (hipEventSynchronize(e1) != hipSuccess) break;
+                float ms = 0.0f;
+                if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) break;
+                const double us = 1000.0 * ms;
+                if (best < 0.0 || us < best) best = us;
+            }
+        }
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+        return best;
+    }
+    double launch_gap_us(const miriam_op *op, int reps) override {
+        // extra time of n back-to-back one-tile launches over one, per launch
+        const int n = 16;
+        hipEvent_t e0, e1;
+        if (hipEventCreate(&e0) != hipSuccess) return -1.0;
+        if (hipEventCreate(&e1) != hipSuccess) {
+            (void)hipEventDestroy(e0);
+            return -1.0;
+        }
+        double best = -1.0;
+        for (int r = 0; r < reps + 1; ++r) {
+            (void)hipEventRecord(e0, prof);
+            bool ok = true;
+            for (int i = 0; i < n && ok; ++i) ok = op_launch(op, 0, 1, 1, 256, prof, nullptr, nullptr, nullptr) == MIRIAM_OK;
+            (void)hipEventRecord(e1, prof);
+            if (!ok || hipEventSynchronize(e1) != hipSuccess) break;
+            float ms = 0.0f;
+            (void)hipEventElapsedTime(&ms, e0, e1);
+            const double us = 1000.0 * ms / n;
+            if (r > 0 && (best < 0.0 || us < best)) best = us;
+        }
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+        return best;
+    }
+    void stop() override {
+        for (hipStream_t s : streams) (void)hipStreamSynchronize(s);
+        for (hipEvent_t e : events) (void)hipEventDestroy(e);
+        for (hipStream_t s : streams) (void)hipStreamDestroy(s);
+        if (prof) {
+            (void)hipStreamSynchronize(prof);
+            (void)hipStreamDestroy(prof);
+        }
+        events.clear();
+        free_ev.clear();
+        streams.clear();
+        prof = nullptr;
+    }
+};
+
+// Host-simulated device for testing the coordinator without a GPU.  Each stream
+// is a FIFO; a launch of l tiles with grid G on a device of n_cu x slots
+// workgroup slots takes launch_ns + ceil(l / min(G, l, n_cu*slots)) * tile_ns.
+struct FakeBackend : Backend {
+    int n_cu = 8, slots = 2;
+    double tile_ns = 1000.0, launch_ns = 2000.0;
+    std::vector<int64_t> busy_until;
+    std::vector<int64_t> ev_time;
+    std::vector<int> free_ev;
+
+    int start(int n) override {
+        busy_until.assign(n, 0);
+        return MIRIAM_OK;
+    }
+    int64_t duration(const miriam_op *op, int64_t l, int grid) const {
+        int64_t conc = std::min<int64_t>(std::min<int64_t>(grid, l), (int64_t)n_cu * slots);
+        int64_t waves = (l + conc - 1) / conc;
+        (void)op;
+        return (int64_t)(launch_ns + waves * tile_ns);
+    }
+    int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) override {
+        if (!op || b < 0 || l < 1 || b + l > op->T || grid < 1 || (block != 64 && block != 128 && block != 256)) {
+            set_error("fake launch: bad shard");
+            return MIRIAM_ERANGE;
+        }
+        const int64_t now = mono_ns();
+        const int64_t st = std::max(now, busy_until[stream]);
+        busy_until[stream] = st + duration(op, l, grid);
+        return MIRIAM_OK;
+    }
+    int record(int stream) override {
+        const int64_t t = std::max(mono_ns(), busy_until[stream]);
+        int id;
+        if (!free_ev.empty()) {
+            id = free_ev.back();
+            free_ev.pop_back();
+            ev_time[id] = t;
+        } else {
+            ev_time.push_back(t);
+            id = (int)ev_time.size() - 1;
+        }
+        return id;
+    }
+    int query(int ev) override { return mono_ns() >= ev_time[ev] ? 1 : 0; }
+    void release(int ev) override { free_ev.push_back(ev); }
+    double time_us(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int reps) override {
+        (void)b; (void)block; (void)reps;
+        return duration(op, l, grid) / 1000.0;
+    }
+    double launch_gap_us(const miriam_op *, int) override { return launch_ns / 1000.0; }
+    void stop() override {}
+};
+
+}  // namespace miriam
+
+using namespace miriam;
+
+// Per-op profile taken when a task is created (a9: occupancy and launch-overhead
+// profiling that feeds Eq. (5)).
+struct OpProf {
+    double t_unsh_us = 0.0;     // unsharded launch (grid = T, block 256)
+    double t_pers_us[3] = {0, 0, 0};  // one persistent shard over the whole GPU, per block
+    double tau1_us[3] = {0, 0, 0};    // time of one tile on one workgroup, per block
+    int cap[3] = {1, 1, 1};     // resident workgroups per CU, per block
+    bool ok_pt[3] = {true, true, true};  // Eq. (5) persistent-thread term under its bar
+    int64_t n_max = 1;          // Eq. (5) launch term: most shards the op may be cut into
+};
+
+struct miriam_task {
+    std::vector<miriam_op *> ops;
+    std::vector<OpProf> prof;
+    int id = 0;
+    std::atomic<int> pending{0};
+};
+
+namespace {
+
+struct Shot {  // one launch in flight
+    int ev;
+    int op;
+};
+
+struct Req {
+    uint64_t ticket = 0;
+    miriam_task *task = nullptr;
+    int crit = 0;
+    int stream = 0;
+    int64_t release = 0, deadline = 0, t_start = 0;
+    int n_shards = 0;
+    int status = MIRIAM_OK;
+    size_t op = 0;       // next op to launch
+    int64_t cursor = 0;  // next tile of that op
+    bool launched_all = false;
+    std::deque<Shot> shots;
+};
+
+struct ReleaseLater {
+    bool operator()(const Req *a, const Req *b) const {
+        if (a->release != b->release) return a->release > b->release;
+        return a->ticket > b->ticket;
+    }
+};
+
+struct Coord {
+    miriam_config cfg{};
+    Backend *be = nullptr;
+    int n_streams = 2;
+    int n_cu = 256, l_threads = 2048;
+    double t_launch_us = 5.0;
+    bool t_launch_measured = false;
+    int next_task_id = 0;
+
+    std::mutex mu;               // inbox, outbox, counters shared with callers
+    std::condition_variable cv;  // wakes the dispatcher
+    std::condition_variable cv_done;
+    std::vector<Req *> inbox;
+    std::deque<miriam_completion> outbox;
+    int64_t outstanding = 0;
+    uint64_t next_ticket = 1;
+    bool stopping = false;
+    std::thread th;
+
+    // dispatcher-owned state
+    std::priority_queue<Req *, std::vector<Req *>, ReleaseLater> timed;
+    std::vector<Req *> crit_ready;                 // released critical requests
+    std::vector<std::deque<Req *>> norm_ready;     // per stream, FIFO
+    std::deque<Req *> crit_active;                 // launched critical requests, stream 0
+    std::vector<std::deque<Req *>> be_active;      // per stream, launched normal requests
+    std::vector<int> inflight;                     // shards in flight per stream
+    int rr_stream = 1;
+
+    std::mutex log_mu;
+    std::vector<miriam_launch_record> log;
+    size_t log_read = 0;
+
+    std::mutex stat_mu;
+    miriam_stats stats{};
+};
+
+Coord *g = nullptr;
+std::mutex g_life;  // serialises init / shutdown
+
+int64_t eq2_limit(int n_cu, int64_t n_rt) { return miriam_plan_eq2_grid_limit(n_cu, n_rt); }
+
+void log_launch(Coord &c, const Req *r, int op_index, int stream, int grid, int block, bool crit_busy,
+                int64_t b, int64_t l, int64_t T, int64_t limit) {
+    if (!c.cfg.log_launches) return;
+    miriam_launch_record rec;
+    rec.ticket = r->ticket;
+    rec.op_index = op_index;
+    rec.stream = stream;
+    rec.criticality = r->crit;
+    rec.grid = grid;
+    rec.block = block;
+    rec.crit_busy = crit_busy ? 1 : 0;
+    rec.shard_begin = b;
+    rec.shard_len = l;
+    rec.num_tiles = T;
+    rec.eq2_grid_limit = limit;
+    rec.t_issue_ns = mono_ns();
+    std::lock_guard<std::mutex> lk(c.log_mu);
+    if (c.log.size() - c.log_read < (1u << 22)) c.log.push_back(rec);
+}
+
+// Launch shard [b, b+l) of op `oi` of request r on `stream` and record its event.
+int issue(Coord &c, Req *r, int oi, int64_t b, int64_t l, int grid, int block, int stream, bool crit_busy,
+          int64_t limit) {
+    const miriam_op *op = r->task->ops[oi];
+    int rc = c.be->launch(op, b, l, grid, block, stream);
+    if (rc != MIRIAM_OK) return rc;
+    int ev = c.be->record(stream);
+    if (ev < 0) return ev;
+    if (r->t_start == 0) r->t_start = mono_ns();
+    r->shots.push_back({ev, oi});
+    r->n_shards++;
+    c.inflight[stream]++;
+    log_launch(c, r, oi, stream, grid, block, crit_busy, b, l, op->T, limit);
+    std::lock_guard<std::mutex> lk(c.stat_mu);
+    c.stats.launches++;
+    return MIRIAM_OK;
+}
+
+void finish(Coord &c, Req *r) {
+    miriam_completion cp;
+    std::memset(&cp, 0, sizeof(cp));
+    cp.ticket = r->ticket;
+    cp.criticality = r->crit;
+    cp.status = r->status;
+    cp.t_release_ns = r->release;
+    cp.t_start_ns = r->t_start;
+    cp.t_end_ns = mono_ns();
+    cp.deadline_ns = r->deadline;
+    cp.deadline_met = (r->deadline == 0 || cp.t_end_ns <= r->deadline) ? 1 : 0;
+    cp.n_shards = r->n_shards;
+    for (miriam_op *op : r->task->ops) op->pending.fetch_sub(1);
+    r->task->pending.fetch_sub(1);
+    delete r;
+    {
+        std::lock_guard<std::mutex> lk(c.mu);
+        c.outbox.push_back(cp);
+        c.outstanding--;
+    }
+    {
+        std::lock_guard<std::mutex> lk(c.stat_mu);
+        c.stats.completed++;
+    }
+    c.cv_done.notify_all();
+}
+
+// Launch every op of a request unsharded (grid = T, block 256) on `stream`.
+void launch_whole(Coord &c, Req *r, int stream) {
+    for (size_t i = 0; i < r->task->ops.size(); ++i) {
+        const miriam_op *op = r->task->ops[i];
+        const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
+        int rc = issue(c, r, (int)i, 0, op->T, grid, 256, stream, false, 0);
+        if (rc != MIRIAM_OK) {
+            r->status = rc;
+            break;
+        }
+    }
+    r->op = r->task->ops.size();
+    r->launched_all = true;
+}
+
+// Retire completed launches of the requests on one stream; returns true if anything completed.
+bool retire(Coord &c, std::deque<Req *> &active, int stream) {
+    bool any = false;
+    while (!active.empty()) {
+        Req *r = active.front();
+        while (!r->shots.empty()) {
+            int q = c.be->query(r->shots.front().ev);
+            if (q == 0) break;
+            if (q < 0) r->status = q;
+            c.be->release(r->shots.front().ev);
+            r->shots.pop_front();
+            c.inflight[stream]--;
+            any = true;
+        }
+        if (r->shots.empty() && r->launched_all) {
+            active.pop_front();
+            finish(c, r);
+            any = true;
+            continue;
+        }
+        break;  // later requests on this stream are behind this one (FIFO)
+    }
+    return any;
+}
+
+// Op index of the critical kernel running now, or -1 if no critical work is in flight.
+int current_critical_op(Coord &c, const miriam_op **op) {
+    if (c.crit_active.empty()) return -1;
+    Req *r = c.crit_active.front();
+    if (r->shots.empty()) return -1;
+    const int oi = r->shots.front().op;
+    *op = r->task->ops[oi];
+    return oi;
+}
+
+struct Decision {
+    int grid, block;
+    int64_t len, limit;
+};
+
+// §6.3 + §7: size the next shard of op `oi` of normal request r.
+Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
+    const miriam_op *op = r->task->ops[r->op];
+    const OpProf &pf = r->task->prof[r->op];
+    const int64_t T = op->T, cursor = r->cursor, remain = T - cursor;
+    Decision d{0, 256, 0, 0};
+    int bi = 2;
+    if (crit_op) {
+        const int64_t n_rt = crit_op->T;  // critical kernels run unsharded: one workgroup per tile
+        const int64_t s_rt = 256;
+        const int64_t gl = eq2_limit(c.n_cu, n_rt);
+        const int64_t sl = miriam_plan_eq2_block_limit(c.l_threads, s_rt);
+        double score[9];
+        int64_t cg[9], cb[9];
+        int n = 0;
+        for (int64_t G : {gl, gl / 2, gl / 4}) {
+            if (G < 1) continue;
+            bool dup = false;
+            for (int i = 0; i < n; ++i) dup |= (cg[i] == G);
+            if (dup) continue;
+            for (int k = 0; k < 3; ++k) {
+                const int64_t B = 64 << k;
+                if (B > sl) continue;
+                cg[n] = G;
+                cb[n] = B;
+                score[n] = miriam_plan_wiscore(c.n_cu, c.l_threads, n_rt, s_rt, G, B) * (pf.ok_pt[k] ? 1.0 : 0.0);
+                ++n;
+            }
+        }
+        if (n == 0) {  // no feasible candidate: smallest footprint
+            cg[0] = 1;
+            cb[0] = 64;
+            score[0] = 0.0;
+            n = 1;
+        }
+        int keep[9];
+        const int k = miriam_plan_top_fraction(n, score, cg, cb, c.cfg.top_frac, keep);
+        (void)k;
+        d.grid = (int)cg[keep[0]];
+        d.block = (int)cb[keep[0]];
+        d.limit = gl;
+        bi = d.block == 64 ? 0 : (d.block == 128 ? 1 : 2);
+    } else {
+        // alone on the GPU: greedy, the whole device
+        bi = pf.ok_pt[2] ? 2 : (pf.ok_pt[1] ? 1 : (pf.ok_pt[0] ? 0 : 2));
+        d.block = 64 << bi;
+        d.grid = (int)std::min<int64_t>((int64_t)c.n_cu * std::max(1, pf.cap[bi]), INT32_MAX);
+    }
+    // tiles per workgroup within one time quantum
+    const double tau = pf.tau1_us[bi] > 0.0 ? pf.tau1_us[bi] : 1.0;
+    int64_t iters = (int64_t)std::floor(c.cfg.quantum_us / tau);
+    if (iters < 1) iters = 1;
+    int64_t max_len = (int64_t)d.grid * iters;
+    const int64_t min_len = (T + pf.n_max - 1) / std::max<int64_t>(1, pf.n_max);
+    max_len = std::max(max_len, min_len);
+    max_len = std::max<int64_t>(1, std::min(max_len, remain));
+    int depth = 0;
+    int64_t len = miriam_plan_tree_head(T, cursor, max_len, &depth);
+    if (len < 1) len = std::min<int64_t>(remain, max_len);
+    d.len = len;
+    d.grid = (int)std::max<int64_t>(1, std::min<int64_t>(d.grid, len));
+    return d;
+}
+
+// Issue shards for the normal requests of one stream while its in-flight budget lasts.
+bool pump_normal(Coord &c, int s) {
+    bool any = false;
+    while (c.inflight[s] < c.cfg.inflight_depth) {
+        Req *r = nullptr;
+        for (Req *q : c.be_active[s])
+            if (!q->launched_all) {
+                r = q;
+                break;
+            }
+        if (!r) {
+            if (c.norm_ready[s].empty()) break;
+            r = c.norm_ready[s].front();
+            c.norm_ready[s].pop_front();
+            c.be_active[s].push_back(r);
+        }
+        const int64_t t0 = mono_ns();
+        const miriam_op *crit_op = nullptr;
+        const bool busy = current_critical_op(c, &crit_op) >= 0;
+        Decision d = decide(c, r, busy ? crit_op : nullptr);
+        const int64_t t1 = mono_ns();
+        const int oi = (int)r->op;
+        int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit);
+        {
+            std::lock_guard<std::mutex> lk(c.stat_mu);
+            c.stats.decisions++;
+            c.stats.decision_ns_total += (double)(t1 - t0);
+            if (busy) {
+                c.stats.shards_sized++;
+                if (d.grid > d.limit) c.stats.eq2_violations++;
+            }
+        }
+        any = true;
+        if (rc != MIRIAM_OK) {
+            r->status = rc;
+            r->launched_all = true;
+            continue;
+        }
+        r->cursor += d.len;
+        if (r->cursor >= r->task->ops[oi]->T) {
+            r->cursor = 0;
+            r->op++;
+            if (r->op >= r->task->ops.size()) r->launched_all = true;
+        }
+    }
+    return any;
+}
+
+bool all_idle(Coord &c) {
+    if (!c.crit_active.empty()) return false;
+    for (auto &q : c.be_active)
+        if (!q.empty()) return false;
+    return true;
+}
+
+void dispatcher(Coord *cp) {
+    Coord &c = *cp;
+    if (c.cfg.backend == MIRIAM_BACKEND_HIP) (void)hipSetDevice(static_cast<HipBackend *>(c.be)->dev);
+    for (;;) {
+        {
+            std::unique_lock<std::mutex> lk(c.mu);
+            for (Req *r : c.inbox) c.timed.push(r);
+            c.inbox.clear();
+            if (c.stopping && c.outstanding == 0) break;
+        }
+        const int64_t now = mono_ns();
+        while (!c.timed.empty() && c.timed.top()->release <= now) {
+            Req *r = c.timed.top();
+            c.timed.pop();
+            if (r->crit) c.crit_ready.push_back(r);
+            else c.norm_ready[r->stream].push_back(r);
+        }
+        bool progress = false;
+        // retire finished work
+        progress |= retire(c, c.crit_active, 0);
+        for (int s = 1; s < c.n_streams; ++s) progress |= retire(c, c.be_active[s], s);
+
+        // order pending critical requests: earliest deadline, then release, then ticket
+        if (c.crit_ready.size() > 1)
+            std::stable_sort(c.crit_ready.begin(), c.crit_ready.end(), [](const Req *a, const Req *b) {
+                const int64_t da = a->deadline ? a->deadline : INT64_MAX, db = b->deadline ? b->deadline : INT64_MAX;
+                if (da != db) return da < db;
+                if (a->release != b->release) return a->release < b->release;
+                return a->ticket < b->ticket;
+            });
+
+        if (c.cfg.policy == MIRIAM_POLICY_SEQUENTIAL) {
+            if (all_idle(c)) {
+                if (!c.crit_ready.empty()) {
+                    Req *r = c.crit_ready.front();
+                    c.crit_ready.erase(c.crit_ready.begin());
+                    launch_whole(c, r, 0);
+                    c.crit_active.push_back(r);
+                    progress = true;
+                } else {
+                    for (int k = 0; k < c.n_streams - 1; ++k) {
+                        const int s = 1 + (c.rr_stream - 1 + k) % (c.n_streams - 1);
+                        if (c.norm_ready[s].empty()) continue;
+                        Req *r = c.norm_ready[s].front();
+                        c.norm_ready[s].pop_front();
+                        launch_whole(c, r, 0);
+                        c.crit_active.push_back(r);  // one stream carries everything
+                        c.rr_stream = 1 + s % (c.n_streams - 1);
+                        progress = true;
+                        break;
+                    }
+                }
+            }
+        } else {
+            // critical requests: unsharded, in order, on the critical stream
+            while (!c.crit_ready.empty()) {
+                Req *r = c.crit_ready.front();
+                c.crit_ready.erase(c.crit_ready.begin());
+                launch_whole(c, r, 0);
+                c.crit_active.push_back(r);
+                progress = true;
+            }
+            for (int s = 1; s < c.n_streams; ++s) {
+                if (c.cfg.policy == MIRIAM_POLICY_MULTISTREAM) {
+                    if (c.be_active[s].empty() && !c.norm_ready[s].empty()) {
+                        Req *r = c.norm_ready[s].front();
+                        c.norm_ready[s].pop_front();
+                        launch_whole(c, r, s);
+                        c.be_active[s].push_back(r);
+                        progress = true;
+                    }
+                } else {
+                    progress |= pump_normal(c, s);
+                }
+            }
+        }
+
+        if (!progress) {
+            bool idle = all_idle(c);
+            for (int s = 1; s < c.n_streams && idle; ++s) idle = c.norm_ready[s].empty();
+            idle = idle && c.crit_ready.empty();
+            if (idle) {
+                // nothing on the GPU: sleep until a submission or the next timed release
+                std::unique_lock<std::mutex> lk(c.mu);
+                if (c.inbox.empty() && !(c.stopping && c.outstanding == 0)) {
+                    int64_t wait_ns = 2000000;
+                    if (!c.timed.empty()) wait_ns = std::min<int64_t>(wait_ns, c.timed.top()->release - mono_ns());
+                    if (wait_ns > 50000) c.cv.wait_for(lk, std::chrono::nanoseconds(wait_ns - 50000));
+                }
+            } else {
+                std::this_thread::yield();
+            }
+        }
+    }
+}
+
+int estate(const char *m) {
+    set_error(m);
+    return MIRIAM_ESTATE;
+}
+
+// a9 + Eq. (5) inputs: time each op unsharded and as one persistent shard per block.
+void profile_task(Coord &c, miriam_task *t) {
+    const int reps = c.cfg.profile_reps > 0 ? c.cfg.profile_reps : 0;
+    if (!c.t_launch_measured && !t->ops.empty() && (reps > 0 || c.cfg.backend == MIRIAM_BACKEND_FAKE)) {
+        const double g = c.be->launch_gap_us(t->ops[0], std::max(1, reps));
+        if (g > 0.0) c.t_launch_us = g;
+        c.t_launch_measured = true;
+    }
+    for (size_t i = 0; i < t->ops.size(); ++i) {
+        const miriam_op *op = t->ops[i];
+        OpProf &p = t->prof[i];
+        for (int k = 0; k < 3; ++k) {
+            p.cap[k] = op->max_wg_per_cu[k] > 0 ? op->max_wg_per_cu[k] : 1;
+            if (c.cfg.backend == MIRIAM_BACKEND_FAKE) p.cap[k] = static_cast<FakeBackend *>(c.be)->slots;
+        }
+        if (reps == 0 && c.cfg.backend == MIRIAM_BACKEND_HIP) {
+            p.n_max = 1;
+            continue;
+        }
+        const int greps = std::max(1, reps);
+        p.t_unsh_us = c.be->time_us(op, 0, op->T, (int)std::min<int64_t>(op->T, INT32_MAX), 256, greps);
+        for (int k = 0; k < 3; ++k) {
+            const int64_t gp = std::min<int64_t>(op->T, (int64_t)c.n_cu * p.cap[k]);
+            p.t_pers_us[k] = c.be->time_us(op, 0, op->T, (int)gp, 64 << k, greps);
+            const int64_t iters = (op->T + gp - 1) / gp;
+            p.tau1_us[k] = p.t_pers_us[k] > 0.0 ? p.t_pers_us[k] / (double)iters : 0.0;
+            p.ok_pt[k] = p.t_unsh_us > 0.0 && (p.t_pers_us[k] - p.t_unsh_us) < c.cfg.max_pt_frac * p.t_unsh_us;
+        }
+        if (!p.ok_pt[0] && !p.ok_pt[1] && !p.ok_pt[2]) p.ok_pt[2] = true;  // keep the full block usable
+        // (n - 1) * t_launch < MAX_blk = max_blk_frac * t_unsharded
+        const double budget = c.cfg.max_blk_frac * std::max(0.0, p.t_unsh_us);
+        p.n_max = 1 + (int64_t)std::floor(budget / std::max(1e-3, c.t_launch_us));
+        p.n_max = std::max<int64_t>(1, std::min<int64_t>(p.n_max, op->T));
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t miriam_now_ns(void) { return mono_ns(); }
+
+int miriam_init(const miriam_config *cfg) {
+    std::lock_guard<std::mutex> life(g_life);
+    if (g) return estate("already initialised");
+    if (!cfg) {
+        set_error("null config");
+        return MIRIAM_EINVAL;
+    }
+    if (cfg->policy < 0 || cfg->policy > 2 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
+        cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
+        !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0) {
+        set_error("invalid coordinator configuration");
+        return MIRIAM_EINVAL;
+    }
+    Coord *c = new (std::nothrow) Coord();
+    if (!c) {
+        set_error("out of host memory");
+        return MIRIAM_ENOMEM;
+    }
+    c->cfg = *cfg;
+    c->n_streams = 1 + cfg->n_be_streams;
+    if (cfg->backend == MIRIAM_BACKEND_HIP) {
+        miriam_device_desc dd;
+        int rc = miriam_device_query(&dd);
+        if (rc != MIRIAM_OK) {
+            delete c;
+            return rc;
+        }
+        c->n_cu = dd.n_cu;
+        c->l_threads = dd.max_threads_per_cu;
+        c->be = new HipBackend();
+    } else {
+        FakeBackend *f = new FakeBackend();
+        f->n_cu = cfg->fake_n_cu > 0 ? cfg->fake_n_cu : 8;
+        f->slots = cfg->fake_slots_per_cu > 0 ? cfg->fake_slots_per_cu : 2;
+        f->tile_ns = cfg->fake_tile_ns > 0 ? cfg->fake_tile_ns : 1000.0;
+        f->launch_ns = cfg->fake_launch_ns >= 0 ? cfg->fake_launch_ns : 2000.0;
+        c->n_cu = f->n_cu;
+        c->l_threads = 2048;
+        c->be = f;
+    }
+    int rc = c->be->start(c->n_streams);
+    if (rc != MIRIAM_OK) {
+        c->be->stop();
+        delete c->be;
+        delete c;
+        return rc;
+    }
+    c->norm_ready.resize(c->n_streams);
+    c->be_active.resize(c->n_streams);
+    c->inflight.assign(c->n_streams, 0);
+    g = c;
+    c->th = std::thread(dispatcher, c);
+    return MIRIAM_OK;
+}
+
+int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out) {
+    if (!ops || n_ops < 1 || !out) {
+        set_error("task needs at least one op");
+        return MIRIAM_EINVAL;
+    }
+    for (int i = 0; i < n_ops; ++i)
+        if (!ops[i]) {
+            set_error("null op in task");
+            return MIRIAM_EINVAL;
+        }
+    std::lock_guard<std::mutex> life(g_life);
+    if (!g) return estate("coordinator not initialised");
+    miriam_task *t = new (std::nothrow) miriam_task();
+    if (!t) {
+        set_error("out of host memory");
+        return MIRIAM_ENOMEM;
+    }
+    t->ops.assign(ops, ops + n_ops);
+    t->prof.resize(n_ops);
+    t->id = g->next_task_id++;
+    profile_task(*g, t);
+    *out = t;
+    return MIRIAM_OK;
+}
+
+int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_t deadline_ns,
+                  uint64_t *ticket_out) {
+    if (!task || (criticality != 0 && criticality != 1) || release_ns < 0 || deadline_ns < 0) {
+        set_error("bad submit arguments");
+        return MIRIAM_EINVAL;
+    }
+    std::lock_guard<std::mutex> life(g_life);
+    if (!g) return estate("coordinator not initialised");
+    Req *r = new (std::nothrow) Req();
+    if (!r) {
+        set_error("out of host memory");
+        return MIRIAM_ENOMEM;
+    }
+    r->task = task;
+    r->crit = criticality;
+    r->release = release_ns > 0 ? release_ns : mono_ns();
+    r->deadline = deadline_ns;
+    r->stream = criticality ? 0 : 1 + task->id % (g->n_streams - 1);
+    task->pending.fetch_add(1);
+    for (miriam_op *op : task->ops) op->pending.fetch_add(1);
+    {
+        std::lock_guard<std::mutex> lk(g->mu);
+        if (g->stopping) {
+            task->pending.fetch_sub(1);
+            for (miriam_op *op : task->ops) op->pending.fetch_sub(1);
+            delete r;
+            return estate("coordinator is shutting down");
+        }
+        r->ticket = g->next_ticket++;
+        g->inbox.push_back(r);
+        g->outstanding++;
+    }
+    g->cv.notify_one();
+    if (ticket_out) *ticket_out = r->ticket;
+    return MIRIAM_OK;
+}
+
+int miriam_poll(miriam_completion *out, int max_out) {
+    if (!out || max_out < 0) {
+        set_error("bad poll arguments");
+        return MIRIAM_EINVAL;
+    }
+    Coord *c = g;
+    if (!c) return estate("coordinator not initialised");
+    std::lock_guard<std::mutex> lk(c->mu);
+    int n = 0;
+    while (n < max_out && !c->outbox.empty()) {
+        out[n++] = c->outbox.front();
+        c->outbox.pop_front();
+    }
+    return n;
+}
+
+int miriam_drain(int64_t timeout_ms) {
+    Coord *c = g;
+    if (!c) return estate("coordinator not initialised");
+    std::unique_lock<std::mutex> lk(c->mu);
+    const bool ok = c->cv_done.wait_for(lk, std::chrono::milliseconds(timeout_ms < 0 ? 0 : timeout_ms),
+                                        [c] { return c->outstanding == 0; });
+    if (!ok) {
+        set_error("requests still in flight");
+        return MIRIAM_EBUSY;
+    }
+    return MIRIAM_OK;
+}
+
+int miriam_stats_get(miriam_stats *out) {
+    if (!out) {
+        set_error("null output");
+        return MIRIAM_EINVAL;
+    }
+    Coord *c = g;
+    if (!c) return estate("coordinator not initialised");
+    std::lock_guard<std::mutex> lk(c->stat_mu);
+    *out = c->stats;
+    return MIRIAM_OK;
+}
+
+int miriam_launch_log(miriam_launch_record *out, int max_out) {
+    if (!out || max_out < 0) {
+        set_error("bad arguments");
+        return MIRIAM_EINVAL;
+    }
+    Coord *c = g;
+    if (!c) return estate("coordinator not initialised");
+    std::lock_guard<std::mutex> lk(c->log_mu);
+    int n = 0;
+    while (n < max_out && c->log_read < c->log.size()) out[n++] = c->log[c->log_read++];
+    if (c->log_read == c->log.size()) {
+        c->log.clear();
+        c->log_read = 0;
+    }
+    return n;
+}
+
+int miriam_task_destroy(miriam_task *t) {
+    if (!t) {
+        set_error("null task");
+        return MIRIAM_EINVAL;
+    }
+    if (t->pending.load() > 0) {
+        set_error("task has pending requests");
+        return MIRIAM_EBUSY;
+    }
+    delete t;
+    return MIRIAM_OK;
+}
+
+int miriam_shutdown(void) {
+    std::lock_guard<std::mutex> life(g_life);
+    Coord *c = g;
+    if (!c) return estate("coordinator not initialised");
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->stopping = true;
+    }
+    c->cv.notify_one();
+    c->th.join();
+    c->be->stop();
+    delete c->be;
+    g = nullptr;
+    delete c;
+    return MIRIAM_OK;
+}
+
+}  // extern "C"

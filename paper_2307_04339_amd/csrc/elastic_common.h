@@ -1,0 +1,112 @@
+// Device-side building blocks shared by every elastic kernel of the library.
+//
+// Elastic grid (§6.2) + persistent threads (§6.1): a launch covers the shard
+// [begin, begin+len) of an operator's logical tile space.  Physical workgroup g
+// of G takes logical rank r(g) (workgroups on one die get consecutive ranks, so
+// tiles that share operands share that die's L2) and runs tiles
+//     t = begin + r(g) + i*G,   i = 0, 1, ...   while t < begin + len.
+// Elastic block (§6.1, N:1 logical-to-physical map): the logical block is
+// always 4 waves (256 threads); a physical block of P = blockDim/64 waves runs
+// logical wave lambda on physical wave lambda mod P, in slot lambda div P.
+// No arithmetic depends on (begin, len, G, P): each output element sees the
+// same instruction sequence, so every elastic configuration is bit-identical.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kargs.h"
+
+namespace miriam {
+
+typedef _Float16 half_t;
+typedef __bf16 bf16_t;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2, ACT_GELU = 3 };
+enum EpiFlag { EPI_BIAS = 1, EPI_BN = 2, EPI_RES = 4 };
+
+// Logical rank of physical workgroup g among G, dies dealt round-robin.
+__device__ __forceinline__ int64_t wg_rank(int64_t g, int64_t G) {
+    const int64_t q = G / kDies, r = G % kDies;
+    const int64_t x = g % kDies, s = g / kDies;
+    return x * q + (x < r ? x : r) + s;
+}
+
+__device__ __forceinline__ void trace_tile(const Shard &sh, int64_t t, int iter) {
+    if (sh.count != nullptr && threadIdx.x == 0) {
+        sh.owner_wg[t] = (int32_t)blockIdx.x;
+        sh.owner_iter[t] = iter;
+        atomicAdd(&sh.count[t], 1);
+    }
+}
+
+// ---------------------------------------------------------------- types
+template <class T> struct TypeOps;
+template <> struct TypeOps<float> {
+    static __device__ __forceinline__ float to_f(float v) { return v; }
+    static __device__ __forceinline__ float from_f(float v) { return v; }
+};
+template <> struct TypeOps<half_t> {
+    static __device__ __forceinline__ float to_f(half_t v) { return (float)v; }
+    static __device__ __forceinline__ half_t from_f(float v) { return (half_t)v; }
+};
+template <> struct TypeOps<bf16_t> {
+    static __device__ __forceinline__ float to_f(bf16_t v) { return (float)v; }
+    static __device__ __forceinline__ bf16_t from_f(float v) { return (bf16_t)v; }
+};
+
+template <class T> __device__ __forceinline__ float ld_f(const T *p) { return TypeOps<T>::to_f(*p); }
+template <class T> __device__ __forceinline__ void st_f(T *p, float v) { *p = TypeOps<T>::from_f(v); }
+
+// 16-byte vector of T: 4 floats or 8 16-bit values.
+template <class T> struct Vec16 {
+    static constexpr int N = 16 / (int)sizeof(T);
+    union { u32x4 u; T e[16 / sizeof(T)]; };
+};
+
+template <class T> __device__ __forceinline__ Vec16<T> ld_vec(const T *p) {
+    Vec16<T> v;
+    v.u = *reinterpret_cast<const u32x4 *>(p);
+    return v;
+}
+template <class T> __device__ __forceinline__ void st_vec(T *p, const Vec16<T> &v) {
+    *reinterpret_cast<u32x4 *>(p) = v.u;
+}
+template <class T> __device__ __forceinline__ Vec16<T> zero_vec() {
+    Vec16<T> v;
+    v.u = u32x4{0u, 0u, 0u, 0u};
+    return v;
+}
+
+// ------------------------------------------------------------- epilogue
+__device__ __forceinline__ float gelu_erf(float v) {
+    return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
+}
+
+__device__ __forceinline__ float apply_act(float v, int act) {
+    switch (act) {
+    case ACT_RELU: return v > 0.0f ? v : 0.0f;
+    case ACT_RELU6: return fminf(fmaxf(v, 0.0f), 6.0f);
+    case ACT_GELU: return gelu_erf(v);
+    default: return v;
+    }
+}
+
+// v = act(BN(acc + bias[c]) + res), in fp32, per element.
+__device__ __forceinline__ float epilogue_apply(const Epilogue &e, float acc, int64_t c, float res) {
+    float v = acc;
+    if (e.flags & EPI_BIAS) v += e.bias[c];
+    if (e.flags & EPI_BN) {
+        const float g = e.bn[c], b = e.bn[e.C + c], mu = e.bn[2 * e.C + c], var = e.bn[3 * e.C + c];
+        v = (v - mu) * (g / sqrtf(var + e.eps)) + b;
+    }
+    if (e.flags & EPI_RES) v += res;
+    return apply_act(v, e.act);
+}
+
+}  // namespace miriam

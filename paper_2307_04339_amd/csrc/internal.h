@@ -1,0 +1,49 @@
+// Host-side internals shared by the library's C++ translation units.
+#pragma once
+
+#include <atomic>
+#include <cstdint>
+#include <string>
+
+#include <hip/hip_runtime_api.h>
+
+#include "../../include/miriam.h"
+#include "kargs.h"
+
+namespace miriam {
+
+void set_error(const std::string &msg);
+int hip_fail(hipError_t e, const char *what);  // records the HIP error text, returns MIRIAM_EHIP
+
+enum Family { FAM_IGEMM = 0, FAM_PIX = 1, FAM_ROW = 2 };
+
+// Kernel tables (one entry per physical block of 64, 128, 256 threads).
+int igemm_kernels_f32(int cfg, int lay, const void *out[3], int *lds);
+int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds);
+int igemm_kernels_bf16(int cfg, int lay, const void *out[3], int *lds);
+int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
+int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
+
+}  // namespace miriam
+
+struct miriam_op {
+    miriam_op_desc d;
+    int family;
+    int64_t T;              // logical tiles
+    int cfg, lay;           // contraction tile config and load layout
+    int tile_m, tile_n;
+    int lds_bytes;
+    const void *kern[3];    // kernels for physical blocks 64, 128, 256
+    int max_wg_per_cu[3];
+    double flops, bytes;
+    miriam::IgemmArgs ig;
+    miriam::PixArgs px;
+    miriam::RowArgs rw;
+    std::atomic<int> pending{0};  // submitted requests that still reference the op
+};
+
+namespace miriam {
+// Launch helper used by the public entry points and by the coordinator.
+int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
+              int32_t *owner_wg, int32_t *owner_iter, int32_t *count);
+}  // namespace miriam

@@ -1,0 +1,81 @@
+// Kernel argument blocks, passed by value to the elastic kernels.  Plain structs
+// so the host runtime can fill them without device headers.
+#pragma once
+
+#include <stdint.h>
+
+namespace miriam {
+
+constexpr int kLogicalWaves = 4;   // logical block = 4 waves
+constexpr int kLogicalBlock = 256;  // threads of the logical block
+constexpr int kWave = 64;           // wavefront size of CDNA
+constexpr int kDies = 8;            // XCDs of an MI355X; workgroups are dealt to them round-robin
+
+// Shard description passed to every kernel.  The trace arrays are null except
+// in traced launches, where they record the tile -> (workgroup, iteration) map.
+struct Shard {
+    int64_t begin;
+    int64_t len;
+    int32_t *owner_wg;
+    int32_t *owner_iter;
+    int32_t *count;
+};
+
+// Fused epilogue: v = act(BN(acc + bias[c]) + residual).
+struct Epilogue {
+    const float *bias;   // [C]
+    const float *bn;     // [4*C]: gamma, beta, mean, var
+    float eps;
+    int act;
+    int flags;
+    int64_t C;           // channels (bn stride)
+};
+
+// Contraction (convolution / GEMM / batched GEMM).
+struct IgemmArgs {
+    const void *x;
+    const void *w;
+    void *y;
+    const void *res;
+    int64_t H, W, C, ldx;  // input image and its pixel (row) stride in elements
+    int64_t Ho, Wo;        // output image
+    int32_t KH, KW, stride, pad;
+    int64_t M, Nc, K;      // GEMM sizes per batch entry
+    int64_t ldw, ldy;      // B row stride, output row stride
+    int64_t mT, nT;        // tiles along m and n
+    int64_t bdiv, sx0, sx1, sw0, sw1, sy0, sy1;  // batch offsets
+    int64_t img_x;         // elements between images of x
+    Epilogue epi;
+};
+
+// Channel-vector kernels (depthwise, pooling, standalone epilogue).
+struct PixArgs {
+    const void *x;
+    const void *w;     // depthwise weights [KH][KW][C]
+    void *y;
+    const void *res;   // same layout as y
+    int64_t N, H, W, C, Ho, Wo;
+    int32_t KH, KW, stride, pad;
+    int64_t items;     // lane items: N*Ho*Wo*(C/V)
+    Epilogue epi;
+};
+
+// Row kernels (softmax, layer normalisation).
+struct RowArgs {
+    const void *x;
+    const void *res;    // LAYERNORM residual (added before normalising)
+    const float *gamma; // LAYERNORM
+    const float *beta;
+    void *y;
+    int64_t rows, n, ldx, ldy;
+    float scale;        // SOFTMAX
+    float eps;          // LAYERNORM
+    int has_res;
+};
+
+enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3 };
+enum RowKind { ROW_SOFTMAX = 0, ROW_LAYERNORM = 1 };
+enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3 };
+enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3 };
+
+}  // namespace miriam

@@ -1,0 +1,404 @@
+// Operator registry of the elastic-kernel library: validation of operator
+// descriptors, tile-space construction, kernel selection, and the elastic launch
+// entry points (§6.1 elastic block, §6.2 elastic grid, §6.4 computation-based
+// index functions).
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "internal.h"
+
+namespace miriam {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string &msg) { g_last_error = msg; }
+
+int hip_fail(hipError_t e, const char *what) {
+    set_error(std::string(what) + ": " + hipGetErrorString(e));
+    return MIRIAM_EHIP;
+}
+
+static int einval(const char *msg) {
+    set_error(msg);
+    return MIRIAM_EINVAL;
+}
+
+static int esize(int dtype) { return dtype == MIRIAM_F32 ? 4 : 2; }
+static int vec_elems(int dtype) { return 16 / esize(dtype); }
+static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+static int get_igemm_table(int dtype, int cfg, int lay, const void *out[3], int *lds) {
+    switch (dtype) {
+    case MIRIAM_F32: return igemm_kernels_f32(cfg, lay, out, lds);
+    case MIRIAM_F16: return igemm_kernels_f16(cfg, lay, out, lds);
+    case MIRIAM_BF16: return igemm_kernels_bf16(cfg, lay, out, lds);
+    default: return -1;
+    }
+}
+
+static int tile_dim(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : 128); }
+
+// Fill the per-physical-block residency of the op's kernels.  Without a device
+// the figures stay 0 ("unknown"); the error state of the runtime is cleared.
+static void query_occupancy(miriam_op *op) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return;
+    }
+    for (int i = 0; i < 3; ++i) {
+        int n = 0;
+        const int block = 64 << i;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, op->kern[i], block, 0) == hipSuccess)
+            op->max_wg_per_cu[i] = n;
+        else
+            (void)hipGetLastError();
+    }
+}
+
+static Epilogue make_epi(const miriam_op_desc &d, int64_t C) {
+    Epilogue e;
+    e.bias = static_cast<const float *>(d.bias);
+    e.bn = static_cast<const float *>(d.bn);
+    e.eps = d.eps;
+    e.act = d.act;
+    e.flags = d.flags;
+    e.C = C;
+    return e;
+}
+
+static int check_epi(const miriam_op_desc &d) {
+    if (d.act < MIRIAM_ACT_NONE || d.act > MIRIAM_ACT_GELU) return einval("unknown activation");
+    if (d.flags & ~(MIRIAM_EPI_BIAS | MIRIAM_EPI_BN | MIRIAM_EPI_RESIDUAL)) return einval("unknown epilogue flag");
+    if ((d.flags & MIRIAM_EPI_BIAS) && !d.bias) return einval("bias flag without bias pointer");
+    if ((d.flags & MIRIAM_EPI_BN) && !d.bn) return einval("bn flag without bn pointer");
+    if ((d.flags & MIRIAM_EPI_RESIDUAL) && !d.residual) return einval("residual flag without residual pointer");
+    if ((d.flags & MIRIAM_EPI_BN) && !(d.eps >= 0.0f)) return einval("negative eps");
+    return MIRIAM_OK;
+}
+
+// Contraction tile choice: the largest tile that still gives at least one tile
+// per compute unit; small problems fall back to 32x32 tiles.
+static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
+    const int64_t want = 256;
+    if (batch * cdiv(M, 128) * cdiv(N, 128) >= want) return CFG_128;
+    if (batch * cdiv(M, 64) * cdiv(N, 64) >= want) return CFG_64;
+    return CFG_32;
+}
+
+static int create_igemm(miriam_op *op) {
+    const miriam_op_desc &d = op->d;
+    IgemmArgs &a = op->ig;
+    std::memset(&a, 0, sizeof(a));
+    const int es = esize(d.dtype), V = vec_elems(d.dtype);
+    int64_t batch = 1;
+    bool a_vec = true, b_vec = true;
+    const bool nmaj = d.kind == MIRIAM_OP_BGEMM && d.b_nmajor;
+    if (d.kind == MIRIAM_OP_CONV2D) {
+        if (d.n < 1 || d.h < 1 || d.w < 1 || d.c < 1 || d.k < 1 || d.kh < 1 || d.kw < 1)
+            return einval("conv2d: sizes must be >= 1");
+        if (d.stride < 1 || d.pad < 0) return einval("conv2d: stride >= 1 and pad >= 0 required");
+        if (d.groups != 0 && d.groups != 1) return einval("conv2d: groups must be 1 (use DWCONV for depthwise)");
+        a.H = d.h; a.W = d.w; a.C = d.c;
+        a.ldx = d.ldx > 0 ? d.ldx : d.c;
+        if (a.ldx < d.c) return einval("conv2d: ldx < c");
+        a.KH = (int32_t)d.kh; a.KW = (int32_t)d.kw; a.stride = (int32_t)d.stride; a.pad = (int32_t)d.pad;
+        a.Ho = (d.h + 2 * d.pad - d.kh) / d.stride + 1;
+        a.Wo = (d.w + 2 * d.pad - d.kw) / d.stride + 1;
+        if (d.h + 2 * d.pad < d.kh || d.w + 2 * d.pad < d.kw || a.Ho < 1 || a.Wo < 1)
+            return einval("conv2d: kernel larger than padded input");
+        a.M = d.n * a.Ho * a.Wo;
+        a.Nc = d.k;
+        a.K = d.kh * d.kw * d.c;
+        a.ldw = d.ldw > 0 ? d.ldw : a.K;
+        a.ldy = d.ldy > 0 ? d.ldy : d.k;
+        if (a.ldw < a.K || a.ldy < d.k) return einval("conv2d: row stride too small");
+        a.img_x = d.h * d.w * a.ldx;
+        a.bdiv = 1;
+        a_vec = (d.c % V == 0) && (a.ldx % V == 0) && aligned16(d.x);
+    } else {
+        if (d.m < 1 || d.nn < 1 || d.kk < 1) return einval("gemm: m, nn, kk must be >= 1");
+        a.H = 1; a.W = 1; a.C = d.kk; a.Ho = 1; a.Wo = 1;
+        a.KH = 1; a.KW = 1; a.stride = 1; a.pad = 0;
+        a.M = d.m; a.Nc = d.nn; a.K = d.kk;
+        a.ldx = d.ldx > 0 ? d.ldx : d.kk;
+        a.ldw = d.ldw > 0 ? d.ldw : (nmaj ? d.nn : d.kk);
+        a.ldy = d.ldy > 0 ? d.ldy : d.nn;
+        if (a.ldx < d.kk || a.ldy < d.nn || a.ldw < (nmaj ? d.nn : d.kk)) return einval("gemm: row stride too small");
+        a.img_x = a.ldx;
+        a.bdiv = 1;
+        if (d.kind == MIRIAM_OP_BGEMM) {
+            if (d.batch < 1 || d.batch_div < 1) return einval("bgemm: batch and batch_div must be >= 1");
+            batch = d.batch;
+            a.bdiv = d.batch_div;
+            a.sx0 = d.sx0; a.sx1 = d.sx1; a.sw0 = d.sw0; a.sw1 = d.sw1; a.sy0 = d.sy0; a.sy1 = d.sy1;
+            if (a.sx0 < 0 || a.sx1 < 0 || a.sw0 < 0 || a.sw1 < 0 || a.sy0 < 0 || a.sy1 < 0)
+                return einval("bgemm: negative batch stride");
+        }
+        a_vec = (d.kk % V == 0) && (a.ldx % V == 0) && (a.sx0 % V == 0) && (a.sx1 % V == 0) && aligned16(d.x);
+    }
+    if (nmaj)
+        b_vec = (d.nn % V == 0) && (a.ldw % V == 0) && (a.sw0 % V == 0) && (a.sw1 % V == 0) && aligned16(d.wt);
+    else
+        b_vec = (a.K % V == 0) && (a.ldw % V == 0) && (a.sw0 % V == 0) && (a.sw1 % V == 0) && aligned16(d.wt);
+    if (nmaj && d.dtype == MIRIAM_F32) return einval("bgemm: [k][n] right operand needs fp16/bf16");
+    if (d.kind == MIRIAM_OP_CONV2D && d.b_nmajor) return einval("conv2d: weights must be [Cout][KH][KW][Cin]");
+    int rc = check_epi(d);
+    if (rc) return rc;
+    a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
+    a.epi = make_epi(d, a.Nc);
+
+    int cfg = d.tile;
+    if (cfg == 0) cfg = choose_cfg(batch, a.M, a.Nc);
+    if (cfg < CFG_32 || cfg > CFG_128) return einval("unknown tile configuration");
+    const int td = tile_dim(cfg);
+    a.mT = cdiv(a.M, td);
+    a.nT = cdiv(a.Nc, td);
+    op->T = batch * a.mT * a.nT;
+    op->cfg = cfg;
+    op->tile_m = op->tile_n = td;
+    if (nmaj) op->lay = (a_vec && b_vec) ? LAY_VEC_NB : LAY_SCALAR_NB;
+    else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
+    if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
+        return einval("no kernel for this dtype / layout");
+    op->flops = 2.0 * (double)batch * (double)a.M * (double)a.Nc * (double)a.K;
+    const double xin = d.kind == MIRIAM_OP_CONV2D ? (double)d.n * d.h * d.w * d.c : (double)batch * a.M * a.K;
+    const double win = (d.kind == MIRIAM_OP_BGEMM ? (double)batch : 1.0) * (double)a.Nc * a.K;
+    const double yout = (double)batch * a.M * a.Nc;
+    op->bytes = es * (xin + win + yout * ((d.flags & MIRIAM_EPI_RESIDUAL) ? 2.0 : 1.0));
+    return MIRIAM_OK;
+}
+
+static int create_pix(miriam_op *op) {
+    const miriam_op_desc &d = op->d;
+    PixArgs &a = op->px;
+    std::memset(&a, 0, sizeof(a));
+    const int es = esize(d.dtype), V = vec_elems(d.dtype);
+    int kind;
+    if (d.kind == MIRIAM_OP_BN_ACT) {
+        if (d.m < 1 || d.nn < 1) return einval("bn_act: m, nn must be >= 1");
+        kind = PIX_EW;
+        a.N = d.m; a.H = 1; a.W = 1; a.C = d.nn; a.Ho = 1; a.Wo = 1;
+        a.KH = 1; a.KW = 1; a.stride = 1; a.pad = 0;
+    } else {
+        if (d.n < 1 || d.h < 1 || d.w < 1 || d.c < 1 || d.kh < 1 || d.kw < 1)
+            return einval("pixel op: sizes must be >= 1");
+        if (d.stride < 1 || d.pad < 0) return einval("pixel op: stride >= 1 and pad >= 0 required");
+        if (d.h + 2 * d.pad < d.kh || d.w + 2 * d.pad < d.kw) return einval("pixel op: window larger than padded input");
+        if (d.pad >= d.kh || d.pad >= d.kw) return einval("pixel op: pad must be smaller than the window");
+        kind = d.kind == MIRIAM_OP_DWCONV ? PIX_DW : (d.kind == MIRIAM_OP_POOL_MAX ? PIX_MAX : PIX_AVG);
+        if (kind == PIX_DW && d.k != 0 && d.k != d.c) return einval("dwconv: k must equal c");
+        if (kind == PIX_DW && d.groups != 0 && d.groups != d.c) return einval("dwconv: groups must equal c");
+        a.N = d.n; a.H = d.h; a.W = d.w; a.C = d.c;
+        a.KH = (int32_t)d.kh; a.KW = (int32_t)d.kw; a.stride = (int32_t)d.stride; a.pad = (int32_t)d.pad;
+        a.Ho = (d.h + 2 * d.pad - d.kh) / d.stride + 1;
+        a.Wo = (d.w + 2 * d.pad - d.kw) / d.stride + 1;
+        if (kind != PIX_DW && (d.flags != 0 || d.act != 0)) return einval("pooling has no epilogue");
+    }
+    if (d.ldx != 0 || d.ldy != 0) return einval("pixel op: dense layouts only");
+    int rc = check_epi(d);
+    if (rc) return rc;
+    const bool vec = (a.C % V == 0) && aligned16(d.x) && aligned16(d.y) &&
+                     (kind != PIX_DW || aligned16(d.wt)) &&
+                     (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
+    const int v = vec ? V : 1;
+    a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
+    a.epi = make_epi(d, a.C);
+    a.items = a.N * a.Ho * a.Wo * (a.C / v);
+    op->T = cdiv(a.items, 256);
+    op->lds_bytes = 0;
+    if (pix_kernels(d.dtype, kind, vec, op->kern) != 0) return einval("no kernel for this dtype");
+    const double outs = (double)a.N * a.Ho * a.Wo * a.C;
+    const double ins = kind == PIX_EW ? outs : (double)a.N * a.H * a.W * a.C;
+    op->flops = kind == PIX_EW ? 4.0 * outs : (kind == PIX_DW ? 2.0 : 1.0) * outs * a.KH * a.KW;
+    op->bytes = es * (ins + outs + (kind == PIX_DW ? (double)a.KH * a.KW * a.C : 0.0) +
+                      ((d.flags & MIRIAM_EPI_RESIDUAL) ? outs : 0.0));
+    return MIRIAM_OK;
+}
+
+static int create_row(miriam_op *op) {
+    const miriam_op_desc &d = op->d;
+    RowArgs &a = op->rw;
+    std::memset(&a, 0, sizeof(a));
+    const int es = esize(d.dtype), V = vec_elems(d.dtype);
+    if (d.m < 1 || d.nn < 1) return einval("row op: m, nn must be >= 1");
+    a.rows = d.m; a.n = d.nn;
+    a.ldx = d.ldx > 0 ? d.ldx : d.nn;
+    a.ldy = d.ldy > 0 ? d.ldy : d.nn;
+    if (a.ldx < d.nn || a.ldy < d.nn) return einval("row op: row stride too small");
+    const int kind = d.kind == MIRIAM_OP_SOFTMAX ? ROW_SOFTMAX : ROW_LAYERNORM;
+    if (kind == ROW_LAYERNORM) {
+        if (!d.wt || !d.bias) return einval("layernorm: gamma (w) and beta (bias) required");
+        if (!(d.eps >= 0.0f)) return einval("layernorm: negative eps");
+        a.has_res = (d.flags & MIRIAM_EPI_RESIDUAL) ? 1 : 0;
+        if (a.has_res && !d.residual) return einval("layernorm: residual flag without pointer");
+        if (d.flags & ~MIRIAM_EPI_RESIDUAL) return einval("layernorm: only the residual flag applies");
+    } else if (d.flags != 0) {
+        return einval("softmax has no epilogue");
+    }
+    if (d.act != 0) return einval("row ops take no activation");
+    a.x = d.x; a.res = d.residual; a.y = d.y;
+    a.gamma = static_cast<const float *>(d.wt);
+    a.beta = static_cast<const float *>(d.bias);
+    a.scale = kind == ROW_SOFTMAX ? (d.scale == 0.0f ? 1.0f : d.scale) : 1.0f;
+    a.eps = d.eps;
+    const bool vec = (d.nn % V == 0) && (a.ldx % V == 0) && (a.ldy % V == 0) && aligned16(d.x) &&
+                     aligned16(d.y) && (!a.has_res || aligned16(d.residual));
+    op->T = cdiv(a.rows, 4);
+    op->lds_bytes = 0;
+    if (row_kernels(d.dtype, kind, vec, op->kern) != 0) return einval("no kernel for this dtype");
+    const double n = (double)a.rows * a.n;
+    op->flops = 5.0 * n;
+    op->bytes = es * (n * 2.0 + (a.has_res ? n : 0.0)) + (kind == ROW_LAYERNORM ? 8.0 * a.n : 0.0);
+    return MIRIAM_OK;
+}
+
+int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
+              int32_t *owner_wg, int32_t *owner_iter, int32_t *count) {
+    if (!op) return einval("null op");
+    if (b < 0 || l < 1 || b + l > op->T || b + l < b) {
+        set_error("shard outside the tile space");
+        return MIRIAM_ERANGE;
+    }
+    if (grid < 1) {
+        set_error("grid must be >= 1");
+        return MIRIAM_ERANGE;
+    }
+    int pi;
+    switch (block) {
+    case 64: pi = 0; break;
+    case 128: pi = 1; break;
+    case 256: pi = 2; break;
+    default: set_error("block must be 64, 128 or 256"); return MIRIAM_ERANGE;
+    }
+    Shard sh{b, l, owner_wg, owner_iter, count};
+    void *args[2];
+    switch (op->family) {
+    case FAM_IGEMM: args[0] = const_cast<IgemmArgs *>(&op->ig); break;
+    case FAM_PIX: args[0] = const_cast<PixArgs *>(&op->px); break;
+    default: args[0] = const_cast<RowArgs *>(&op->rw); break;
+    }
+    args[1] = &sh;
+    hipError_t e = hipLaunchKernel(op->kern[pi], dim3(grid), dim3(block), args, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return MIRIAM_OK;
+}
+
+}  // namespace miriam
+
+using namespace miriam;
+
+extern "C" {
+
+const char *miriam_last_error(void) { return g_last_error.c_str(); }
+
+int miriam_device_query(miriam_device_desc *out) {
+    if (!out) return einval("null output");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    hipDeviceProp_t p;
+    e = hipGetDeviceProperties(&p, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    std::memset(out, 0, sizeof(*out));
+    out->n_cu = p.multiProcessorCount;
+    out->max_threads_per_cu = p.maxThreadsPerMultiProcessor;
+    out->lds_per_cu = (int32_t)p.maxSharedMemoryPerMultiProcessor;
+    out->n_xcd = kDies;
+    out->wave_size = p.warpSize;
+    out->clock_khz = p.clockRate;
+    std::snprintf(out->arch, sizeof(out->arch), "%s", p.gcnArchName);
+    return MIRIAM_OK;
+}
+
+int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
+    if (!d || !out) return einval("null argument");
+    *out = nullptr;
+    if (d->dtype < MIRIAM_F32 || d->dtype > MIRIAM_BF16) return einval("unknown dtype");
+    if (!d->x || !d->y) return einval("x and y are required");
+    miriam_op *op = new (std::nothrow) miriam_op();
+    if (!op) {
+        set_error("out of host memory");
+        return MIRIAM_ENOMEM;
+    }
+    op->d = *d;
+    int rc;
+    switch (d->kind) {
+    case MIRIAM_OP_CONV2D:
+    case MIRIAM_OP_GEMM:
+    case MIRIAM_OP_BGEMM:
+        if (!d->wt) { rc = einval("weights required"); break; }
+        op->family = FAM_IGEMM;
+        rc = create_igemm(op);
+        break;
+    case MIRIAM_OP_DWCONV:
+        if (!d->wt) { rc = einval("weights required"); break; }
+        op->family = FAM_PIX;
+        rc = create_pix(op);
+        break;
+    case MIRIAM_OP_POOL_MAX:
+    case MIRIAM_OP_POOL_AVG:
+    case MIRIAM_OP_BN_ACT:
+        op->family = FAM_PIX;
+        rc = create_pix(op);
+        break;
+    case MIRIAM_OP_SOFTMAX:
+    case MIRIAM_OP_LAYERNORM:
+        op->family = FAM_ROW;
+        rc = create_row(op);
+        break;
+    default:
+        rc = einval("unknown op kind");
+    }
+    if (rc != MIRIAM_OK) {
+        delete op;
+        return rc;
+    }
+    query_occupancy(op);
+    *out = op;
+    return MIRIAM_OK;
+}
+
+int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
+    if (!op || !out) return einval("null argument");
+    std::memset(out, 0, sizeof(*out));
+    out->num_tiles = op->T;
+    out->logical_block = kLogicalBlock;
+    out->lds_bytes = op->lds_bytes;
+    out->tile_m = op->family == FAM_IGEMM ? op->tile_m : 0;
+    out->tile_n = op->family == FAM_IGEMM ? op->tile_n : 0;
+    for (int i = 0; i < 3; ++i) out->max_wg_per_cu[i] = op->max_wg_per_cu[i];
+    out->flops = op->flops;
+    out->bytes = op->bytes;
+    return MIRIAM_OK;
+}
+
+int miriam_elastic_launch(const miriam_op *op, int64_t shard_begin, int64_t shard_len, int grid, int block,
+                          void *stream) {
+    return op_launch(op, shard_begin, shard_len, grid, block, static_cast<hipStream_t>(stream), nullptr,
+                     nullptr, nullptr);
+}
+
+int miriam_elastic_launch_traced(const miriam_op *op, int64_t shard_begin, int64_t shard_len, int grid,
+                                 int block, void *stream, int32_t *owner_wg, int32_t *owner_iter,
+                                 int32_t *count) {
+    if (!owner_wg || !owner_iter || !count) return einval("trace arrays required");
+    return op_launch(op, shard_begin, shard_len, grid, block, static_cast<hipStream_t>(stream), owner_wg,
+                     owner_iter, count);
+}
+
+int miriam_op_destroy(miriam_op *op) {
+    if (!op) return einval("null op");
+    if (op->pending.load() > 0) {
+        set_error("op referenced by a pending request");
+        return MIRIAM_EBUSY;
+    }
+    delete op;
+    return MIRIAM_OK;
+}
+
+}  // extern "C"

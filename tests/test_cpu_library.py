@@ -1,0 +1,175 @@
+"""Host-side checks of libmiriam.so (no GPU needed): the library loads and exports
+every entry point declared in include/miriam.h, the planner matches the oracle,
+and operator descriptors are validated before anything could be launched."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2307_04339_amd import _lib as L
+    return L.load()
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if not fn.endswith(".h"):
+            continue
+        src = open(os.path.join(ROOT, "include", fn)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_ ]*[\s\*]+(miriam_[a-z0-9_]+)\s*\(",
+                             src, flags=re.M):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for must in ["miriam_elastic_launch", "miriam_submit", "miriam_poll", "miriam_op_create",
+                 "miriam_init", "miriam_shutdown", "miriam_plan_dichotomy"]:
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    from paper_2307_04339_amd import _lib as L
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert missing == []
+    # and the binding covers them all
+    assert sorted(set(_declared_functions()) - set(L.SIGNATURES)) == []
+
+
+# ------------------------------------------------------------ planner vs oracle
+def test_dichotomy_matches_oracle(lib, orc):
+    out = (ctypes.c_int64 * 64)()
+    for M in list(range(1, 300)) + [1568, 3136, 6272, 401408]:
+        n = lib.miriam_plan_dichotomy(M, out, 64)
+        assert list(out[:n]) == orc.dichotomy(M)
+    assert lib.miriam_plan_dichotomy(0, out, 64) < 0
+
+
+def test_split_matches_oracle(lib, orc):
+    for T in list(range(1, 60)) + [196, 3136, 10**12 + 7]:
+        for n in sorted({1, 2, 3, 4, 7, 8, 16, min(T, 64)}):
+            if n > T:
+                continue
+            b = (ctypes.c_int64 * n)()
+            l = (ctypes.c_int64 * n)()
+            assert lib.miriam_plan_split(T, n, b, l) == 0
+            if T < 10**6:
+                assert list(zip(b, l)) == orc.balanced_split(T, n)
+            else:  # large T: the partition property (the oracle's product j*T would overflow)
+                assert b[0] == 0 and b[n - 1] + l[n - 1] == T
+                assert all(b[j] + l[j] == b[j + 1] for j in range(n - 1))
+
+
+def test_wg_rank_matches_oracle(lib, orc):
+    for G in list(range(1, 50)) + [255, 256, 257, 1000]:
+        for g in range(G):
+            assert lib.miriam_plan_wg_rank(g, G, 8) == orc.wg_rank(g, G, 8)
+
+
+def test_eq2_wiscore_oscore_match_oracle(lib, orc):
+    for n_sm in [8, 30, 256]:
+        for n_rt in [0, 1, 49, 255, 256, 300]:
+            assert lib.miriam_plan_eq2_grid_limit(n_sm, n_rt) == orc.eq2_grid_limit(n_sm, n_rt)
+            for s_rt in [64, 256]:
+                assert lib.miriam_plan_eq2_block_limit(2048, s_rt) == orc.eq2_block_limit(2048, s_rt)
+                for n_be in [1, 7, 64]:
+                    for s_be in [64, 128, 256]:
+                        assert lib.miriam_plan_wiscore(n_sm, 2048, n_rt, s_rt, n_be, s_be) == \
+                            orc.wiscore(n_sm, 2048, n_rt, s_rt, n_be, s_be)
+    for lo_b, lo_p, mb, mp in [([1, 2], [0.5, 0.5], 4.0, 2.0), ([1, 3], [0.5, 0.5], 4.0, 2.0),
+                               ([1, 2], [1.0, 1.5], 4.0, 2.0)]:
+        a = np.array(lo_b, dtype=np.float64)
+        b = np.array(lo_p, dtype=np.float64)
+        got = lib.miriam_plan_oscore(len(a), a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                     b.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), mb, mp)
+        assert got == orc.oscore(lo_b, lo_p, mb, mp)
+
+
+def test_top_fraction_matches_oracle(lib, orc):
+    rng = np.random.default_rng(3)
+    for n in [1, 3, 5, 10, 11, 40]:
+        sc = rng.choice([0.0, 0.5, 1.0], n).astype(np.float64)
+        gr = rng.choice([8, 64, 256], n).astype(np.int64)
+        bl = rng.choice([64, 128, 256], n).astype(np.int64)
+        keep = (ctypes.c_int * n)()
+        k = lib.miriam_plan_top_fraction(n, sc.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                         gr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                         bl.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0.2, keep)
+        assert list(keep[:k]) == orc.top_fraction(sc, gr, bl, 0.2)
+
+
+def test_tree_head_matches_oracle(lib, orc):
+    d = ctypes.c_int()
+    for T in [1, 2, 3, 7, 12, 49, 64, 100, 196]:
+        for L_ in [1, 2, 3, 5, 16, T]:
+            cur = 0
+            while cur < T:
+                ln = lib.miriam_plan_tree_head(T, cur, L_, ctypes.byref(d))
+                assert (ln, d.value) == orc.tree_head(T, cur, L_)
+                cur += ln
+
+
+# --------------------------------------------------------- descriptor checks
+def _desc(**kw):
+    from paper_2307_04339_amd import _lib as L
+    d = L.OpDesc()
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+FAKE = 0x100000  # never dereferenced: creation does not touch device memory
+
+
+def _create(lib, d):
+    h = ctypes.c_void_p()
+    rc = lib.miriam_op_create(ctypes.byref(d), ctypes.byref(h))
+    return rc, h
+
+
+def test_op_create_rejects_bad_descriptors(lib):
+    from paper_2307_04339_amd import _lib as L
+    ok = dict(kind=L.OP_CONV2D, dtype=L.F16, n=1, h=8, w=8, c=16, k=16, kh=3, kw=3, stride=1, pad=1,
+              x=FAKE, wt=FAKE, y=FAKE)
+    rc, h = _create(lib, _desc(**ok))
+    assert rc == 0
+    info = L.OpInfo()
+    assert lib.miriam_op_query(h, ctypes.byref(info)) == 0
+    assert info.num_tiles >= 1 and info.logical_block == 256
+    # launch validation happens before any device call
+    assert lib.miriam_elastic_launch(h, 0, info.num_tiles + 1, 1, 256, None) == L.ERANGE
+    assert lib.miriam_elastic_launch(h, -1, 1, 1, 256, None) == L.ERANGE
+    assert lib.miriam_elastic_launch(h, 0, 0, 1, 256, None) == L.ERANGE
+    assert lib.miriam_elastic_launch(h, 0, 1, 0, 256, None) == L.ERANGE
+    assert lib.miriam_elastic_launch(h, 0, 1, 1, 96, None) == L.ERANGE
+    assert lib.miriam_op_destroy(h) == 0
+    bad = [dict(ok, kind=99), dict(ok, dtype=7), dict(ok, x=None), dict(ok, stride=0),
+           dict(ok, kh=20, pad=0), dict(ok, groups=4), dict(ok, act=9), dict(ok, flags=1),
+           dict(ok, flags=64), dict(ok, c=0), dict(ok, tile=7)]
+    for d in bad:
+        rc, _ = _create(lib, _desc(**d))
+        assert rc == L.EINVAL, d
+    assert lib.miriam_last_error()
+
+
+@pytest.mark.parametrize("M,N,K,tile,T", [(3136, 64, 576, 1, 98 * 2), (3136, 64, 576, 2, 49),
+                                          (3136, 64, 576, 3, 25), (49, 512, 4608, 1, 2 * 16)])
+def test_gemm_tile_space(lib, M, N, K, tile, T):
+    from paper_2307_04339_amd import _lib as L
+    rc, h = _create(lib, _desc(kind=L.OP_GEMM, dtype=L.BF16, m=M, nn=N, kk=K, tile=tile,
+                               x=FAKE, wt=FAKE, y=FAKE))
+    assert rc == 0
+    info = L.OpInfo()
+    lib.miriam_op_query(h, ctypes.byref(info))
+    assert info.num_tiles == T
+    assert info.flops == 2.0 * M * N * K
+    lib.miriam_op_destroy(h)

@@ -1,0 +1,148 @@
+"""GPU parity of the elastic implicit-GEMM convolution against the CPU oracle,
+bitwise invariance across elastic configurations, and the device tile map.
+
+The single-conv workload: x 1x64x56x56 and w 64x64x3x3 ~ U[-1,1] (seed 0),
+bias ~ U[-1,1], stride 1, pad 1, ReLU, fp32; run unsharded and as 1/2/4/8
+shards with blocks of 64/128/256 threads, in forward and reverse shard order.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import RTOL, bits, empty, f32_dev, gpu_available, ints, rand, rel_err, to_f64
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X")]
+
+
+@pytest.fixture(scope="module")
+def ops():
+    from paper_2307_04339_amd import ops as o
+    return o
+
+
+def _cfg1(ops, tile=0, dtype="f32"):
+    x, x64 = rand((1, 56, 56, 64), dtype, seed=0)
+    w, w64 = rand((64, 3, 3, 64), dtype, seed=1)
+    b64 = np.random.default_rng(2).uniform(-1, 1, 64)
+    bias = f32_dev(b64)
+    y = empty((1, 56, 56, 64), dtype)
+    op = ops.conv2d(x, w, y, stride=1, pad=1, bias=bias, act="relu", tile=tile)
+    return op, y, (x64, w64, b64.astype(np.float32).astype(np.float64))
+
+
+def _persistent_grid(op, block, n_cu=256):
+    cap = max(1, op.info.max_wg_per_cu[{64: 0, 128: 1, 256: 2}[block]])
+    return n_cu * cap
+
+
+def test_conv_cfg1_matches_oracle(ops, orc):
+    op, y, (x64, w64, b64) = _cfg1(ops)
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, stride=1, pad=1, bias=b64, act="relu")
+    err = rel_err(to_f64(y), ref)
+    print(f"cfg1 conv fp32: T={op.T} tile={op.info.tile_m} rel={err:.3e}")
+    assert err <= RTOL["f32"]
+
+
+@pytest.mark.parametrize("tile", [1, 2, 3])
+def test_conv_cfg1_bitwise_across_elastic_configs(ops, orc, tile):
+    op, y, _ = _cfg1(ops, tile=tile)
+    op.run()
+    torch.cuda.synchronize()
+    ref_bits = bits(y)
+    T = op.T
+    for n in [1, 2, 4, 8]:
+        if n > T:
+            continue
+        plan = orc.balanced_split(T, n)
+        for block in [64, 128, 256]:
+            for order in ["fwd", "rev"]:
+                for gmode in ["persistent", "one-per-tile", "tiny"]:
+                    y.fill_(float("nan"))
+                    seq = list(range(n)) if order == "fwd" else list(reversed(range(n)))
+                    for j in seq:
+                        b, l = plan[j]
+                        g = {"persistent": min(l, _persistent_grid(op, block)),
+                             "one-per-tile": l, "tiny": 3}[gmode]
+                        op.launch(b, l, g, block)
+                    torch.cuda.synchronize()
+                    assert bits(y) == ref_bits, (tile, n, block, order, gmode)
+
+
+def test_conv_tile_map_matches_oracle(ops, orc):
+    op, y, _ = _cfg1(ops, tile=1)
+    T = op.T
+    for n, grids, block in [(1, [T], 256), (4, [5, 64, 1, 33], 128), (3, [7, 7, 7], 64),
+                            (8, [256] * 8, 256)]:
+        plan = orc.balanced_split(T, n)
+        ow = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+        oi = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros((T,), dtype=torch.int32, device="cuda")
+        for (b, l), g in zip(plan, grids):
+            op.launch_traced(b, l, g, block, ow, oi, cnt)
+        torch.cuda.synchronize()
+        _, wg_ref, it_ref, cnt_ref = orc.owner_map(T, plan, grids)
+        assert np.array_equal(cnt.cpu().numpy(), cnt_ref)
+        assert np.array_equal(ow.cpu().numpy(), wg_ref)
+        assert np.array_equal(oi.cpu().numpy(), it_ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_conv_integer_inputs_exact(ops, orc, dtype):
+    # integer operands in {-2..2}: every partial sum is an integer below 2^11, so
+    # fp32 accumulation is exact and GPU == oracle bit for bit (fp16 output exact up to 2048)
+    x, x64 = ints((1, 12, 12, 32), dtype, seed=3, lo=-2, hi=2)
+    w, w64 = ints((16, 3, 3, 32), dtype, seed=4, lo=-2, hi=2)
+    y = empty((1, 12, 12, 16), dtype)
+    op = ops.conv2d(x, w, y, stride=1, pad=1)
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, stride=1, pad=1)
+    assert np.abs(ref).max() < 2048
+    assert np.array_equal(to_f64(y), ref)
+
+
+CASES = [
+    # N, H, W, C, K, KH, stride, pad, act, epilogue
+    (1, 56, 56, 64, 64, 3, 1, 1, "relu", "bn"),
+    (1, 224, 224, 3, 64, 7, 2, 3, "relu", "bn"),      # ResNet stem: element loads (C=3)
+    (2, 17, 13, 32, 48, 3, 2, 1, "none", "bias"),     # ragged tiles
+    (1, 14, 14, 256, 512, 1, 2, 0, "none", "bn"),     # 1x1 downsample
+    (2, 7, 7, 96, 40, 1, 1, 0, "relu6", "bn_res"),    # residual, K not a tile multiple
+    (1, 9, 9, 24, 144, 1, 1, 0, "relu6", "bn"),       # C = 24 (not a chunk multiple)
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("case", CASES)
+def test_conv_shapes_match_oracle(ops, orc, dtype, case):
+    N, H, W, C, K, KH, s, p, act, epi = case
+    seed = abs(hash(case)) % 1000
+    x, x64 = rand((N, H, W, C), dtype, seed=seed)
+    w, w64 = rand((K, KH, KH, C), dtype, seed=seed + 1, lo=-0.2, hi=0.2)
+    Ho, Wo = (H + 2 * p - KH) // s + 1, (W + 2 * p - KH) // s + 1
+    rng = np.random.default_rng(seed + 2)
+    bias = bn = res = None
+    b64 = bn64 = r64 = None
+    if "bias" in epi:
+        b64 = rng.uniform(-1, 1, K).astype(np.float32).astype(np.float64)
+        bias = f32_dev(b64)
+    if "bn" in epi:
+        g_, be_ = rng.uniform(0.8, 1.2, K), rng.uniform(-0.1, 0.1, K)
+        mu, var = rng.uniform(-0.1, 0.1, K), rng.uniform(0.8, 1.2, K)
+        bn64 = np.stack([g_, be_, mu, var]).astype(np.float32).astype(np.float64)
+        bn = f32_dev(bn64)
+    if "res" in epi:
+        res, r64 = rand((N, Ho, Wo, K), dtype, seed=seed + 3)
+    y = empty((N, Ho, Wo, K), dtype)
+    for tile in [1, 2, 3]:
+        y.fill_(float("nan"))
+        op = ops.conv2d(x, w, y, stride=s, pad=p, bias=bias, bn=bn, residual=res, act=act, tile=tile)
+        op.run()
+        torch.cuda.synchronize()
+        ref = orc.conv2d(x64, w64, stride=s, pad=p, bias=b64,
+                         bn=None if bn64 is None else tuple(bn64), residual=r64, act=act)
+        err = rel_err(to_f64(y), ref)
+        assert err <= RTOL[dtype], (tile, err)
