@@ -1,0 +1,222 @@
+"""Coordinator behaviour on the host-simulated device (FAKE backend, no GPU).
+
+Checks, for every policy: each request completes exactly once; critical ops are
+never sharded; normal shards partition each op's tile space in tree-head order;
+no normal shard sized next to a critical kernel exceeds the Eq. (2) grid limit;
+one stream is FIFO; SEQUENTIAL never overlaps requests; deadlines, timed
+release, draining shutdown and busy-object errors behave as documented.
+"""
+import ctypes
+import time
+
+import pytest
+
+FAKE = 0x100000
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2307_04339_amd import _lib
+    _lib.load()
+    return _lib
+
+
+def _op(L, kind, **kw):
+    d = L.OpDesc()
+    d.kind = kind
+    d.dtype = L.F16
+    d.x = FAKE
+    d.wt = FAKE
+    d.y = FAKE
+    for k, v in kw.items():
+        setattr(d, k, v)
+    h = ctypes.c_void_p()
+    assert L.load().miriam_op_create(ctypes.byref(d), ctypes.byref(h)) == 0, L.load().miriam_last_error()
+    return h
+
+
+class _H:  # minimal op holder accepted by Coordinator.task
+    def __init__(self, h):
+        self.handle = h
+
+
+def _net(L, sizes):
+    """A chain of GEMM ops with the given tile counts (64x64 tiles)."""
+    ops = []
+    for t in sizes:
+        ops.append(_H(_op(L, L.OP_GEMM, m=64 * t, nn=64, kk=64, tile=2)))
+    return ops
+
+
+def _coord(**kw):
+    from paper_2307_04339_amd.runtime import Coordinator
+    base = dict(backend="fake", log_launches=1, fake_n_cu=8, fake_slots_per_cu=2,
+                fake_tile_ns=2000.0, fake_launch_ns=3000.0, quantum_us=10.0, profile_reps=1)
+    base.update(kw)
+    return Coordinator(**base)
+
+
+def _collect(co, n, timeout=20.0):
+    got = []
+    t0 = time.time()
+    while len(got) < n and time.time() - t0 < timeout:
+        got.extend(co.poll())
+        time.sleep(0.002)
+    return got
+
+
+@pytest.mark.parametrize("policy", ["elastic", "sequential", "multistream"])
+def test_every_request_completes_once(L, policy):
+    co = _coord(policy=policy, n_be_streams=2, inflight_depth=2)
+    try:
+        crit = co.task(_net(L, [3, 5, 2]))
+        be1 = co.task(_net(L, [40, 17, 64]))
+        be2 = co.task(_net(L, [9, 33]))
+        tickets = []
+        now = co.now_ns()
+        for i in range(6):
+            tickets.append(co.submit(crit, True, release_ns=now + i * 300_000))
+        for i in range(5):
+            tickets.append(co.submit(be1, False))
+            tickets.append(co.submit(be2, False))
+        recs = _collect(co, len(tickets))
+        assert sorted(r.ticket for r in recs) == sorted(tickets)
+        assert all(r.status == 0 for r in recs)
+        assert all(r.t_end_ns >= r.t_start_ns >= r.t_release_ns > 0 for r in recs)
+        co.drain(5000)
+        assert co.poll() == []
+        log = co.launch_log()
+        st = co.stats()
+        assert st.completed == len(tickets)
+        assert st.eq2_violations == 0
+        assert st.launches == len(log)
+        _check_log(log, policy)
+    finally:
+        co.shutdown()
+
+
+def _check_log(log, policy):
+    by_req = {}
+    for r in log:
+        by_req.setdefault((r.ticket, r.op_index), []).append(r)
+        if r.criticality == 1 or policy != "elastic":
+            # critical ops (and baselines) are never sharded
+            assert (r.shard_begin, r.shard_len, r.grid, r.block) == (0, r.num_tiles, r.num_tiles, 256)
+        if r.criticality == 0 and r.crit_busy:
+            assert r.eq2_grid_limit > 0 and r.grid <= r.eq2_grid_limit
+        assert 1 <= r.grid <= r.shard_len
+    for (tk, oi), shards in by_req.items():
+        # shards of one op: issued in increasing tile order, covering [0, T) exactly once
+        cur = 0
+        for s in shards:
+            assert s.shard_begin == cur
+            cur += s.shard_len
+        assert cur == shards[0].num_tiles
+    if policy != "sequential":
+        for r in log:
+            assert (r.stream == 0) == (r.criticality == 1)
+
+
+def test_elastic_shards_follow_the_tree_and_eq2(L):
+    from oracle import oracle as orc
+    co = _coord(policy="elastic", n_be_streams=1, inflight_depth=1, quantum_us=6.0)
+    try:
+        crit = co.task(_net(L, [3] * 12))
+        be = co.task(_net(L, [400, 256]))
+        now = co.now_ns()
+        tickets = [co.submit(be, False) for _ in range(12)]
+        tickets += [co.submit(crit, True, release_ns=now + 200_000 + i * 700_000) for i in range(4)]
+        recs = _collect(co, len(tickets))
+        assert len(recs) == len(tickets)
+        log = co.launch_log()
+        normal = [r for r in log if r.criticality == 0]
+        assert any(r.crit_busy for r in normal), "no shard was sized next to a critical kernel"
+        assert any(r.shard_len < r.num_tiles for r in normal), "nothing was sharded"
+        for r in normal:
+            # each shard is a node of the op's shaded binary tree, taken at its head
+            ln, _ = orc.tree_head(r.num_tiles, r.shard_begin, r.shard_len)
+            assert ln == r.shard_len
+            if r.crit_busy:
+                # Eq. (2): 8 simulated CUs, critical kernels of 3 tiles -> 8 - 3 = 5
+                assert r.eq2_grid_limit == orc.eq2_grid_limit(8, 3)
+                assert r.grid <= r.eq2_grid_limit
+    finally:
+        co.shutdown()
+
+
+def test_sequential_never_overlaps(L):
+    co = _coord(policy="sequential", n_be_streams=2)
+    try:
+        crit = co.task(_net(L, [4, 4]))
+        be = co.task(_net(L, [30, 30]))
+        now = co.now_ns()
+        tk = [co.submit(be, False) for _ in range(4)]
+        tk += [co.submit(crit, True, release_ns=now + i * 150_000) for i in range(4)]
+        recs = sorted(_collect(co, len(tk)), key=lambda r: r.t_start_ns)
+        assert len(recs) == len(tk)
+        for a, b in zip(recs, recs[1:]):
+            assert a.t_end_ns <= b.t_start_ns
+        assert all(r.stream == 0 for r in co.launch_log())
+    finally:
+        co.shutdown()
+
+
+def test_fifo_within_a_task_and_critical_edf(L):
+    co = _coord(policy="elastic", n_be_streams=1)
+    try:
+        be = co.task(_net(L, [20]))
+        crit = co.task(_net(L, [2]))
+        tks = [co.submit(be, False) for _ in range(5)]
+        rel = co.now_ns() + 2_000_000
+        late = co.submit(crit, True, release_ns=rel, deadline_ns=rel + 10**9)
+        early = co.submit(crit, True, release_ns=rel, deadline_ns=rel + 10**6)
+        recs = _collect(co, 7)
+        normal = [r.ticket for r in sorted(recs, key=lambda r: r.t_end_ns) if r.criticality == 0]
+        assert normal == tks
+        first_crit = [r.ticket for r in co.launch_log() if r.criticality == 1][0]
+        assert first_crit == early and late != early
+    finally:
+        co.shutdown()
+
+
+def test_deadlines_and_timed_release(L):
+    co = _coord()
+    try:
+        t = co.task(_net(L, [2]))
+        now = co.now_ns()
+        a = co.submit(t, True, release_ns=now + 3_000_000, deadline_ns=now + 10**10)
+        b = co.submit(t, True, deadline_ns=now + 1)  # already missed
+        recs = {r.ticket: r for r in _collect(co, 2)}
+        assert recs[a].deadline_met == 1 and recs[b].deadline_met == 0
+        assert recs[a].t_start_ns >= now + 3_000_000
+    finally:
+        co.shutdown()
+
+
+def test_busy_objects_and_state_errors(L):
+    lib = L.load()
+    co = _coord()
+    try:
+        ops = _net(L, [50, 50])
+        t = co.task(ops)
+        now = co.now_ns()
+        co.submit(t, False, release_ns=now + 50_000_000)  # held back 50 ms
+        assert lib.miriam_task_destroy(t.handle) == L.EBUSY
+        assert lib.miriam_op_destroy(ops[0].handle) == L.EBUSY
+        assert lib.miriam_init(ctypes.byref(co.cfg)) == L.ESTATE
+        assert lib.miriam_submit(None, 0, 0, 0, None) == L.EINVAL
+        assert lib.miriam_submit(t.handle, 2, 0, 0, None) == L.EINVAL
+        assert lib.miriam_drain(1) == L.EBUSY
+    finally:
+        co.shutdown()  # drains the held-back request first
+    assert lib.miriam_poll((L.Completion * 1)(), 1) == L.ESTATE
+    assert lib.miriam_op_destroy(ops[0].handle) == 0
+
+
+def test_bad_configs_rejected(L):
+    from paper_2307_04339_amd.runtime import default_config
+    lib = L.load()
+    for bad in [dict(policy=5), dict(n_be_streams=0), dict(n_be_streams=9), dict(inflight_depth=0),
+                dict(top_frac=0.0), dict(quantum_us=0.0), dict(backend=3)]:
+        c = default_config(**dict(dict(backend="fake"), **bad))
+        assert lib.miriam_init(ctypes.byref(c)) == L.EINVAL, bad
