@@ -1,0 +1,376 @@
+#!/usr/bin/env python3
+"""Miriam co-run benchmark on one MI355X.
+
+Default workload (two-task co-run, fp16): the critical task is a ResNet-18-shaped
+CNN at batch 1 released every 20 ms; the best-effort task is a VGG-16-shaped CNN
+at batch 8 run closed-loop on 224x224 inputs.  Inputs and weights are seeded
+synthetic tensors resident in HBM before timing starts.
+
+Phases: (1) per-kernel timing of the best-effort network with HIP events (the
+roofline object for its dominant kernel and the elastic-shard overhead of that
+kernel); (2) critical task alone (solo); (3) the Sequential baseline; (4) Miriam
+(elastic policy).  A "step" is one critical release period of the co-run; W
+warm-up periods are run first, then exactly K timed periods.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "critical p99 latency overhead vs solo; best-effort inf/s; kernel % roofline"
+PEAK_TFLOPS = {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+
+CONFIGS = {
+    "corun-resnet18-vgg16-fp16": dict(
+        dtype="f16", crit=("resnet18", dict(batch=1)), period_ms=20.0, arrival="periodic",
+        be=[("vgg16", dict(batch=8))]),
+    "corun-encoder-mobilenetv2-bf16": dict(
+        dtype="bf16", crit=("encoder", dict(batch=1, seq=128)), period_ms=10.0, arrival="periodic",
+        be=[("mobilenetv2", dict(batch=16))]),
+    "mix4-bf16": dict(
+        dtype="bf16", crit=("resnet18", dict(batch=1)), period_ms=15.0, arrival="poisson",
+        be=[("vgg16", dict(batch=8)), ("encoder", dict(batch=4, seq=256)), ("mobilenetv2", dict(batch=32))]),
+}
+DEFAULT_CONFIG = "corun-resnet18-vgg16-fp16"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pct(xs, q):
+    return float(np.percentile(np.asarray(xs, dtype=np.float64), q)) if len(xs) else float("nan")
+
+
+# ----------------------------------------------------------- kernel timing
+def time_layers(net, reps, flush):
+    """Average unsharded duration of every layer, HIP events on torch's current stream."""
+    import torch
+    out = []
+    for layer in net.layers:
+        layer.op.run()
+        torch.cuda.synchronize()
+        total = 0.0
+        for _ in range(reps):
+            flush.zero_()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            layer.op.run()
+            e1.record()
+            e1.synchronize()
+            total += e0.elapsed_time(e1)
+        us = 1000.0 * total / reps
+        out.append(dict(name=layer.name, us=us, flops=layer.op.info.flops, bytes=layer.op.info.bytes,
+                        tiles=layer.op.T))
+    return out
+
+
+def roofline_of(k, dtype):
+    ai = k["flops"] / max(1.0, k["bytes"])
+    ridge = PEAK_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if ai >= ridge:
+        ach = k["flops"] / (k["us"] * 1e-6) / 1e12
+        return dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_TFLOPS[dtype], unit="TFLOP/s",
+                    frac=round(ach / PEAK_TFLOPS[dtype], 4), traffic=None)
+    ach = k["bytes"] / (k["us"] * 1e-6) / 1e9
+    return dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                frac=round(ach / PEAK_HBM_GBS, 4), traffic=None)
+
+
+def shard_overhead(layer, reps, flush, n_cu, lib):
+    import ctypes
+    import torch
+    op = layer.op
+    T = op.T
+    cap = max(1, op.info.max_wg_per_cu[2])
+
+    def timed(plan):
+        tot = 0.0
+        for _ in range(reps):
+            flush.zero_()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for (b, l, g, bl) in plan:
+                op.launch(b, l, g, bl)
+            e1.record()
+            e1.synchronize()
+            tot += e0.elapsed_time(e1)
+        return 1000.0 * tot / reps
+
+    base = timed([(0, T, T, 256)])
+    res = {"unsharded_us": round(base, 2)}
+    for n in (1, 2, 4, 8):
+        if n > T:
+            continue
+        b = (ctypes.c_int64 * n)()
+        ln = (ctypes.c_int64 * n)()
+        lib.miriam_plan_split(T, n, b, ln)
+        plan = [(b[j], ln[j], int(min(ln[j], n_cu * cap)), 256) for j in range(n)]
+        t = timed(plan)
+        res[f"shards{n}_us"] = round(t, 2)
+        res[f"shards{n}_overhead"] = round(t / base - 1.0, 4)
+    return res
+
+
+# ----------------------------------------------------------------- co-run
+def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, seed, ccfg, with_be=True):
+    import torch
+    from paper_2307_04339_amd import synth
+    from paper_2307_04339_amd.runtime import Coordinator
+    torch.cuda.synchronize()
+    co = Coordinator(policy=policy, n_be_streams=max(1, len(be_nets)), **ccfg)
+    try:
+        ct = co.task(crit_net.ops())
+        bts = [co.task(n.ops()) for n in be_nets] if with_be else []
+        period_ns = int(period_ms * 1e6)
+        n_rel = n_warm + n_steps
+        if arrival == "poisson":
+            rel = synth.poisson_releases(n_rel, period_ns, seed)
+        else:
+            rel = synth.periodic_releases(n_rel, period_ns)
+        t0 = co.now_ns() + 20_000_000
+        crit_tickets = {}
+        for i, r in enumerate(rel):
+            tk = co.submit(ct, True, release_ns=int(t0 + r), deadline_ns=int(t0 + r + period_ns))
+            crit_tickets[tk] = i
+        t_win0 = int(t0 + rel[n_warm])
+        t_end_rel = int(t0 + rel[-1] + period_ns)
+        be_out = {}
+        be_done = []   # (task index, t_end)
+        be_ticket_task = {}
+        for j, bt in enumerate(bts):
+            for _ in range(2):
+                tk = co.submit(bt, False)
+                be_ticket_task[tk] = j
+            be_out[j] = 2
+        crit_lat = {}
+        while len(crit_lat) < n_rel:
+            recs = co.poll()
+            for r in recs:
+                if r.criticality == 1:
+                    crit_lat[crit_tickets[r.ticket]] = (r.t_end_ns - r.t_release_ns, r.t_end_ns)
+                else:
+                    j = be_ticket_task.pop(r.ticket)
+                    be_done.append((j, r.t_end_ns))
+                    be_out[j] -= 1
+                    if co.now_ns() < t_end_rel:
+                        tk = co.submit(bts[j], False)
+                        be_ticket_task[tk] = j
+                        be_out[j] += 1
+            if not recs:
+                time.sleep(0.0002)
+        t_win1 = max(v[1] for v in crit_lat.values())
+        co.drain(120000)
+        for r in co.poll():
+            if r.criticality == 0:
+                be_done.append((be_ticket_task.pop(r.ticket), r.t_end_ns))
+        st = co.stats()
+        torch.cuda.synchronize()
+    finally:
+        co.shutdown()
+    lat_ms = [crit_lat[i][0] / 1e6 for i in range(n_warm, n_rel)]
+    win_s = (t_win1 - t_win0) / 1e9
+    per_task = []
+    for j, n in enumerate(be_nets if with_be else []):
+        cnt = sum(1 for (jj, te) in be_done if jj == j and t_win0 <= te <= t_win1)
+        per_task.append(dict(net=n.name, batch=n.batch, req_s=cnt / win_s, img_s=cnt * n.batch / win_s))
+    return dict(policy=policy, p50_ms=pct(lat_ms, 50), p99_ms=pct(lat_ms, 99), mean_ms=float(np.mean(lat_ms)),
+                max_ms=float(np.max(lat_ms)), window_s=win_s, be=per_task,
+                be_img_s=sum(p["img_s"] for p in per_task), be_req_s=sum(p["req_s"] for p in per_task),
+                crit_req_s=n_steps / win_s, launches=st.launches,
+                decision_us=st.decision_ns_total / max(1, st.decisions) / 1000.0,
+                eq2_violations=st.eq2_violations)
+
+
+# ------------------------------------------------------------ cpu baseline
+def cpu_baseline(net_name, kw, budget_macs=1.5e9, seed=0):
+    """Oracle time of one best-effort inference image, from a bounded sample: each
+    convolution computes sampled output pixels (all channels), scaled by the pixel
+    count; pooling and FC layers run in full for one image."""
+    from oracle import oracle as orc
+    from paper_2307_04339_amd import models  # shapes only
+    rng = np.random.default_rng(seed)
+    shapes = []
+    # replay the network's layer shapes on the host (batch 1)
+    import torch  # noqa: F401
+    net = models.BUILDERS[net_name](**dict(kw, batch=1))
+    for l in net.layers:
+        x = l.t.get("x")
+        shapes.append((l.kind, None if x is None else tuple(x.shape), l.t["y"].shape,
+                       None if l.t.get("w") is None else tuple(l.t["w"].shape), dict(l.params)))
+    del net
+    total = 0.0
+    t_start = time.time()
+    for kind, xs, ys, ws, p in shapes:
+        if kind == "conv":
+            N, H, W, C = xs
+            K, KH, KW, _ = ws
+            _, Ho, Wo, _ = ys
+            npx = Ho * Wo
+            per = K * KH * KW * C
+            s = int(max(1, min(npx, budget_macs // per)))
+            crops = rng.uniform(-1, 1, (s, KH, KW, C))
+            w = rng.uniform(-1, 1, ws)
+            t0 = time.perf_counter()
+            orc.conv2d(crops, w, stride=1, pad=0, act=p["act"])
+            total += (time.perf_counter() - t0) * npx / s
+        elif kind in ("maxpool", "avgpool"):
+            x = rng.uniform(-1, 1, xs)
+            fn = orc.maxpool if kind == "maxpool" else orc.avgpool
+            t0 = time.perf_counter()
+            fn(x, p["k"], p["stride"], p["pad"])
+            total += time.perf_counter() - t0
+        elif kind == "gemm":
+            x = rng.uniform(-1, 1, (1, xs[1]))
+            w = rng.uniform(-1, 1, ws)
+            t0 = time.perf_counter()
+            orc.linear(x, w, act=p["act"])
+            total += time.perf_counter() - t0
+    wall = time.time() - t_start
+    return dict(value=round(1.0 / total, 5), unit="img/s", cores=1, kind="oracle",
+                sample=f"one {net_name} image: <= {budget_macs:.0e} MACs of sampled output pixels per "
+                       f"convolution (scaled by pixel count), pooling and FC in full; "
+                       f"{wall:.1f} s of CPU work, single thread")
+
+
+# ------------------------------------------------------------------- main
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=sorted(CONFIGS))
+    ap.add_argument("--reps", type=int, default=20, help="repetitions per kernel timing")
+    ap.add_argument("--quantum-us", type=float, default=40.0)
+    ap.add_argument("--depth", type=int, default=1)
+    ap.add_argument("--phases", default="kernels,solo,sequential,elastic")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(each task set is placed on one device; see the multi-GPU note in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2307_04339_amd import _lib as L
+    from paper_2307_04339_amd import models
+    from paper_2307_04339_amd.ops import device_info
+
+    cfg = CONFIGS[args.config]
+    dtype = cfg["dtype"]
+    dev = device_info()
+    log(f"device {dev.arch.decode()} cus={dev.n_cu} config={args.config}")
+    cname, ckw = cfg["crit"]
+    crit_net = models.BUILDERS[cname](dtype=dtype, **ckw)
+    be_nets = [models.BUILDERS[n](dtype=dtype, **kw) for (n, kw) in cfg["be"]]
+    crit_net.forward()
+    for n in be_nets:
+        n.forward()
+    torch.cuda.synchronize()
+    phases = set(args.phases.split(","))
+    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
+    result = {}
+
+    kern = None
+    if "kernels" in phases:
+        log("timing kernels ...")
+        table = []
+        for n in be_nets + [crit_net]:
+            for k in time_layers(n, args.reps, flush):
+                k["net"] = n.name
+                table.append(k)
+        dom_net = be_nets[0]
+        dom = max((k for k in table if k["net"] == dom_net.name), key=lambda k: k["us"])
+        kern = roofline_of(dom, dtype)
+        kern["kernel"] = f"{dom_net.name}.{dom['name']}"
+        kern["launch_us"] = round(dom["us"], 2)
+        kern["flops_per_launch"] = dom["flops"]
+        kern["bytes_per_launch"] = dom["bytes"]
+        layer = next(l for l in dom_net.layers if l.name == dom["name"])
+        result["elastic_overhead"] = dict(kernel=kern["kernel"],
+                                          **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load()))
+        result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
+                                  **{kk: vv for kk, vv in roofline_of(k, dtype).items()
+                                     if kk in ("bound", "achieved", "unit", "frac")})
+                             for k in sorted(table, key=lambda k: -k["us"])[:12]]
+        result["be_solo_ms_per_request"] = {n.name: round(sum(k["us"] for k in table if k["net"] == n.name) / 1000, 3)
+                                            for n in be_nets}
+        result["crit_kernel_sum_ms"] = round(sum(k["us"] for k in table if k["net"] == crit_net.name) / 1000, 3)
+    del flush
+    torch.cuda.empty_cache()
+
+    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, profile_reps=3)
+    runs = {}
+    for ph in ("solo", "sequential", "multistream", "elastic"):
+        if ph not in phases:
+            continue
+        log(f"phase {ph} ...")
+        policy = "elastic" if ph == "solo" else ph
+        runs[ph] = run_phase(policy, crit_net, be_nets, args.warmup, args.steps, cfg["period_ms"],
+                             cfg["arrival"], seed=11, ccfg=ccfg, with_be=(ph != "solo"))
+        r = runs[ph]
+        log(f"  p50 {r['p50_ms']:.3f} ms  p99 {r['p99_ms']:.3f} ms  be {r['be_img_s']:.1f} img/s "
+            f"launches {r['launches']}")
+
+    main_run = runs.get("elastic") or next(iter(runs.values()), None)
+    value = main_run["be_img_s"] if main_run else float("nan")
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "img/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1000.0 * main_run["window_s"] / args.steps, 4) if main_run else None,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": args.config,
+                   "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
+                   "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
+                   "quantum_us": args.quantum_us, "inflight_depth": args.depth},
+    }
+    if "solo" in runs and main_run:
+        solo = runs["solo"]
+        out["critical"] = {
+            "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
+            "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
+            "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
+    for ph, r in runs.items():
+        out.setdefault("phases", {})[ph] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+    if "sequential" in runs and main_run:
+        seq = runs["sequential"]
+        out["best_effort"] = {
+            "elastic_img_s": round(main_run["be_img_s"], 2), "sequential_img_s": round(seq["be_img_s"], 2),
+            "speedup_vs_sequential": round(main_run["be_img_s"] / max(1e-9, seq["be_img_s"]), 3),
+            "sequential_p99_ms": round(seq["p99_ms"], 4)}
+    if kern:
+        out["roofline"] = kern
+    out.update({k: v for k, v in result.items()})
+    if not args.no_cpu_baseline:
+        bname, bkw = cfg["be"][0]
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(bname, dict(bkw, dtype=dtype))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
