@@ -102,7 +102,8 @@ typedef struct miriam_op_desc {
     int64_t ldx, ldw, ldy;               /* row strides in elements, 0 = dense */
     int64_t sx0, sx1, sw0, sw1, sy0, sy1; /* BGEMM batch strides in elements */
     int32_t b_nmajor;
-    int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128 tiles */
+    int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128, 4 = 128x64,
+                           5 = 16-column split-K (GEMM, fp16/bf16, m <= 16) */
     float eps;          /* BN / LN epsilon */
     float scale;        /* SOFTMAX scale */
     const void *x, *wt, *bias, *bn, *residual; /* device pointers (wt = weights) */

@@ -97,16 +97,39 @@ __device__ __forceinline__ float apply_act(float v, int act) {
     }
 }
 
-// v = act(BN(acc + bias[c]) + res), in fp32, per element.
-__device__ __forceinline__ float epilogue_apply(const Epilogue &e, float acc, int64_t c, float res) {
-    float v = acc;
-    if (e.flags & EPI_BIAS) v += e.bias[c];
+// The fused epilogue  v = act(BN(acc + bias[c]) + res)  in fp32.  Split into the
+// per-channel affine part (applied where the accumulator lives) and the residual /
+// activation part (applied where the output is stored); same operations, same order.
+struct ChanParams {
+    float bias, mean, scale, beta;
+};
+
+__device__ __forceinline__ ChanParams chan_params(const Epilogue &e, int64_t c) {
+    ChanParams p{0.0f, 0.0f, 1.0f, 0.0f};
+    if (e.flags & EPI_BIAS) p.bias = e.bias[c];
     if (e.flags & EPI_BN) {
-        const float g = e.bn[c], b = e.bn[e.C + c], mu = e.bn[2 * e.C + c], var = e.bn[3 * e.C + c];
-        v = (v - mu) * (g / sqrtf(var + e.eps)) + b;
+        p.scale = e.bn[c] / sqrtf(e.bn[3 * e.C + c] + e.eps);
+        p.mean = e.bn[2 * e.C + c];
+        p.beta = e.bn[e.C + c];
     }
+    return p;
+}
+
+__device__ __forceinline__ float epilogue_pre(const Epilogue &e, const ChanParams &p, float acc) {
+    float v = acc;
+    if (e.flags & EPI_BIAS) v += p.bias;
+    if (e.flags & EPI_BN) v = (v - p.mean) * p.scale + p.beta;
+    return v;
+}
+
+__device__ __forceinline__ float epilogue_post(const Epilogue &e, float v, float res) {
     if (e.flags & EPI_RES) v += res;
     return apply_act(v, e.act);
+}
+
+// Whole epilogue for one element of channel c.
+__device__ __forceinline__ float epilogue_apply(const Epilogue &e, float acc, int64_t c, float res) {
+    return epilogue_post(e, epilogue_pre(e, chan_params(e, c), acc), res);
 }
 
 }  // namespace miriam

@@ -79,13 +79,15 @@ struct IgemmKernel {
     static constexpr int NT = kWave * P;                 // physical threads
     static constexpr int VEC = 16 / (int)sizeof(T);      // elements per 16-byte vector
     static constexpr int KSTEP = (kWave / MS) * MF::KPL; // K consumed by one MFMA
-    static constexpr int KT = sizeof(T) == 4 ? 16 : 32;  // K per LDS chunk
+    static constexpr int KT = sizeof(T) == 4 ? 32 : 64;  // K per LDS chunk
     static constexpr int PK = VEC;                       // row padding (16 bytes)
     static constexpr int LDK = KT + PK;                  // LDS row length in elements
     static constexpr int KPR = KT / VEC;                 // vectors per K-chunk row
     static constexpr int BM = TM / 2 / MS, BN = TN / 2 / MS;
     static constexpr int LW = kLogicalWaves / P;         // logical waves per physical wave
-    static constexpr int MAXSL = (8 * 16 / MF::NACC) / (BM * BN) > 0 ? (8 * 16 / MF::NACC) / (BM * BN) : 1;
+    // accumulators held at once: 128 per lane, 64 for single-wave blocks (they also hold all loads)
+    static constexpr int MAXACC = P == 1 ? 64 : 128;
+    static constexpr int MAXSL = (MAXACC / MF::NACC) / (BM * BN) > 0 ? (MAXACC / MF::NACC) / (BM * BN) : 1;
     static constexpr int SL = LW < MAXSL ? LW : MAXSL;   // logical waves held at once
     static constexpr int ROUNDS = LW / SL;               // sequential passes over K
     static constexpr bool A_VEC = (LAY == LAY_VEC || LAY == LAY_VEC_NB);
@@ -93,10 +95,14 @@ struct IgemmKernel {
     static constexpr bool B_VEC = (LAY == LAY_VEC || LAY == LAY_VEC_NB);
     static constexpr int NVA = (TM * KPR + NT - 1) / NT;           // A vectors per thread
     static constexpr int NVB = (TN * KPR + NT - 1) / NT;           // B vectors per thread
+    static constexpr int LDC = TN + 4;                   // staged output row (fp32)
+    static constexpr int AB_BYTES = 2 * (TM + TN) * LDK * (int)sizeof(T);
+    static constexpr int C_BYTES = TM * LDC * 4;
+    static constexpr int LDS_BYTES = AB_BYTES > C_BYTES ? AB_BYTES : C_BYTES;
     static_assert(LW % SL == 0, "slots must divide logical waves");
     static_assert(KT % KSTEP == 0, "chunk must hold whole MFMA steps");
     static_assert(BM >= 1 && BN >= 1, "tile too small for the MFMA shape");
-    static constexpr int LDS_BYTES = 2 * (TM + TN) * LDK * (int)sizeof(T);
+    static_assert((TN / 2) % VEC == 0, "sub-tile rows must hold whole vectors");
 };
 
 template <class T, int TM, int TN, int MS, int P, int LAY>
@@ -107,10 +113,14 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
     typedef typename K_::acc_t acc_t;
     constexpr int NT = K_::NT, VEC = K_::VEC, KT = K_::KT, LDK = K_::LDK, KPR = K_::KPR;
     constexpr int BM = K_::BM, BN = K_::BN, SL = K_::SL, ROUNDS = K_::ROUNDS;
-    constexpr int NVA = K_::NVA, NVB = K_::NVB, KSTEP = K_::KSTEP;
+    constexpr int NVA = K_::NVA, NVB = K_::NVB, KSTEP = K_::KSTEP, LDC = K_::LDC;
 
-    __shared__ __attribute__((aligned(16))) T As[2][TM][LDK];
-    __shared__ __attribute__((aligned(16))) T Bs[2][TN][LDK];
+    __shared__ __attribute__((aligned(16))) char smem[K_::LDS_BYTES];
+    T *const lds = reinterpret_cast<T *>(smem);
+    float *const Cs = reinterpret_cast<float *>(smem);
+    // A tile of buffer b: rows [b*(TM+TN), +TM); B tile: the following TN rows
+    auto As = [&](int b, int row) -> T * { return lds + ((b * (TM + TN)) + row) * LDK; };
+    auto Bs = [&](int b, int row) -> T * { return lds + ((b * (TM + TN)) + TM + row) * LDK; };
 
     const int tid = threadIdx.x;
     const int pw = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -123,6 +133,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
     const int64_t nch = (a.K + KT - 1) / KT;
     const int64_t G = gridDim.x;
     const int64_t rank = wg_rank(blockIdx.x, G);
+    const int32_t C32 = (int32_t)a.C, KW32 = a.KW, KH32 = a.KH;
 
     int iter = 0;
     for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
@@ -167,15 +178,15 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
 #pragma unroll
                         for (int e = 0; e < MF::NACC; ++e) acc[s][i][jn][e] = 0.0f;
 
-            // K-position of this thread's A/B vector slot within a chunk.
+            // (tap row, tap column, channel) of k = chunk*KT + kv*VEC for this thread's slot
             const int kv = tid % KPR;
-            int32_t kr, ks, kc;  // tap row, tap column, channel of k = chunk*KT + kv*VEC
+            int32_t kr, ks, kc;
             {
-                const int64_t k = (int64_t)kv * VEC;
-                kc = (int32_t)(k % a.C);
-                const int64_t tap = k / a.C;
-                ks = (int32_t)(tap % a.KW);
-                kr = (int32_t)(tap / a.KW);
+                const int32_t k = kv * VEC;
+                kc = k % C32;
+                const int32_t tap = k / C32;
+                ks = tap % KW32;
+                kr = tap / KW32;
             }
 
             Vec16<T> ra[NVA], rb[NVB];
@@ -187,19 +198,22 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                 for (int j = 0; j < NVA; ++j) {
                     if constexpr (K_::A_VEC) {
                         const int32_t h = a_h0[j] + kr, w = a_w0[j] + ks;
-                        const bool ok = a_ok[j] && kr < a.KH && h >= 0 && h < a.H && w >= 0 && w < a.W;
+                        const bool ok = a_ok[j] && kr < KH32 && h >= 0 && h < a.H && w >= 0 && w < a.W;
                         ra[j] = ok ? ld_vec(Xb + a_img[j] + ((int64_t)h * a.W + w) * a.ldx + kc) : zero_vec<T>();
                     } else {
+                        // element loads; (r, s, c) stepped incrementally from the slot's first element
                         Vec16<T> v = zero_vec<T>();
+                        int32_t r_ = kr, s_ = ks, c_ = kc;
 #pragma unroll
                         for (int e = 0; e < VEC; ++e) {
-                            const int64_t k = k0 + kv * VEC + e;
-                            if (a_ok[j] && k < a.K) {
-                                const int64_t c = k % a.C, tap = k / a.C;
-                                const int32_t s_ = (int32_t)(tap % a.KW), r_ = (int32_t)(tap / a.KW);
+                            if (a_ok[j] && r_ < KH32) {
                                 const int32_t h = a_h0[j] + r_, w = a_w0[j] + s_;
                                 if (h >= 0 && h < a.H && w >= 0 && w < a.W)
-                                    v.e[e] = Xb[a_img[j] + ((int64_t)h * a.W + w) * a.ldx + c];
+                                    v.e[e] = Xb[a_img[j] + ((int64_t)h * a.W + w) * a.ldx + c_];
+                            }
+                            if (++c_ == C32) {
+                                c_ = 0;
+                                if (++s_ == KW32) { s_ = 0; ++r_; }
                             }
                         }
                         ra[j] = v;
@@ -240,11 +254,11 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                         }
                     }
                 }
-                // advance the vector slot's (r, s, c) by one chunk
+                // advance the slot's (r, s, c) by one chunk
                 kc += KT;
-                while (kc >= a.C) {
-                    kc -= (int32_t)a.C;
-                    if (++ks == a.KW) { ks = 0; ++kr; }
+                while (kc >= C32) {
+                    kc -= C32;
+                    if (++ks == KW32) { ks = 0; ++kr; }
                 }
             };
 
@@ -252,19 +266,19 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
 #pragma unroll
                 for (int j = 0; j < NVA; ++j) {
                     const int v = tid + j * NT;
-                    if (v < TM * KPR) st_vec(&As[buf][v / KPR][(v % KPR) * VEC], ra[j]);
+                    if (v < TM * KPR) st_vec(As(buf, v / KPR) + (v % KPR) * VEC, ra[j]);
                 }
 #pragma unroll
                 for (int j = 0; j < NVB; ++j) {
                     const int v = tid + j * NT;
                     if (v < TN * KPR) {
                         if constexpr (!K_::B_NMAJ) {
-                            st_vec(&Bs[buf][v / KPR][(v % KPR) * VEC], rb[j]);
+                            st_vec(Bs(buf, v / KPR) + (v % KPR) * VEC, rb[j]);
                         } else {
                             constexpr int NPR = TN / VEC;
                             const int kl = v / NPR, nv = v % NPR;
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) Bs[buf][nv * VEC + e][kl] = rb[j].e[e];
+                            for (int e = 0; e < VEC; ++e) Bs(buf, nv * VEC + e)[kl] = rb[j].e[e];
                         }
                     }
                 }
@@ -281,12 +295,10 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                         op_t bop[BN];
 #pragma unroll
                         for (int jn = 0; jn < BN; ++jn)
-                            bop[jn] = *reinterpret_cast<const op_t *>(
-                                &Bs[buf][wn * (TN / 2) + jn * MS + lane % MS][kcol]);
+                            bop[jn] = *reinterpret_cast<const op_t *>(Bs(buf, wn * (TN / 2) + jn * MS + lane % MS) + kcol);
 #pragma unroll
                         for (int i = 0; i < BM; ++i) {
-                            const op_t aop = *reinterpret_cast<const op_t *>(
-                                &As[buf][wm * (TM / 2) + i * MS + lane % MS][kcol]);
+                            const op_t aop = *reinterpret_cast<const op_t *>(As(buf, wm * (TM / 2) + i * MS + lane % MS) + kcol);
 #pragma unroll
                             for (int jn = 0; jn < BN; ++jn) acc[s][i][jn] = MF::run(aop, bop[jn], acc[s][i][jn]);
                         }
@@ -305,7 +317,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                 __syncthreads();
             }
 
-            // ---- epilogue: MFMA accumulator (block row/col) -> output element
+            // ---- epilogue, stage 1: accumulators (+ bias, BN) -> LDS as fp32
 #pragma unroll
             for (int s = 0; s < SL; ++s) {
                 const int lam = (rd * SL + s) * P + pw;
@@ -313,19 +325,51 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
 #pragma unroll
                 for (int i = 0; i < BM; ++i)
 #pragma unroll
-                    for (int jn = 0; jn < BN; ++jn)
+                    for (int jn = 0; jn < BN; ++jn) {
+                        const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                        const int64_t n = n0 + col;
+                        const ChanParams cp = chan_params(a.epi, n < a.Nc ? n : 0);
 #pragma unroll
                         for (int e = 0; e < MF::NACC; ++e) {
                             const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
-                            const int64_t m = m0 + wm * (TM / 2) + i * MS + rr;
-                            const int64_t n = n0 + wn * (TN / 2) + jn * MS + lane % MS;
-                            if (m < a.M && n < a.Nc) {
-                                const int64_t off = yoff + m * a.ldy + n;
-                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off) : 0.0f;
-                                st_f(Y + off, epilogue_apply(a.epi, acc[s][i][jn][e], n, res));
-                            }
+                            const int row = wm * (TM / 2) + i * MS + rr;
+                            Cs[row * LDC + col] = epilogue_pre(a.epi, cp, acc[s][i][jn][e]);
                         }
+                    }
             }
+            __syncthreads();
+            // ---- stage 2: + residual, activation, one rounding, coalesced row stores
+            {
+                constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
+                const int lam0 = rd * SL * P;
+                for (int idx = tid; idx < SL * P * SUBR * CV; idx += NT) {
+                    const int sub = idx / (SUBR * CV);
+                    const int rem2 = idx - sub * (SUBR * CV);
+                    const int r = rem2 / CV, cv = rem2 - (rem2 / CV) * CV;
+                    const int lam = lam0 + sub;
+                    const int row = (lam >> 1) * SUBR + r, col = (lam & 1) * SUBC + cv * VEC;
+                    const int64_t m = m0 + row, n = n0 + col;
+                    if (m >= a.M) continue;
+                    const float *cr = Cs + row * LDC + col;
+                    const int64_t off = yoff + m * a.ldy + n;
+                    if (a.vec_store && n + VEC <= a.Nc) {
+                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
+                        Vec16<T> o;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, cr[e], TypeOps<T>::to_f(rv.e[e])));
+                        st_vec(Y + off, o);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (n + e < a.Nc) {
+                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
+                                st_f(Y + off + e, epilogue_post(a.epi, cr[e], res));
+                            }
+                    }
+                }
+            }
+            __syncthreads();
         }
     }
 }
@@ -355,6 +399,7 @@ inline int igemm_table_cfg(int cfg, const void *out[3], int *lds) {
     case CFG_32: igemm_table<T, 32, 32, 16, LAY>(out, lds); return 0;
     case CFG_64: igemm_table<T, 64, 64, 32, LAY>(out, lds); return 0;
     case CFG_128: igemm_table<T, 128, 128, 32, LAY>(out, lds); return 0;
+    case CFG_128x64: igemm_table<T, 128, 64, 32, LAY>(out, lds); return 0;
     default: return -1;
     }
 }

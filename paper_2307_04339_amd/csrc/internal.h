@@ -15,7 +15,7 @@ namespace miriam {
 void set_error(const std::string &msg);
 int hip_fail(hipError_t e, const char *what);  // records the HIP error text, returns MIRIAM_EHIP
 
-enum Family { FAM_IGEMM = 0, FAM_PIX = 1, FAM_ROW = 2 };
+enum Family { FAM_IGEMM = 0, FAM_PIX = 1, FAM_ROW = 2, FAM_SKINNY = 3 };
 
 // Kernel tables (one entry per physical block of 64, 128, 256 threads).
 int igemm_kernels_f32(int cfg, int lay, const void *out[3], int *lds);
@@ -23,6 +23,7 @@ int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds);
 int igemm_kernels_bf16(int cfg, int lay, const void *out[3], int *lds);
 int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
+int skinny_kernels(int dtype, const void *out[3]);
 
 }  // namespace miriam
 

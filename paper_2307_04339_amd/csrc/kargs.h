@@ -45,6 +45,7 @@ struct IgemmArgs {
     int64_t mT, nT;        // tiles along m and n
     int64_t bdiv, sx0, sx1, sw0, sw1, sy0, sy1;  // batch offsets
     int64_t img_x;         // elements between images of x
+    int32_t vec_store;     // 1: output / residual rows allow 16-byte vector access
     Epilogue epi;
 };
 
@@ -76,6 +77,6 @@ struct RowArgs {
 enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3 };
 enum RowKind { ROW_SOFTMAX = 0, ROW_LAYERNORM = 1 };
 enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3 };
-enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3 };
+enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4 };
 
 }  // namespace miriam

@@ -1,0 +1,115 @@
+// Elastic kernel for skinny products (fully connected layers at small batch):
+// Y[m][n] = sum_k X[m][k] * W[n][k] with M <= 16.  Such a product is bound by
+// streaming W from HBM, so the logical tile is 16 output columns (all M rows)
+// and the K range is split into 4 fixed quarters, one per logical wave; each
+// wave streams its quarter of the 16 weight rows with 16-byte loads straight
+// into MFMA 16x16x32 operands (no LDS staging: nothing is reused), and the 4
+// partial sums are added in fixed order (wave 0 + 1 + 2 + 3) through LDS before
+// the epilogue.  The split and the order depend only on K, never on the shard,
+// grid or physical block, so results stay bit-identical across elastic
+// configurations.
+//
+// K-order inside a wave: for four consecutive MFMA steps the lanes of k-group g
+// hold the 32 consecutive elements [k0 + 32 g, k0 + 32 g + 32), so each lane
+// reads 64 contiguous bytes per weight row; A and B use the same assignment, so
+// every MFMA still sums A[m][k] * W[n][k] over matching k.
+#include "elastic_common.h"
+#include "igemm.h"
+
+namespace miriam {
+
+constexpr int kSkinnyTN = 16;
+
+template <class T, int P>
+__global__ __launch_bounds__(kWave * P) void skinny_kernel(IgemmArgs a, Shard sh) {
+    typedef Mfma<T, 16> MF;
+    typedef typename MF::op_t op_t;
+    constexpr int GROUP = 128;  // K consumed by 4 MFMA steps
+    __shared__ float part[kLogicalWaves][16][17];
+
+    const int tid = threadIdx.x;
+    const int pw = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const T *__restrict__ X = static_cast<const T *>(a.x);
+    const T *__restrict__ Wt = static_cast<const T *>(a.w);
+    T *__restrict__ Y = static_cast<T *>(a.y);
+    const T *__restrict__ R = static_cast<const T *>(a.res);
+    // quarter length, a multiple of GROUP
+    const int64_t kq = ((a.K + 4 * GROUP - 1) / (4 * GROUP)) * GROUP;
+    const int64_t G = gridDim.x;
+    const int64_t rank = wg_rank(blockIdx.x, G);
+    const int row = lane % 16, grp = lane / 16;
+
+    int iter = 0;
+    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+        trace_tile(sh, t, iter);
+        const int64_t n0 = t * kSkinnyTN;
+        const int64_t n = n0 + row;
+        const bool a_ok = row < a.M, b_ok = n < a.Nc;
+        const T *xr = X + (int64_t)row * a.ldx;
+        const T *wr = Wt + n * a.ldw;
+        for (int s = 0; s < kLogicalWaves / P; ++s) {
+            const int lam = s * P + pw;
+            const int64_t kb = lam * kq;
+            const int64_t ke = kb + kq < a.K ? kb + kq : a.K;
+            f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            Vec16<T> av[4], bv[4], an[4], bn_[4];
+            auto load = [&](int64_t k0, Vec16<T> *ao, Vec16<T> *bo) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t k = k0 + grp * 32 + j * 8;
+                    const bool kin = k + 8 <= ke;
+                    ao[j] = (a_ok && kin) ? ld_vec(xr + k) : zero_vec<T>();
+                    bo[j] = (b_ok && kin) ? ld_vec(wr + k) : zero_vec<T>();
+                }
+            };
+            int64_t k0 = kb;
+            if (k0 < ke) load(k0, av, bv);
+            while (k0 < ke) {
+                const int64_t k1 = k0 + GROUP;
+                if (k1 < ke) load(k1, an, bn_);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc = MF::run(*reinterpret_cast<const op_t *>(&av[j].u), *reinterpret_cast<const op_t *>(&bv[j].u), acc);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    av[j] = an[j];
+                    bv[j] = bn_[j];
+                }
+                k0 = k1;
+            }
+            // 16x16 accumulator: lane holds column (lane % 16), rows 4 * (lane / 16) + e
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part[lam][4 * grp + e][row] = acc[e];
+        }
+        __syncthreads();
+        for (int idx = tid; idx < 16 * kSkinnyTN; idx += kWave * P) {
+            const int m = idx / kSkinnyTN, c = idx % kSkinnyTN;
+            const int64_t nn = n0 + c;
+            if (m < a.M && nn < a.Nc) {
+                const float v = ((part[0][m][c] + part[1][m][c]) + part[2][m][c]) + part[3][m][c];
+                const int64_t off = m * a.ldy + nn;
+                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off) : 0.0f;
+                st_f(Y + off, epilogue_apply(a.epi, v, nn, res));
+            }
+        }
+        __syncthreads();
+    }
+}
+
+template <class T>
+static void skinny_table(const void *out[3]) {
+    out[0] = reinterpret_cast<const void *>(&skinny_kernel<T, 1>);
+    out[1] = reinterpret_cast<const void *>(&skinny_kernel<T, 2>);
+    out[2] = reinterpret_cast<const void *>(&skinny_kernel<T, 4>);
+}
+
+int skinny_kernels(int dtype, const void *out[3]) {
+    switch (dtype) {
+    case 1: skinny_table<half_t>(out); return 0;
+    case 2: skinny_table<bf16_t>(out); return 0;
+    default: return -1;
+    }
+}
+
+}  // namespace miriam

@@ -40,7 +40,9 @@ static int get_igemm_table(int dtype, int cfg, int lay, const void *out[3], int 
     }
 }
 
-static int tile_dim(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : 128); }
+static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : 128); }
+static int tile_n_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 || cfg == CFG_128x64 ? 64 : 128); }
+constexpr int TILE_SKINNY = 5;  // descriptor tile code of the split-K skinny kernel
 
 // Fill the per-physical-block residency of the op's kernels.  Without a device
 // the figures stay 0 ("unknown"); the error state of the runtime is cleared.
@@ -81,11 +83,15 @@ static int check_epi(const miriam_op_desc &d) {
     return MIRIAM_OK;
 }
 
-// Contraction tile choice: the largest tile that still gives at least one tile
-// per compute unit; small problems fall back to 32x32 tiles.
+// Contraction tile choice: the largest tile that still yields about one tile per
+// compute unit (3/4 of them); a 128-row tile keeps 64 columns when N <= 64.
 static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
-    const int64_t want = 256;
-    if (batch * cdiv(M, 128) * cdiv(N, 128) >= want) return CFG_128;
+    const int64_t want = 192;
+    if (N <= 64) {
+        if (batch * cdiv(M, 128) >= want) return CFG_128x64;
+    } else if (batch * cdiv(M, 128) * cdiv(N, 128) >= want) {
+        return CFG_128;
+    }
     if (batch * cdiv(M, 64) * cdiv(N, 64) >= want) return CFG_64;
     return CFG_32;
 }
@@ -152,19 +158,36 @@ static int create_igemm(miriam_op *op) {
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.Nc);
 
+    a.vec_store = (a.ldy % V == 0) && (a.sy0 % V == 0) && (a.sy1 % V == 0) && aligned16(d.y) &&
+                  (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
+    // fully connected layers at small batch: split-K skinny kernel
+    const bool skinny_ok = d.kind == MIRIAM_OP_GEMM && d.dtype != MIRIAM_F32 && a.M <= 16 && a_vec && b_vec;
     int cfg = d.tile;
-    if (cfg == 0) cfg = choose_cfg(batch, a.M, a.Nc);
-    if (cfg < CFG_32 || cfg > CFG_128) return einval("unknown tile configuration");
-    const int td = tile_dim(cfg);
-    a.mT = cdiv(a.M, td);
-    a.nT = cdiv(a.Nc, td);
-    op->T = batch * a.mT * a.nT;
-    op->cfg = cfg;
-    op->tile_m = op->tile_n = td;
-    if (nmaj) op->lay = (a_vec && b_vec) ? LAY_VEC_NB : LAY_SCALAR_NB;
-    else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
-    if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
-        return einval("no kernel for this dtype / layout");
+    if (cfg == 0) cfg = skinny_ok ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
+    if (cfg == TILE_SKINNY) {
+        if (!skinny_ok) return einval("skinny tile needs an fp16/bf16 GEMM with m <= 16 and 16-byte rows");
+        op->family = FAM_SKINNY;
+        a.mT = 1;
+        a.nT = cdiv(a.Nc, 16);
+        op->T = a.nT;
+        op->cfg = cfg;
+        op->tile_m = op->tile_n = 16;
+        op->lay = LAY_VEC;
+        op->lds_bytes = 4 * 16 * 17 * 4;
+        if (skinny_kernels(d.dtype, op->kern) != 0) return einval("no skinny kernel for this dtype");
+    } else {
+        if (cfg < CFG_32 || cfg > CFG_128x64) return einval("unknown tile configuration");
+        a.mT = cdiv(a.M, tile_m_of(cfg));
+        a.nT = cdiv(a.Nc, tile_n_of(cfg));
+        op->T = batch * a.mT * a.nT;
+        op->cfg = cfg;
+        op->tile_m = tile_m_of(cfg);
+        op->tile_n = tile_n_of(cfg);
+        if (nmaj) op->lay = (a_vec && b_vec) ? LAY_VEC_NB : LAY_SCALAR_NB;
+        else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
+        if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
+            return einval("no kernel for this dtype / layout");
+    }
     op->flops = 2.0 * (double)batch * (double)a.M * (double)a.Nc * (double)a.K;
     const double xin = d.kind == MIRIAM_OP_CONV2D ? (double)d.n * d.h * d.w * d.c : (double)batch * a.M * a.K;
     const double win = (d.kind == MIRIAM_OP_BGEMM ? (double)batch : 1.0) * (double)a.Nc * a.K;
@@ -278,7 +301,8 @@ int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hi
     Shard sh{b, l, owner_wg, owner_iter, count};
     void *args[2];
     switch (op->family) {
-    case FAM_IGEMM: args[0] = const_cast<IgemmArgs *>(&op->ig); break;
+    case FAM_IGEMM:
+    case FAM_SKINNY: args[0] = const_cast<IgemmArgs *>(&op->ig); break;
     case FAM_PIX: args[0] = const_cast<PixArgs *>(&op->px); break;
     default: args[0] = const_cast<RowArgs *>(&op->rw); break;
     }
@@ -369,8 +393,9 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
     out->num_tiles = op->T;
     out->logical_block = kLogicalBlock;
     out->lds_bytes = op->lds_bytes;
-    out->tile_m = op->family == FAM_IGEMM ? op->tile_m : 0;
-    out->tile_n = op->family == FAM_IGEMM ? op->tile_n : 0;
+    const bool contraction = op->family == FAM_IGEMM || op->family == FAM_SKINNY;
+    out->tile_m = contraction ? op->tile_m : 0;
+    out->tile_n = contraction ? op->tile_n : 0;
     for (int i = 0; i < 3; ++i) out->max_wg_per_cu[i] = op->max_wg_per_cu[i];
     out->flops = op->flops;
     out->bytes = op->bytes;

@@ -46,7 +46,7 @@ def test_conv_cfg1_matches_oracle(ops, orc):
     assert err <= RTOL["f32"]
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4])
 def test_conv_cfg1_bitwise_across_elastic_configs(ops, orc, tile):
     op, y, _ = _cfg1(ops, tile=tile)
     op.run()
@@ -137,7 +137,7 @@ def test_conv_shapes_match_oracle(ops, orc, dtype, case):
     if "res" in epi:
         res, r64 = rand((N, Ho, Wo, K), dtype, seed=seed + 3)
     y = empty((N, Ho, Wo, K), dtype)
-    for tile in [1, 2, 3]:
+    for tile in [1, 2, 3, 4]:
         y.fill_(float("nan"))
         op = ops.conv2d(x, w, y, stride=s, pad=p, bias=bias, bn=bn, residual=res, act=act, tile=tile)
         op.run()

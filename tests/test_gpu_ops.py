@@ -46,6 +46,8 @@ GEMM_CASES = [
     (128, 3072, 768, "bias", "gelu"),        # FFN up-projection
     (128, 768, 3072, "bias_res", "none"),    # FFN down-projection + residual
     (77, 45, 33, "bias", "relu"),            # ragged everything, K not a vector multiple
+    (16, 1000, 1280, "bias", "none"),        # MobileNetV2 classifier at batch 16
+    (3, 77, 200, "bias_res", "relu"),        # skinny with ragged N and a K tail
 ]
 
 
@@ -63,7 +65,10 @@ def test_gemm_matches_oracle(ops, orc, dtype, case):
         res, r64 = rand((M, N), dtype, seed + 3)
     y = empty((M, N), dtype)
     ref = orc.linear(x64, w64, bias=b64, residual=r64, act=act)
-    for tile in [1, 2, 3]:
+    tiles = [0, 1, 2, 3, 4]
+    if M <= 16 and dtype != "f32" and K % 8 == 0:
+        tiles.append(5)  # split-K skinny kernel
+    for tile in tiles:
         y.fill_(float("nan"))
         op = ops.gemm(x, w, y, bias=bias, residual=res, act=act, tile=tile)
         op.run()
