@@ -248,6 +248,41 @@ def cpu_baseline(net_name, kw, budget_macs=1.5e9, seed=0):
                        f"{wall:.1f} s of CPU work, single thread")
 
 
+def profile_op(args, cfg):
+    """One layer's unsharded launch --reps times, then a plain device copy of 256 MiB
+    --reps times (its FETCH_SIZE / WRITE_SIZE calibrate the traffic counters)."""
+    import torch
+    from paper_2307_04339_amd import models
+    net_name, layer_name = args.profile_op.split(".", 1)
+    kw = next((dict(k) for (n, k) in [cfg["crit"]] + cfg["be"] if n == net_name), None)
+    if kw is None:
+        raise SystemExit(f"{net_name} is not part of workload {args.config}")
+    net = models.BUILDERS[net_name](dtype=cfg["dtype"], **kw)
+    layer = next(l for l in net.layers if l.name == layer_name)
+    src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.reps):
+        layer.op.run()
+    e1.record()
+    e1.synchronize()
+    us = 1000.0 * e0.elapsed_time(e1) / args.reps
+    e0.record()
+    for _ in range(args.reps):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    cus = 1000.0 * e0.elapsed_time(e1) / args.reps
+    info = layer.op.info
+    print(json.dumps({"op": args.profile_op, "reps": args.reps, "avg_us": round(us, 3),
+                      "tiles": layer.op.T, "tile": [info.tile_m, info.tile_n],
+                      "flops": info.flops, "bytes": info.bytes,
+                      "copy_bytes_each_way": src.numel() * 4, "copy_avg_us": round(cus, 3)}), flush=True)
+
+
 # ------------------------------------------------------------------- main
 def main():
     ap = argparse.ArgumentParser()
@@ -260,6 +295,9 @@ def main():
     ap.add_argument("--depth", type=int, default=1)
     ap.add_argument("--phases", default="kernels,solo,sequential,elastic")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
+                    help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
+                         "--reps times as the counter calibration kernel (for rocprofv3 runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
@@ -274,6 +312,9 @@ def main():
 
     cfg = CONFIGS[args.config]
     dtype = cfg["dtype"]
+    if args.profile_op:
+        profile_op(args, cfg)
+        return
     dev = device_info()
     log(f"device {dev.arch.decode()} cus={dev.n_cu} config={args.config}")
     cname, ckw = cfg["crit"]

@@ -1,0 +1,330 @@
+// Pipelined variant of the elastic contraction kernel for 16-byte aligned, K-major
+// operands (the common case: NHWC convolutions with C a multiple of 8 elements,
+// fully connected layers, attention scores).
+//
+// Operands go straight from global memory into LDS with global_load_lds_dwordx4
+// (no register staging) through a ring of S K-chunks (double buffered: the next
+// chunk is in flight while one is multiplied, and two workgroups fit per CU).  An LDS row holds one 128-byte K-chunk of one
+// tile row; its eight 16-byte pieces are stored XOR-swizzled (piece c of row r
+// sits at slot c ^ ((r >> 1) & 7)), which keeps the MFMA operand reads of 32
+// consecutive rows free of bank conflicts without padding (each load instruction
+// writes 1024 contiguous LDS bytes).  Padded taps and out-of-range rows load from
+// a zero-filled device block.
+//
+// The arithmetic is exactly the one of igemm_kernel: same tile, same 2x2 logical
+// waves, same MFMA opcode and K order, same staged epilogue; only how operands
+// reach LDS differs.  Results are therefore bit-identical for every shard plan,
+// grid and physical block.
+#pragma once
+
+#include "igemm.h"
+
+namespace miriam {
+
+// 16-byte zero source for lanes whose element lies in the padding or past a bound.
+static __device__ __attribute__((aligned(64))) uint32_t g_zero_src[16];
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 s_waitcnt: vmcnt bits [3:0] and [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at max
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <class T, int TM, int TN, int MS, int P>
+struct DmaKernel {
+    typedef Mfma<T, MS> MF;
+    static constexpr int NT = kWave * P;
+    static constexpr int VEC = 16 / (int)sizeof(T);
+    static constexpr int KT = 128 / (int)sizeof(T);      // one 128-byte row per chunk
+    static constexpr int KSTEP = (kWave / MS) * MF::KPL;
+    static constexpr int S = 2;                          // stages: double buffer keeps 2 workgroups per CU
+    static constexpr int NIA = TM / 8 / P;               // A load instructions per wave per chunk
+    static constexpr int NIB = TN / 8 / P;
+    static constexpr int LPC = NIA + NIB;
+    static constexpr int BM = TM / 2 / MS, BN = TN / 2 / MS;
+    static constexpr int LW = kLogicalWaves / P;
+    static constexpr int MAXACC = P == 1 ? 64 : 128;
+    static constexpr int MAXSL = (MAXACC / MF::NACC) / (BM * BN) > 0 ? (MAXACC / MF::NACC) / (BM * BN) : 1;
+    static constexpr int SL = LW < MAXSL ? LW : MAXSL;
+    static constexpr int ROUNDS = LW / SL;
+    static constexpr int STAGE = (TM + TN) * 128;        // bytes per stage
+    static constexpr int LDC = TN + 4;
+    static constexpr int C_BYTES = TM * LDC * 4;
+    static constexpr int LDS_BYTES = S * STAGE > C_BYTES ? S * STAGE : C_BYTES;
+    static_assert(TM % (8 * P) == 0 && TN % (8 * P) == 0, "load instructions must divide evenly");
+    static_assert((S - 2) * LPC < 64, "vmcnt range");
+    static_assert(LW % SL == 0, "slots must divide logical waves");
+    static_assert(KT % KSTEP == 0, "chunk must hold whole MFMA steps");
+};
+
+template <class T, int TM, int TN, int MS, int P>
+__global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard sh) {
+    typedef DmaKernel<T, TM, TN, MS, P> K_;
+    typedef typename K_::MF MF;
+    typedef typename MF::op_t op_t;
+    typedef typename MF::acc_t acc_t;
+    constexpr int NT = K_::NT, VEC = K_::VEC, KT = K_::KT, KSTEP = K_::KSTEP, S = K_::S;
+    constexpr int NIA = K_::NIA, NIB = K_::NIB, LPC = K_::LPC;
+    constexpr int BM = K_::BM, BN = K_::BN, SL = K_::SL, ROUNDS = K_::ROUNDS, LDC = K_::LDC;
+
+    __shared__ __attribute__((aligned(1024))) char smem_[K_::LDS_BYTES];
+    char *const smem = smem_;
+    float *const Cs = reinterpret_cast<float *>(smem_);
+
+    const int tid = threadIdx.x;
+    const int pw = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave;
+    const T *__restrict__ X = static_cast<const T *>(a.x);
+    const T *__restrict__ Wt = static_cast<const T *>(a.w);
+    T *__restrict__ Y = static_cast<T *>(a.y);
+    const T *__restrict__ R = static_cast<const T *>(a.res);
+    const T *const zsrc = reinterpret_cast<const T *>(g_zero_src);
+    const int64_t HoWo = a.Ho * a.Wo;
+    const int nch = (int)((a.K + KT - 1) / KT);
+    const int64_t G = gridDim.x;
+    const int64_t rank = wg_rank(blockIdx.x, G);
+    const int32_t C32 = (int32_t)a.C, KW32 = a.KW, KH32 = a.KH, H32 = (int32_t)a.H, W32 = (int32_t)a.W;
+    // this lane's place in every load instruction: row offset in the 8-row group, slot
+    const int lrow = lane >> 3, slot = lane & 7;
+
+    int iter = 0;
+    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+        trace_tile(sh, t, iter);
+        const int64_t per = a.mT * a.nT;
+        const int64_t bi = t / per;
+        const int64_t rem = t - bi * per;
+        const int64_t mt = rem / a.nT, nt = rem - (rem / a.nT) * a.nT;
+        const int64_t b0 = bi / a.bdiv, b1 = bi - b0 * a.bdiv;
+        const T *Xb = X + b0 * a.sx0 + b1 * a.sx1;
+        const T *Wb = Wt + b0 * a.sw0 + b1 * a.sw1;
+        const int64_t yoff = b0 * a.sy0 + b1 * a.sy1;
+        const int64_t m0 = mt * TM, n0 = nt * TN;
+
+        // A instruction j of this wave covers tile rows 8q..8q+7, q = j*P + pw
+        const T *a_base[NIA];
+        int32_t a_h0[NIA], a_w0[NIA];
+        int32_t a_kr0[NIA], a_ks0[NIA], a_kc0[NIA];
+        bool a_ok[NIA];
+#pragma unroll
+        for (int j = 0; j < NIA; ++j) {
+            const int row = 8 * (j * P + pw) + lrow;
+            const int64_t m = m0 + row;
+            a_ok[j] = m < a.M;
+            const int64_t mm = a_ok[j] ? m : 0;
+            const int64_t img = mm / HoWo;
+            const int64_t pq = mm - img * HoWo;
+            const int64_t p = pq / a.Wo, q = pq - (pq / a.Wo) * a.Wo;
+            a_base[j] = Xb + img * a.img_x;
+            a_h0[j] = (int32_t)(p * a.stride - a.pad);
+            a_w0[j] = (int32_t)(q * a.stride - a.pad);
+            const int32_t k = ((slot ^ ((row >> 1) & 7)) * VEC);  // logical 16-byte piece of this slot
+            a_kc0[j] = k % C32;
+            const int32_t tap = k / C32;
+            a_ks0[j] = tap % KW32;
+            a_kr0[j] = tap / KW32;
+        }
+        const T *b_base[NIB];
+        int32_t b_k0[NIB];
+        bool b_ok[NIB];
+#pragma unroll
+        for (int j = 0; j < NIB; ++j) {
+            const int row = 8 * (j * P + pw) + lrow;
+            const int64_t n = n0 + row;
+            b_ok[j] = n < a.Nc;
+            b_base[j] = Wb + (b_ok[j] ? n : 0) * a.ldw;
+            b_k0[j] = (slot ^ ((row >> 1) & 7)) * VEC;
+        }
+
+        for (int rd = 0; rd < ROUNDS; ++rd) {
+            acc_t acc[SL][BM][BN];
+#pragma unroll
+            for (int s = 0; s < SL; ++s)
+#pragma unroll
+                for (int i = 0; i < BM; ++i)
+#pragma unroll
+                    for (int jn = 0; jn < BN; ++jn)
+#pragma unroll
+                        for (int e = 0; e < MF::NACC; ++e) acc[s][i][jn][e] = 0.0f;
+
+            int32_t kr[NIA], ks[NIA], kc[NIA];
+#pragma unroll
+            for (int j = 0; j < NIA; ++j) {
+                kr[j] = a_kr0[j];
+                ks[j] = a_ks0[j];
+                kc[j] = a_kc0[j];
+            }
+
+            // issue chunk ch into stage st (all lanes issue every instruction)
+            auto issue = [&](int ch, int st) {
+                char *stage = smem + st * K_::STAGE;
+#pragma unroll
+                for (int j = 0; j < NIA; ++j) {
+                    const int32_t h = a_h0[j] + kr[j], w = a_w0[j] + ks[j];
+                    const bool ok = a_ok[j] && kr[j] < KH32 && h >= 0 && h < H32 && w >= 0 && w < W32;
+                    const T *src = ok ? a_base[j] + ((int64_t)h * a.W + w) * a.ldx + kc[j] : zsrc;
+                    char *dst = stage + (8 * (j * P + pw)) * 128;
+                    __builtin_amdgcn_global_load_lds((const void *)(src), (__attribute__((address_space(3))) void *)(dst), 16, 0, 0);
+                    kc[j] += KT;
+                    while (kc[j] >= C32) {
+                        kc[j] -= C32;
+                        if (++ks[j] == KW32) { ks[j] = 0; ++kr[j]; }
+                    }
+                }
+                const int64_t k0 = (int64_t)ch * KT;
+#pragma unroll
+                for (int j = 0; j < NIB; ++j) {
+                    const int64_t k = k0 + b_k0[j];
+                    const T *src = (b_ok[j] && k < a.K) ? b_base[j] + k : zsrc;
+                    char *dst = stage + (TM + 8 * (j * P + pw)) * 128;
+                    __builtin_amdgcn_global_load_lds((const void *)(src), (__attribute__((address_space(3))) void *)(dst), 16, 0, 0);
+                }
+            };
+
+            auto compute = [&](int st) {
+                const char *stage = smem + st * K_::STAGE;
+                constexpr int NK = KT / KSTEP;
+                // read every operand of the chunk first, so LDS latency overlaps the MFMAs
+                op_t aop[NK][SL][BM], bop[NK][SL][BN];
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) {
+                    const int kcol = kk * KSTEP + (lane / MS) * MF::KPL;
+                    const int piece = kcol / VEC, within = (kcol % VEC) * (int)sizeof(T);
+#pragma unroll
+                    for (int s = 0; s < SL; ++s) {
+                        const int lam = (rd * SL + s) * P + pw;
+                        const int wm = lam >> 1, wn = lam & 1;
+#pragma unroll
+                        for (int jn = 0; jn < BN; ++jn) {
+                            const int row = wn * (TN / 2) + jn * MS + lane % MS;
+                            bop[kk][s][jn] = *reinterpret_cast<const op_t *>(
+                                stage + (TM + row) * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
+                        }
+#pragma unroll
+                        for (int i = 0; i < BM; ++i) {
+                            const int row = wm * (TM / 2) + i * MS + lane % MS;
+                            aop[kk][s][i] = *reinterpret_cast<const op_t *>(
+                                stage + row * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
+                        }
+                    }
+                }
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+                    for (int s = 0; s < SL; ++s)
+#pragma unroll
+                        for (int i = 0; i < BM; ++i)
+#pragma unroll
+                            for (int jn = 0; jn < BN; ++jn)
+                                acc[s][i][jn] = MF::run(aop[kk][s][i], bop[kk][s][jn], acc[s][i][jn]);
+                // schedule: operand reads run two MFMA steps ahead of the MFMAs that use them
+                constexpr int RD = SL * (BM + BN), MM = SL * BM * BN;
+                __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+                if constexpr (NK > 1) __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, MM, 0);
+                    if (kk + 2 < NK) __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+                }
+            };
+
+#pragma unroll
+            for (int st = 0; st < S - 1; ++st)
+                if (st < nch) issue(st, st);
+            for (int c = 0; c < nch; ++c) {
+                // chunks issued after c and still allowed in flight: c+1 .. min(c+S-2, nch-1)
+                const int pending = (nch - 1 - c) < (S - 2) ? (nch - 1 - c) : (S - 2);
+                if constexpr (S - 2 >= 2) {
+                    if (pending >= 2) wait_vmcnt<2 * LPC>();
+                    else if (pending == 1) wait_vmcnt<LPC>();
+                    else wait_vmcnt<0>();
+                } else if constexpr (S - 2 == 1) {
+                    if (pending >= 1) wait_vmcnt<LPC>();
+                    else wait_vmcnt<0>();
+                } else {
+                    (void)pending;
+                    wait_vmcnt<0>();
+                }
+                __syncthreads();
+                if (c + S - 1 < nch) issue(c + S - 1, (c + S - 1) % S);
+                compute(c % S);
+            }
+            __syncthreads();
+
+            // ---- epilogue, stage 1: accumulators (+ bias, BN) -> LDS as fp32
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                const int lam = (rd * SL + s) * P + pw;
+                const int wm = lam >> 1, wn = lam & 1;
+#pragma unroll
+                for (int i = 0; i < BM; ++i)
+#pragma unroll
+                    for (int jn = 0; jn < BN; ++jn) {
+                        const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                        const int64_t n = n0 + col;
+                        const ChanParams cp = chan_params(a.epi, n < a.Nc ? n : 0);
+#pragma unroll
+                        for (int e = 0; e < MF::NACC; ++e) {
+                            const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
+                            const int row = wm * (TM / 2) + i * MS + rr;
+                            Cs[row * LDC + col] = epilogue_pre(a.epi, cp, acc[s][i][jn][e]);
+                        }
+                    }
+            }
+            __syncthreads();
+            // ---- stage 2: + residual, activation, one rounding, coalesced row stores
+            {
+                constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
+                const int lam0 = rd * SL * P;
+                for (int idx = tid; idx < SL * P * SUBR * CV; idx += NT) {
+                    const int sub = idx / (SUBR * CV);
+                    const int rem2 = idx - sub * (SUBR * CV);
+                    const int r = rem2 / CV, cv = rem2 - (rem2 / CV) * CV;
+                    const int lam = lam0 + sub;
+                    const int row = (lam >> 1) * SUBR + r, col = (lam & 1) * SUBC + cv * VEC;
+                    const int64_t m = m0 + row, n = n0 + col;
+                    if (m >= a.M) continue;
+                    const float *cr = Cs + row * LDC + col;
+                    const int64_t off = yoff + m * a.ldy + n;
+                    if (a.vec_store && n + VEC <= a.Nc) {
+                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
+                        Vec16<T> o;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, cr[e], TypeOps<T>::to_f(rv.e[e])));
+                        st_vec(Y + off, o);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (n + e < a.Nc) {
+                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
+                                st_f(Y + off + e, epilogue_post(a.epi, cr[e], res));
+                            }
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+template <class T, int TM, int TN, int MS>
+inline void igemm_dma_table(const void *out[3], int *lds) {
+    out[0] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 1>);
+    out[1] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 2>);
+    out[2] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 4>);
+    *lds = DmaKernel<T, TM, TN, MS, 4>::LDS_BYTES;
+}
+
+template <class T>
+inline int igemm_dma_table_cfg(int cfg, const void *out[3], int *lds) {
+    switch (cfg) {
+    case CFG_32: igemm_dma_table<T, 32, 32, 16>(out, lds); return 0;
+    case CFG_64: igemm_dma_table<T, 64, 64, 32>(out, lds); return 0;
+    case CFG_128: igemm_dma_table<T, 128, 128, 32>(out, lds); return 0;
+    case CFG_128x64: igemm_dma_table<T, 128, 64, 32>(out, lds); return 0;
+    default: return -1;
+    }
+}
+
+}  // namespace miriam

@@ -1,11 +1,11 @@
 // Kernel table of the elastic contraction kernel for f16 operands (one translation unit
 // per element type keeps the build parallel).
-#include "igemm.h"
+#include "igemm_dma.h"
 
 namespace miriam {
 int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds) {
     switch (lay) {
-    case LAY_VEC: return igemm_table_cfg<half_t, LAY_VEC>(cfg, out, lds);
+    case LAY_VEC: return igemm_dma_table_cfg<half_t>(cfg, out, lds);
     case LAY_SCALAR: return igemm_table_cfg<half_t, LAY_SCALAR>(cfg, out, lds);
     case LAY_VEC_NB: return igemm_table_cfg<half_t, LAY_VEC_NB>(cfg, out, lds);
     case LAY_SCALAR_NB: return igemm_table_cfg<half_t, LAY_SCALAR_NB>(cfg, out, lds);

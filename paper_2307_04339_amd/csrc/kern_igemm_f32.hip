@@ -1,11 +1,11 @@
 // Kernel table of the elastic contraction kernel for f32 operands (one translation unit
 // per element type keeps the build parallel).
-#include "igemm.h"
+#include "igemm_dma.h"
 
 namespace miriam {
 int igemm_kernels_f32(int cfg, int lay, const void *out[3], int *lds) {
     switch (lay) {
-    case LAY_VEC: return igemm_table_cfg<float, LAY_VEC>(cfg, out, lds);
+    case LAY_VEC: return igemm_dma_table_cfg<float>(cfg, out, lds);
     case LAY_SCALAR: return igemm_table_cfg<float, LAY_SCALAR>(cfg, out, lds);
     default: return -1;
     }
