@@ -74,7 +74,11 @@ def time_layers(net, reps, flush):
             e1.synchronize()
             total += e0.elapsed_time(e1)
         us = 1000.0 * total / reps
-        out.append(dict(name=layer.name, us=us, flops=layer.op.info.flops, bytes=layer.op.info.bytes,
+        flops = layer.op.info.flops
+        if layer.kind == "conv" and layer.params.get("logical_c"):
+            # an image stored with zero channels appended: count the logical convolution only
+            flops *= layer.params["logical_c"] / layer.t["x"].shape[-1]
+        out.append(dict(name=layer.name, us=us, flops=flops, bytes=layer.op.info.bytes,
                         tiles=layer.op.T))
     return out
 
@@ -211,8 +215,13 @@ def cpu_baseline(net_name, kw, budget_macs=1.5e9, seed=0):
     net = models.BUILDERS[net_name](**dict(kw, batch=1))
     for l in net.layers:
         x = l.t.get("x")
-        shapes.append((l.kind, None if x is None else tuple(x.shape), l.t["y"].shape,
-                       None if l.t.get("w") is None else tuple(l.t["w"].shape), dict(l.params)))
+        xs = None if x is None else tuple(x.shape)
+        ws = None if l.t.get("w") is None else tuple(l.t["w"].shape)
+        if l.kind == "conv" and l.params.get("logical_c"):
+            lc = l.params["logical_c"]  # the oracle convolves the logical channels only
+            xs = xs[:-1] + (lc,)
+            ws = ws[:-1] + (lc,)
+        shapes.append((l.kind, xs, l.t["y"].shape, ws, dict(l.params)))
     del net
     total = 0.0
     t_start = time.time()
@@ -287,13 +296,14 @@ def profile_op(args, cfg):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=sorted(CONFIGS))
     ap.add_argument("--reps", type=int, default=20, help="repetitions per kernel timing")
     ap.add_argument("--quantum-us", type=float, default=40.0)
-    ap.add_argument("--depth", type=int, default=1)
-    ap.add_argument("--phases", default="kernels,solo,sequential,elastic")
+    ap.add_argument("--depth", type=int, default=4)
+    ap.add_argument("--inflight-us", type=float, default=100.0)
+    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
                     help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
@@ -356,7 +366,8 @@ def main():
     del flush
     torch.cuda.empty_cache()
 
-    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, profile_reps=3)
+    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
+                profile_reps=3)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "elastic"):
         if ph not in phases:
@@ -387,7 +398,8 @@ def main():
         "config": {"workload": args.config,
                    "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
-                   "quantum_us": args.quantum_us, "inflight_depth": args.depth},
+                   "quantum_us": args.quantum_us, "inflight_depth": args.depth,
+                   "inflight_us": args.inflight_us},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

@@ -225,6 +225,8 @@ typedef struct miriam_config {
     double max_blk_frac;     /* Eq. (5) MAX_blk as a fraction of the unsharded time (0.1) */
     double max_pt_frac;      /* Eq. (5) MAX_pt as a fraction of the unsharded time (0.1) */
     double quantum_us;       /* target duration of one normal shard */
+    double inflight_us;      /* normal work (estimated from the task profile) kept queued per
+                                normal stream; 0 = bounded by inflight_depth only */
     int32_t log_launches;    /* keep miriam_launch_record entries (diagnostics, tests) */
     int32_t profile_reps;    /* timed repetitions per op when a task is created (HIP backend) */
     /* FAKE backend only: simulated compute units, WG slots per CU, ns per tile, launch ns */

@@ -68,7 +68,7 @@ class Config(ctypes.Structure):
         ("policy", ctypes.c_int32), ("backend", ctypes.c_int32), ("n_be_streams", ctypes.c_int32),
         ("inflight_depth", ctypes.c_int32), ("top_frac", ctypes.c_double),
         ("max_blk_frac", ctypes.c_double), ("max_pt_frac", ctypes.c_double),
-        ("quantum_us", ctypes.c_double),
+        ("quantum_us", ctypes.c_double), ("inflight_us", ctypes.c_double),
         ("log_launches", ctypes.c_int32), ("profile_reps", ctypes.c_int32),
         ("fake_n_cu", ctypes.c_int32), ("fake_slots_per_cu", ctypes.c_int32),
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),

@@ -246,6 +246,7 @@ namespace {
 struct Shot {  // one launch in flight
     int ev;
     int op;
+    double est_us;  // estimated duration (task profile), counted against cfg.inflight_us
 };
 
 struct Req {
@@ -295,6 +296,7 @@ struct Coord {
     std::deque<Req *> crit_active;                 // launched critical requests, stream 0
     std::vector<std::deque<Req *>> be_active;      // per stream, launched normal requests
     std::vector<int> inflight;                     // shards in flight per stream
+    std::vector<double> inflight_us;               // their estimated duration per stream
     int rr_stream = 1;
 
     std::mutex log_mu;
@@ -332,16 +334,17 @@ void log_launch(Coord &c, const Req *r, int op_index, int stream, int grid, int 
 
 // Launch shard [b, b+l) of op `oi` of request r on `stream` and record its event.
 int issue(Coord &c, Req *r, int oi, int64_t b, int64_t l, int grid, int block, int stream, bool crit_busy,
-          int64_t limit) {
+          int64_t limit, double est_us = 0.0) {
     const miriam_op *op = r->task->ops[oi];
     int rc = c.be->launch(op, b, l, grid, block, stream);
     if (rc != MIRIAM_OK) return rc;
     int ev = c.be->record(stream);
     if (ev < 0) return ev;
     if (r->t_start == 0) r->t_start = mono_ns();
-    r->shots.push_back({ev, oi});
+    r->shots.push_back({ev, oi, est_us});
     r->n_shards++;
     c.inflight[stream]++;
+    c.inflight_us[stream] += est_us;
     log_launch(c, r, oi, stream, grid, block, crit_busy, b, l, op->T, limit);
     std::lock_guard<std::mutex> lk(c.stat_mu);
     c.stats.launches++;
@@ -400,6 +403,8 @@ bool retire(Coord &c, std::deque<Req *> &active, int stream) {
             if (q == 0) break;
             if (q < 0) r->status = q;
             c.be->release(r->shots.front().ev);
+            c.inflight_us[stream] -= r->shots.front().est_us;
+            if (c.inflight_us[stream] < 1e-9) c.inflight_us[stream] = 0.0;
             r->shots.pop_front();
             c.inflight[stream]--;
             any = true;
@@ -428,6 +433,7 @@ int current_critical_op(Coord &c, const miriam_op **op) {
 struct Decision {
     int grid, block;
     int64_t len, limit;
+    double est_us;  // estimated duration of the shard
 };
 
 // §6.3 + §7: size the next shard of op `oi` of normal request r.
@@ -435,7 +441,7 @@ Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
     const miriam_op *op = r->task->ops[r->op];
     const OpProf &pf = r->task->prof[r->op];
     const int64_t T = op->T, cursor = r->cursor, remain = T - cursor;
-    Decision d{0, 256, 0, 0};
+    Decision d{0, 256, 0, 0, 0.0};
     int bi = 2;
     if (crit_op) {
         const int64_t n_rt = crit_op->T;  // critical kernels run unsharded: one workgroup per tile
@@ -491,13 +497,17 @@ Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
     if (len < 1) len = std::min<int64_t>(remain, max_len);
     d.len = len;
     d.grid = (int)std::max<int64_t>(1, std::min<int64_t>(d.grid, len));
+    // estimated duration: the larger of the op's unsharded rate and the persistent rounds
+    const double waves = (double)((len + d.grid - 1) / d.grid);
+    d.est_us = std::max(pf.t_unsh_us * (double)len / (double)T, waves * pf.tau1_us[bi]);
     return d;
 }
 
 // Issue shards for the normal requests of one stream while its in-flight budget lasts.
 bool pump_normal(Coord &c, int s) {
     bool any = false;
-    while (c.inflight[s] < c.cfg.inflight_depth) {
+    while (c.inflight[s] < c.cfg.inflight_depth &&
+           (c.cfg.inflight_us <= 0.0 || c.inflight[s] == 0 || c.inflight_us[s] < c.cfg.inflight_us)) {
         Req *r = nullptr;
         for (Req *q : c.be_active[s])
             if (!q->launched_all) {
@@ -516,7 +526,7 @@ bool pump_normal(Coord &c, int s) {
         Decision d = decide(c, r, busy ? crit_op : nullptr);
         const int64_t t1 = mono_ns();
         const int oi = (int)r->op;
-        int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit);
+        int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit, d.est_us);
         {
             std::lock_guard<std::mutex> lk(c.stat_mu);
             c.stats.decisions++;
@@ -701,7 +711,8 @@ int miriam_init(const miriam_config *cfg) {
     }
     if (cfg->policy < 0 || cfg->policy > 2 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
-        !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0) {
+        !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
+        cfg->inflight_us < 0.0) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -742,6 +753,7 @@ int miriam_init(const miriam_config *cfg) {
     c->norm_ready.resize(c->n_streams);
     c->be_active.resize(c->n_streams);
     c->inflight.assign(c->n_streams, 0);
+    c->inflight_us.assign(c->n_streams, 0.0);
     g = c;
     c->th = std::thread(dispatcher, c);
     return MIRIAM_OK;

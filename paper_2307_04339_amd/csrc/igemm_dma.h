@@ -80,7 +80,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
     T *__restrict__ Y = static_cast<T *>(a.y);
     const T *__restrict__ R = static_cast<const T *>(a.res);
     const T *const zsrc = reinterpret_cast<const T *>(g_zero_src);
-    const int64_t HoWo = a.Ho * a.Wo;
+    const uint32_t HoWo32 = (uint32_t)(a.Ho * a.Wo), Wo32 = (uint32_t)a.Wo;
     const int nch = (int)((a.K + KT - 1) / KT);
     const int64_t G = gridDim.x;
     const int64_t rank = wg_rank(blockIdx.x, G);
@@ -91,15 +91,16 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
     int iter = 0;
     for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
         trace_tile(sh, t, iter);
-        const int64_t per = a.mT * a.nT;
-        const int64_t bi = t / per;
-        const int64_t rem = t - bi * per;
-        const int64_t mt = rem / a.nT, nt = rem - (rem / a.nT) * a.nT;
-        const int64_t b0 = bi / a.bdiv, b1 = bi - b0 * a.bdiv;
+        // tile id -> (batch, m tile, n tile); every index here is below 2^31 (checked at creation)
+        const uint32_t per = (uint32_t)(a.mT * a.nT), t32 = (uint32_t)t;
+        const uint32_t bi = t32 / per;
+        const uint32_t rem = t32 - bi * per;
+        const uint32_t mt = rem / (uint32_t)a.nT, nt = rem - mt * (uint32_t)a.nT;
+        const uint32_t b0 = bi / (uint32_t)a.bdiv, b1 = bi - b0 * (uint32_t)a.bdiv;
         const T *Xb = X + b0 * a.sx0 + b1 * a.sx1;
         const T *Wb = Wt + b0 * a.sw0 + b1 * a.sw1;
         const int64_t yoff = b0 * a.sy0 + b1 * a.sy1;
-        const int64_t m0 = mt * TM, n0 = nt * TN;
+        const int64_t m0 = (int64_t)mt * TM, n0 = (int64_t)nt * TN;
 
         // A instruction j of this wave covers tile rows 8q..8q+7, q = j*P + pw
         const T *a_base[NIA];
@@ -111,13 +112,13 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
             const int row = 8 * (j * P + pw) + lrow;
             const int64_t m = m0 + row;
             a_ok[j] = m < a.M;
-            const int64_t mm = a_ok[j] ? m : 0;
-            const int64_t img = mm / HoWo;
-            const int64_t pq = mm - img * HoWo;
-            const int64_t p = pq / a.Wo, q = pq - (pq / a.Wo) * a.Wo;
-            a_base[j] = Xb + img * a.img_x;
-            a_h0[j] = (int32_t)(p * a.stride - a.pad);
-            a_w0[j] = (int32_t)(q * a.stride - a.pad);
+            const uint32_t mm = a_ok[j] ? (uint32_t)m : 0u;
+            const uint32_t img = mm / HoWo32;
+            const uint32_t pq = mm - img * HoWo32;
+            const uint32_t p = pq / Wo32, q = pq - p * Wo32;
+            a_base[j] = Xb + (int64_t)img * a.img_x;
+            a_h0[j] = (int32_t)p * a.stride - a.pad;
+            a_w0[j] = (int32_t)q * a.stride - a.pad;
             const int32_t k = ((slot ^ ((row >> 1) & 7)) * VEC);  // logical 16-byte piece of this slot
             a_kc0[j] = k % C32;
             const int32_t tap = k / C32;

@@ -23,9 +23,11 @@ template <class T, int V, int KIND>
 __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
     const T *__restrict__ X = static_cast<const T *>(a.x);
     T *__restrict__ Y = static_cast<T *>(a.y);
-    const int64_t CV = a.C / V;
-    const int64_t pix = u / CV;
-    const int64_t c0 = (u - pix * CV) * V;
+    // item indices stay below 2^31 (checked at creation): 32-bit division
+    const uint32_t CV = (uint32_t)(a.C / V), u32 = (uint32_t)u;
+    const uint32_t pixu = u32 / CV;
+    const int64_t pix = pixu;
+    const int64_t c0 = (int64_t)(u32 - pixu * CV) * V;
     float acc[V];
     if constexpr (KIND == PIX_EW) {
         // pixel == row of C channels; elementwise epilogue
@@ -37,10 +39,10 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
             acc[e] = epilogue_apply(a.epi, ld_f(src + e), c0 + e, r);
         }
     } else {
-        const int64_t HoWo = a.Ho * a.Wo;
-        const int64_t n = pix / HoWo;
-        const int64_t pq = pix - n * HoWo;
-        const int64_t p = pq / a.Wo, q = pq - (pq / a.Wo) * a.Wo;
+        const uint32_t HoWo = (uint32_t)(a.Ho * a.Wo), Wo = (uint32_t)a.Wo;
+        const int64_t n = pixu / HoWo;
+        const uint32_t pq = pixu - (uint32_t)n * HoWo;
+        const int64_t p = pq / Wo, q = pq - (pq / Wo) * Wo;
         const int64_t h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[e] = (KIND == PIX_MAX) ? -INFINITY : 0.0f;

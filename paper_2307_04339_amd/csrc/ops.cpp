@@ -188,6 +188,9 @@ static int create_igemm(miriam_op *op) {
         if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
             return einval("no kernel for this dtype / layout");
     }
+    // kernels index tiles, rows and batch entries with 32-bit arithmetic
+    if (op->T >= (int64_t)INT32_MAX || a.M >= (int64_t)INT32_MAX || batch >= (int64_t)INT32_MAX)
+        return einval("contraction too large for 32-bit tile indexing");
     op->flops = 2.0 * (double)batch * (double)a.M * (double)a.Nc * (double)a.K;
     const double xin = d.kind == MIRIAM_OP_CONV2D ? (double)d.n * d.h * d.w * d.c : (double)batch * a.M * a.K;
     const double win = (d.kind == MIRIAM_OP_BGEMM ? (double)batch : 1.0) * (double)a.Nc * a.K;
@@ -232,6 +235,7 @@ static int create_pix(miriam_op *op) {
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.C);
     a.items = a.N * a.Ho * a.Wo * (a.C / v);
+    if (a.items >= (int64_t)INT32_MAX) return einval("pixel op too large for 32-bit item indexing");
     op->T = cdiv(a.items, 256);
     op->lds_bytes = 0;
     if (pix_kernels(d.dtype, kind, vec, op->kern) != 0) return einval("no kernel for this dtype");

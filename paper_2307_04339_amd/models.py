@@ -72,17 +72,25 @@ class Net:
         return layer.t["y"]
 
     # ------------------------------------------------------------ layers
-    def conv(self, x, K, k, stride, pad, bn=True, bias=False, act="relu", residual=None, name=None):
+    def conv(self, x, K, k, stride, pad, bn=True, bias=False, act="relu", residual=None, name=None,
+             logical_c=None):
+        """logical_c: channels that carry data when x is stored with zero channels appended
+        (the padded weights of those channels are zero, so the result is the logical conv)."""
         N, H, W, C = x.shape
-        fan = C * k * k
-        w = self._u((K, k, k, C), math.sqrt(6.0 / fan), "w")
+        lc = logical_c or C
+        fan = lc * k * k
+        w64 = synth.uniform((K, k, k, lc), -math.sqrt(6.0 / fan), math.sqrt(6.0 / fan),
+                            synth.tensor_seed(self.seed, self._n, "w"))
+        if lc != C:
+            w64 = np.concatenate([w64, np.zeros((K, k, k, C - lc))], axis=3)
+        w = self._dev(w64)
         b = self._u((K,), 1.0 / math.sqrt(fan), "b", "f32") if bias else None
         bnp = self._bn(K) if bn else None
         Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
         y = self.act_buf((N, Ho, Wo, K))
         op = O.conv2d(x, w, y, stride=stride, pad=pad, bias=b, bn=bnp, residual=residual, act=act)
         return self._add(Layer(name or f"conv{self._n}", "conv", op,
-                               dict(stride=stride, pad=pad, act=act, eps=1e-5),
+                               dict(stride=stride, pad=pad, act=act, eps=1e-5, logical_c=lc),
                                dict(x=x, w=w, bias=b, bn=bnp, residual=residual, y=y)))
 
     def dwconv(self, x, stride, act="relu6", name=None):
@@ -135,13 +143,24 @@ class Net:
 
 
 # ------------------------------------------------------------------ networks
+IMAGE_C = 8  # storage channels of a 3-channel input image (16-byte pixels)
+
+
+def image_input(batch, seed):
+    """Batch of 224x224 RGB images ~ U[-1, 1], stored NHWC with the 3 data channels
+    padded by zeros to 8 so every pixel is one 16-byte vector."""
+    x = synth.uniform((batch, 224, 224, 3), -1, 1, synth.tensor_seed(seed, -1, "input"))
+    return np.concatenate([x, np.zeros((batch, 224, 224, IMAGE_C - 3))], axis=3)
+
+
+
 def resnet18(batch=1, dtype="f16", seed=0, num_classes=1000) -> Net:
     """7x7/2 stem, 3x3/2 max pool, 4 stages of two 3x3 basic blocks (64/128/256/512),
     global average pool, FC 512 -> classes.  23 operators."""
     net = Net("resnet18", dtype, batch, seed)
-    x = net._dev(synth.uniform((batch, 224, 224, 3), -1, 1, synth.tensor_seed(seed, -1, "input")))
+    x = net._dev(image_input(batch, seed))
     net.input = x
-    h = net.conv(x, 64, 7, 2, 3, name="stem")
+    h = net.conv(x, 64, 7, 2, 3, name="stem", logical_c=3)
     h = net.pool(h, 3, 2, 1, "max", name="maxpool")
     cin = 64
     for stage, cout in enumerate([64, 128, 256, 512]):
@@ -161,12 +180,13 @@ def resnet18(batch=1, dtype="f16", seed=0, num_classes=1000) -> Net:
 def vgg16(batch=8, dtype="f16", seed=1, num_classes=1000) -> Net:
     """13 3x3 convs (64..512, bias + ReLU), 5 2x2 max pools, FC 25088->4096->4096->classes."""
     net = Net("vgg16", dtype, batch, seed)
-    x = net._dev(synth.uniform((batch, 224, 224, 3), -1, 1, synth.tensor_seed(seed, -1, "input")))
+    x = net._dev(image_input(batch, seed))
     net.input = x
     h = x
     for si, (c, n) in enumerate([(64, 2), (128, 2), (256, 3), (512, 3), (512, 3)]):
         for j in range(n):
-            h = net.conv(h, c, 3, 1, 1, bn=False, bias=True, act="relu", name=f"conv{si + 1}_{j + 1}")
+            h = net.conv(h, c, 3, 1, 1, bn=False, bias=True, act="relu", name=f"conv{si + 1}_{j + 1}",
+                         logical_c=3 if (si, j) == (0, 0) else None)
         h = net.pool(h, 2, 2, 0, "max", name=f"pool{si + 1}")
     f = h.reshape(batch, 7 * 7 * 512)
     f = net.linear(f, 4096, act="relu", name="fc6")
@@ -179,9 +199,9 @@ def mobilenetv2(batch=16, dtype="bf16", seed=2, num_classes=1000) -> Net:
     """Stem 3x3/2 conv 3->32, inverted residual blocks (expansion 6, width 1.0),
     1x1 conv 320->1280, global average pool, FC 1280->classes."""
     net = Net("mobilenetv2", dtype, batch, seed)
-    x = net._dev(synth.uniform((batch, 224, 224, 3), -1, 1, synth.tensor_seed(seed, -1, "input")))
+    x = net._dev(image_input(batch, seed))
     net.input = x
-    h = net.conv(x, 32, 3, 2, 1, act="relu6", name="stem")
+    h = net.conv(x, 32, 3, 2, 1, act="relu6", name="stem", logical_c=3)
     cin = 32
     for bi, (t, c, n, s) in enumerate([(1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2),
                                        (6, 96, 3, 1), (6, 160, 3, 2), (6, 320, 1, 1)]):
