@@ -303,7 +303,9 @@ def main():
     ap.add_argument("--quantum-us", type=float, default=40.0)
     ap.add_argument("--depth", type=int, default=4)
     ap.add_argument("--inflight-us", type=float, default=100.0)
-    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic")
+    ap.add_argument("--busy-policy", type=int, default=0,
+                    help="normal shards next to a running critical kernel: 0 paper rule, 1 none, 2 smallest")
+    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
                     help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
@@ -367,20 +369,24 @@ def main():
     torch.cuda.empty_cache()
 
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
-                profile_reps=3)
+                busy_policy=args.busy_policy, profile_reps=3)
     runs = {}
-    for ph in ("solo", "sequential", "multistream", "elastic"):
+    for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
         if ph not in phases:
             continue
         log(f"phase {ph} ...")
-        policy = "elastic" if ph == "solo" else ph
+        policy = {"solo": "elastic", "elastic_pause": "elastic"}.get(ph, ph)
+        pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else ccfg
         runs[ph] = run_phase(policy, crit_net, be_nets, args.warmup, args.steps, cfg["period_ms"],
-                             cfg["arrival"], seed=11, ccfg=ccfg, with_be=(ph != "solo"))
+                             cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
         r = runs[ph]
         log(f"  p50 {r['p50_ms']:.3f} ms  p99 {r['p99_ms']:.3f} ms  be {r['be_img_s']:.1f} img/s "
             f"launches {r['launches']}")
 
-    main_run = runs.get("elastic") or next(iter(runs.values()), None)
+    # main line: Miriam with normal shards held back while a critical kernel runs (the paper's
+    # padding rule is reported beside it as "elastic")
+    main_name = next((n for n in ("elastic_pause", "elastic") if n in runs), None)
+    main_run = runs[main_name] if main_name else next(iter(runs.values()), None)
     value = main_run["be_img_s"] if main_run else float("nan")
     out = {
         "metric": METRIC,
@@ -399,19 +405,24 @@ def main():
                    "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
-                   "inflight_us": args.inflight_us},
+                   "inflight_us": args.inflight_us, "busy_policy": args.busy_policy},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]
         out["critical"] = {
+            "policy": main_name,
             "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
             "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
             "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
+        for other in ("elastic", "multistream", "sequential"):
+            if other in runs and other != main_name:
+                out["critical"][f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
     for ph, r in runs.items():
         out.setdefault("phases", {})[ph] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
     if "sequential" in runs and main_run:
         seq = runs["sequential"]
         out["best_effort"] = {
+            "policy": main_name,
             "elastic_img_s": round(main_run["be_img_s"], 2), "sequential_img_s": round(seq["be_img_s"], 2),
             "speedup_vs_sequential": round(main_run["be_img_s"] / max(1e-9, seq["be_img_s"]), 3),
             "sequential_p99_ms": round(seq["p99_ms"], 4)}

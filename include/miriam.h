@@ -102,8 +102,11 @@ typedef struct miriam_op_desc {
     int64_t ldx, ldw, ldy;               /* row strides in elements, 0 = dense */
     int64_t sx0, sx1, sw0, sw1, sy0, sy1; /* BGEMM batch strides in elements */
     int32_t b_nmajor;
+    int32_t ksplit;     /* contractions: 0 = library choice, 1 = no split, n = split K over n workgroups
+                           per output tile (partials reduced in fixed order; the op then owns a device
+                           workspace, and every pass over the op must cover its whole tile space) */
     int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128, 4 = 128x64,
-                           5 = 16-column split-K (GEMM, fp16/bf16, m <= 16) */
+                           5 = 16-column split-K (GEMM, fp16/bf16, m <= 16), 6 = 256x128 */
     float eps;          /* BN / LN epsilon */
     float scale;        /* SOFTMAX scale */
     const void *x, *wt, *bias, *bn, *residual; /* device pointers (wt = weights) */
@@ -227,6 +230,9 @@ typedef struct miriam_config {
     double quantum_us;       /* target duration of one normal shard */
     double inflight_us;      /* normal work (estimated from the task profile) kept queued per
                                 normal stream; 0 = bounded by inflight_depth only */
+    int32_t busy_policy;     /* normal shards while a critical kernel runs: 0 = Eq. (2) + WIScore x OScore
+                                top fraction (the paper's rule), 1 = issue none until it completes,
+                                2 = smallest feasible footprint (grid = Eq. (2) limit / 4, block 64) */
     int32_t log_launches;    /* keep miriam_launch_record entries (diagnostics, tests) */
     int32_t profile_reps;    /* timed repetitions per op when a task is created (HIP backend) */
     /* FAKE backend only: simulated compute units, WG slots per CU, ns per tile, launch ns */

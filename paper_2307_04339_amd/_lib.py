@@ -40,7 +40,7 @@ class OpDesc(ctypes.Structure):
         ("ldx", ctypes.c_int64), ("ldw", ctypes.c_int64), ("ldy", ctypes.c_int64),
         ("sx0", ctypes.c_int64), ("sx1", ctypes.c_int64), ("sw0", ctypes.c_int64),
         ("sw1", ctypes.c_int64), ("sy0", ctypes.c_int64), ("sy1", ctypes.c_int64),
-        ("b_nmajor", ctypes.c_int32), ("tile", ctypes.c_int32),
+        ("b_nmajor", ctypes.c_int32), ("ksplit", ctypes.c_int32), ("tile", ctypes.c_int32),
         ("eps", ctypes.c_float), ("scale", ctypes.c_float),
         ("x", ctypes.c_void_p), ("wt", ctypes.c_void_p), ("bias", ctypes.c_void_p),
         ("bn", ctypes.c_void_p), ("residual", ctypes.c_void_p), ("y", ctypes.c_void_p),
@@ -69,6 +69,7 @@ class Config(ctypes.Structure):
         ("inflight_depth", ctypes.c_int32), ("top_frac", ctypes.c_double),
         ("max_blk_frac", ctypes.c_double), ("max_pt_frac", ctypes.c_double),
         ("quantum_us", ctypes.c_double), ("inflight_us", ctypes.c_double),
+        ("busy_policy", ctypes.c_int32),
         ("log_launches", ctypes.c_int32), ("profile_reps", ctypes.c_int32),
         ("fake_n_cu", ctypes.c_int32), ("fake_slots_per_cu", ctypes.c_int32),
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),

@@ -26,6 +26,7 @@
 #include <mutex>
 #include <new>
 #include <queue>
+#include <sys/prctl.h>
 #include <thread>
 #include <vector>
 
@@ -476,6 +477,10 @@ Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
         (void)k;
         d.grid = (int)cg[keep[0]];
         d.block = (int)cb[keep[0]];
+        if (c.cfg.busy_policy == 2) {  // ablation: smallest feasible footprint
+            d.grid = (int)std::max<int64_t>(1, gl / 4);
+            d.block = 64;
+        }
         d.limit = gl;
         bi = d.block == 64 ? 0 : (d.block == 128 ? 1 : 2);
     } else {
@@ -523,6 +528,7 @@ bool pump_normal(Coord &c, int s) {
         const int64_t t0 = mono_ns();
         const miriam_op *crit_op = nullptr;
         const bool busy = current_critical_op(c, &crit_op) >= 0;
+        if (busy && c.cfg.busy_policy == 1) break;  // ablation: hold normal work back
         Decision d = decide(c, r, busy ? crit_op : nullptr);
         const int64_t t1 = mono_ns();
         const int oi = (int)r->op;
@@ -559,8 +565,13 @@ bool all_idle(Coord &c) {
     return true;
 }
 
+// The dispatcher sleeps only until this long before a timed release; the rest is spun.
+constexpr int64_t kWakeEarlyNs = 300000;
+
 void dispatcher(Coord *cp) {
     Coord &c = *cp;
+    // timer slack of 1 us: a sleeping dispatcher must wake on time for releases
+    (void)prctl(PR_SET_TIMERSLACK, 1000UL, 0UL, 0UL, 0UL);
     if (c.cfg.backend == MIRIAM_BACKEND_HIP) (void)hipSetDevice(static_cast<HipBackend *>(c.be)->dev);
     for (;;) {
         {
@@ -644,9 +655,10 @@ void dispatcher(Coord *cp) {
                 // nothing on the GPU: sleep until a submission or the next timed release
                 std::unique_lock<std::mutex> lk(c.mu);
                 if (c.inbox.empty() && !(c.stopping && c.outstanding == 0)) {
+                    // sleep until shortly before the next timed release, then spin to it
                     int64_t wait_ns = 2000000;
                     if (!c.timed.empty()) wait_ns = std::min<int64_t>(wait_ns, c.timed.top()->release - mono_ns());
-                    if (wait_ns > 50000) c.cv.wait_for(lk, std::chrono::nanoseconds(wait_ns - 50000));
+                    if (wait_ns > kWakeEarlyNs) c.cv.wait_for(lk, std::chrono::nanoseconds(wait_ns - kWakeEarlyNs));
                 }
             } else {
                 std::this_thread::yield();
@@ -712,7 +724,7 @@ int miriam_init(const miriam_config *cfg) {
     if (cfg->policy < 0 || cfg->policy > 2 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
-        cfg->inflight_us < 0.0) {
+        cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }

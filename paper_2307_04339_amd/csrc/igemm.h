@@ -401,6 +401,7 @@ inline int igemm_table_cfg(int cfg, const void *out[3], int *lds) {
     case CFG_64: igemm_table<T, 64, 64, 32, LAY>(out, lds); return 0;
     case CFG_128: igemm_table<T, 128, 128, 32, LAY>(out, lds); return 0;
     case CFG_128x64: igemm_table<T, 128, 64, 32, LAY>(out, lds); return 0;
+    case CFG_256x128: igemm_table<T, 256, 128, 32, LAY>(out, lds); return 0;
     default: return -1;
     }
 }

@@ -3,8 +3,8 @@
 // fully connected layers, attention scores).
 //
 // Operands go straight from global memory into LDS with global_load_lds_dwordx4
-// (no register staging) through a ring of S K-chunks (double buffered: the next
-// chunk is in flight while one is multiplied, and two workgroups fit per CU).  An LDS row holds one 128-byte K-chunk of one
+// (no register staging) through a ring of S K-chunks (S-1 chunks in flight while one
+// is multiplied; S is as deep as two workgroups per CU allow).  An LDS row holds one 128-byte K-chunk of one
 // tile row; its eight 16-byte pieces are stored XOR-swizzled (piece c of row r
 // sits at slot c ^ ((r >> 1) & 7)), which keeps the MFMA operand reads of 32
 // consecutive rows free of bank conflicts without padding (each load instruction
@@ -38,7 +38,10 @@ struct DmaKernel {
     static constexpr int VEC = 16 / (int)sizeof(T);
     static constexpr int KT = 128 / (int)sizeof(T);      // one 128-byte row per chunk
     static constexpr int KSTEP = (kWave / MS) * MF::KPL;
-    static constexpr int S = 2;                          // stages: double buffer keeps 2 workgroups per CU
+    static constexpr int STAGE_B = (TM + TN) * 128;      // bytes per stage
+    // as many stages (2..4) as keep two workgroups within a CU's 160 KB of LDS
+    static constexpr int S_FIT = (80 * 1024) / STAGE_B;
+    static constexpr int S = S_FIT < 2 ? 2 : (S_FIT > 4 ? 4 : S_FIT);
     static constexpr int NIA = TM / 8 / P;               // A load instructions per wave per chunk
     static constexpr int NIB = TN / 8 / P;
     static constexpr int LPC = NIA + NIB;
@@ -91,8 +94,10 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
     int iter = 0;
     for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
         trace_tile(sh, t, iter);
-        // tile id -> (batch, m tile, n tile); every index here is below 2^31 (checked at creation)
-        const uint32_t per = (uint32_t)(a.mT * a.nT), t32 = (uint32_t)t;
+        // tile id -> (output tile, K slice) -> (batch, m tile, n tile); indices < 2^31 (checked at creation)
+        const uint32_t kslices = (uint32_t)a.ksplit;
+        const uint32_t otile = (uint32_t)t / kslices, slice = (uint32_t)t - otile * kslices;
+        const uint32_t per = (uint32_t)(a.mT * a.nT), t32 = otile;
         const uint32_t bi = t32 / per;
         const uint32_t rem = t32 - bi * per;
         const uint32_t mt = rem / (uint32_t)a.nT, nt = rem - mt * (uint32_t)a.nT;
@@ -119,7 +124,8 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
             a_base[j] = Xb + (int64_t)img * a.img_x;
             a_h0[j] = (int32_t)p * a.stride - a.pad;
             a_w0[j] = (int32_t)q * a.stride - a.pad;
-            const int32_t k = ((slot ^ ((row >> 1) & 7)) * VEC);  // logical 16-byte piece of this slot
+            // logical 16-byte piece of this slot, in the slice's first chunk
+            const int32_t k = (int32_t)(slice * (uint32_t)a.cps) * KT + ((slot ^ ((row >> 1) & 7)) * VEC);
             a_kc0[j] = k % C32;
             const int32_t tap = k / C32;
             a_ks0[j] = tap % KW32;
@@ -136,6 +142,10 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
             b_base[j] = Wb + (b_ok[j] ? n : 0) * a.ldw;
             b_k0[j] = (slot ^ ((row >> 1) & 7)) * VEC;
         }
+
+        const int c0 = (int)slice * a.cps;
+        const int nsl = c0 >= nch ? 0 : ((nch - c0) < a.cps ? (nch - c0) : a.cps);  // chunks of this slice
+        float *const part = a.ksplit > 1 ? a.work + (int64_t)t * (TM * TN) : nullptr;
 
         for (int rd = 0; rd < ROUNDS; ++rd) {
             acc_t acc[SL][BM][BN];
@@ -172,7 +182,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
                         if (++ks[j] == KW32) { ks[j] = 0; ++kr[j]; }
                     }
                 }
-                const int64_t k0 = (int64_t)ch * KT;
+                const int64_t k0 = (int64_t)(c0 + ch) * KT;
 #pragma unroll
                 for (int j = 0; j < NIB; ++j) {
                     const int64_t k = k0 + b_k0[j];
@@ -231,10 +241,10 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
 
 #pragma unroll
             for (int st = 0; st < S - 1; ++st)
-                if (st < nch) issue(st, st);
-            for (int c = 0; c < nch; ++c) {
-                // chunks issued after c and still allowed in flight: c+1 .. min(c+S-2, nch-1)
-                const int pending = (nch - 1 - c) < (S - 2) ? (nch - 1 - c) : (S - 2);
+                if (st < nsl) issue(st, st);
+            for (int c = 0; c < nsl; ++c) {
+                // chunks issued after c and still allowed in flight: c+1 .. min(c+S-2, nsl-1)
+                const int pending = (nsl - 1 - c) < (S - 2) ? (nsl - 1 - c) : (S - 2);
                 if constexpr (S - 2 >= 2) {
                     if (pending >= 2) wait_vmcnt<2 * LPC>();
                     else if (pending == 1) wait_vmcnt<LPC>();
@@ -247,10 +257,33 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
                     wait_vmcnt<0>();
                 }
                 __syncthreads();
-                if (c + S - 1 < nch) issue(c + S - 1, (c + S - 1) % S);
+                if (c + S - 1 < nsl) issue(c + S - 1, (c + S - 1) % S);
                 compute(c % S);
             }
             __syncthreads();
+
+            if (a.ksplit > 1) {
+                // split K: store this slice's raw partial tile; the reduction follows the rounds
+#pragma unroll
+                for (int s = 0; s < SL; ++s) {
+                    const int lam = (rd * SL + s) * P + pw;
+                    const int wm = lam >> 1, wn = lam & 1;
+#pragma unroll
+                    for (int i = 0; i < BM; ++i)
+#pragma unroll
+                        for (int jn = 0; jn < BN; ++jn) {
+                            const int col = wn * (TN / 2) + jn * MS + lane % MS;
+#pragma unroll
+                            for (int e = 0; e < MF::NACC; ++e) {
+                                const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
+                                const int row = wm * (TM / 2) + i * MS + rr;
+                                __hip_atomic_store(part + row * TN + col, acc[s][i][jn][e], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+                            }
+                        }
+                }
+                continue;
+            }
 
             // ---- epilogue, stage 1: accumulators (+ bias, BN) -> LDS as fp32
 #pragma unroll
@@ -306,6 +339,62 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
             }
             __syncthreads();
         }
+
+        if (a.ksplit > 1) {
+            // count this slice's arrival; the last slice of the output tile reduces all of
+            // them in slice order 0, 1, ..., ksplit-1 (same order whichever workgroup it is)
+            // The partials were written with agent-scope (device-coherent) stores; waiting for
+            // them to complete before the arrival is counted orders them before the count, and
+            // the reducer reads them back with agent-scope loads, so no cache-wide fence is needed.
+            __shared__ int s_last;
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (tid == 0) {
+                const int prev = __hip_atomic_fetch_add(a.counters + otile, 1, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+                s_last = prev == a.ksplit - 1;
+                if (s_last) __hip_atomic_store(a.counters + otile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            __syncthreads();
+            if (s_last) {
+                const float *base = a.work + (int64_t)otile * a.ksplit * (TM * TN);
+                constexpr int CVT = TN / VEC;
+                for (int idx = tid; idx < TM * CVT; idx += NT) {
+                    const int row = idx / CVT, col = (idx - (idx / CVT) * CVT) * VEC;
+                    const int64_t m = m0 + row, n = n0 + col;
+                    if (m >= a.M) continue;
+                    float v[VEC];
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        v[e] = __hip_atomic_load(base + row * TN + col + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int sl = 1; sl < a.ksplit; ++sl)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            v[e] += __hip_atomic_load(base + (int64_t)sl * (TM * TN) + row * TN + col + e,
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const int64_t off = yoff + m * a.ldy + n;
+                    if (a.vec_store && n + VEC <= a.Nc) {
+                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
+                        Vec16<T> o;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            const float pre = epilogue_pre(a.epi, chan_params(a.epi, n + e), v[e]);
+                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, pre, TypeOps<T>::to_f(rv.e[e])));
+                        }
+                        st_vec(Y + off, o);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (n + e < a.Nc) {
+                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
+                                const float pre = epilogue_pre(a.epi, chan_params(a.epi, n + e), v[e]);
+                                st_f(Y + off + e, epilogue_post(a.epi, pre, res));
+                            }
+                    }
+                }
+            }
+            __syncthreads();
+        }
     }
 }
 
@@ -324,6 +413,7 @@ inline int igemm_dma_table_cfg(int cfg, const void *out[3], int *lds) {
     case CFG_64: igemm_dma_table<T, 64, 64, 32>(out, lds); return 0;
     case CFG_128: igemm_dma_table<T, 128, 128, 32>(out, lds); return 0;
     case CFG_128x64: igemm_dma_table<T, 128, 64, 32>(out, lds); return 0;
+    case CFG_256x128: igemm_dma_table<T, 256, 128, 32>(out, lds); return 0;
     default: return -1;
     }
 }

@@ -41,6 +41,8 @@ struct miriam_op {
     miriam::PixArgs px;
     miriam::RowArgs rw;
     std::atomic<int> pending{0};  // submitted requests that still reference the op
+    void *work = nullptr;         // split-K partial tiles (device memory owned by the op)
+    void *counters = nullptr;     // split-K arrival counters (device memory owned by the op)
 };
 
 namespace miriam {

@@ -2,6 +2,7 @@
 // descriptors, tile-space construction, kernel selection, and the elastic launch
 // entry points (§6.1 elastic block, §6.2 elastic grid, §6.4 computation-based
 // index functions).
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -40,7 +41,7 @@ static int get_igemm_table(int dtype, int cfg, int lay, const void *out[3], int 
     }
 }
 
-static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : 128); }
+static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : (cfg == CFG_256x128 ? 256 : 128)); }
 static int tile_n_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 || cfg == CFG_128x64 ? 64 : 128); }
 constexpr int TILE_SKINNY = 5;  // descriptor tile code of the split-K skinny kernel
 
@@ -83,15 +84,32 @@ static int check_epi(const miriam_op_desc &d) {
     return MIRIAM_OK;
 }
 
-// Contraction tile choice: the largest tile that still yields about one tile per
-// compute unit (3/4 of them); a 128-row tile keeps 64 columns when N <= 64.
-static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
-    const int64_t want = 192;
-    if (N <= 64) {
-        if (batch * cdiv(M, 128) >= want) return CFG_128x64;
-    } else if (batch * cdiv(M, 128) * cdiv(N, 128) >= want) {
-        return CFG_128;
+// Compute units of the current device (256 when no device is visible).
+static int device_cus() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0;
+        hipDeviceProp_t p;
+        if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&p, dev) == hipSuccess)
+            n = p.multiProcessorCount;
+        else {
+            (void)hipGetLastError();
+            n = 256;
+        }
     }
+    return n;
+}
+
+// Workgroups wanted per launch: one and a half per compute unit, so that two
+// resident workgroups per CU stay busy through the tail.
+static int64_t wanted_tiles() { return (int64_t)device_cus() * 3 / 2; }
+
+// Contraction tile choice: the largest tile (128x128, 128x64, 64x64, 32x32) that
+// still yields the wanted number of tiles; 128x128 is skipped when N <= 64.
+static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
+    const int64_t want = wanted_tiles();
+    if (N > 64 && batch * cdiv(M, 128) * cdiv(N, 128) >= want) return CFG_128;
+    if (batch * cdiv(M, 128) * cdiv(N, 64) >= want) return CFG_128x64;
     if (batch * cdiv(M, 64) * cdiv(N, 64) >= want) return CFG_64;
     return CFG_32;
 }
@@ -176,10 +194,47 @@ static int create_igemm(miriam_op *op) {
         op->lds_bytes = 4 * 16 * 17 * 4;
         if (skinny_kernels(d.dtype, op->kern) != 0) return einval("no skinny kernel for this dtype");
     } else {
-        if (cfg < CFG_32 || cfg > CFG_128x64) return einval("unknown tile configuration");
+        if (cfg < CFG_32 || cfg > CFG_256x128 || cfg == TILE_SKINNY) return einval("unknown tile configuration");
         a.mT = cdiv(a.M, tile_m_of(cfg));
         a.nT = cdiv(a.Nc, tile_n_of(cfg));
         op->T = batch * a.mT * a.nT;
+        a.ksplit = 1;
+        a.cps = (int32_t)cdiv(a.K, d.dtype == MIRIAM_F32 ? 32 : 64);  // K chunks of one 128-byte row
+        // few output tiles over a deep K (batch-1 layers): split K over workgroups with a
+        // fixed-order reduction (pipelined kernel only), up to 16 slices of >= 2 chunks,
+        // aiming at the wanted number of workgroups
+        const int64_t want = wanted_tiles();
+        const int64_t nch = a.cps;
+        const bool vec_layout = (a_vec && b_vec && !nmaj);
+        const bool sparse = op->T < (int64_t)device_cus() / 2;  // under half a tile per compute unit
+        if (d.ksplit != 1 && vec_layout && (d.ksplit > 1 || (d.tile == 0 && sparse && nch >= 4))) {
+            int64_t ks = d.ksplit > 1 ? d.ksplit : std::min<int64_t>({16, cdiv(want, op->T), nch / 2});
+            ks = std::max<int64_t>(1, std::min<int64_t>(ks, nch));
+            if (ks > 1) {
+                const int64_t cps = cdiv(nch, ks);
+                ks = cdiv(nch, cps);  // no empty slices
+                const size_t wbytes = (size_t)op->T * (size_t)ks * tile_m_of(cfg) * tile_n_of(cfg) * sizeof(float);
+                const size_t cbytes = (size_t)op->T * sizeof(int32_t);
+                if (hipMalloc(&op->work, wbytes) == hipSuccess && hipMalloc(&op->counters, cbytes) == hipSuccess &&
+                    hipMemset(op->counters, 0, cbytes) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
+                    a.ksplit = (int32_t)ks;
+                    a.cps = (int32_t)cps;
+                    a.work = static_cast<float *>(op->work);
+                    a.counters = static_cast<int32_t *>(op->counters);
+                    op->T *= ks;
+                } else {
+                    (void)hipGetLastError();
+                    if (op->work) (void)hipFree(op->work);
+                    if (op->counters) (void)hipFree(op->counters);
+                    (void)hipGetLastError();
+                    op->work = op->counters = nullptr;
+                    if (d.ksplit > 1) {
+                        set_error("split-K workspace allocation failed");
+                        return MIRIAM_ENOMEM;
+                    }
+                }
+            }
+        }
         op->cfg = cfg;
         op->tile_m = tile_m_of(cfg);
         op->tile_n = tile_n_of(cfg);
@@ -383,6 +438,8 @@ int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
         rc = einval("unknown op kind");
     }
     if (rc != MIRIAM_OK) {
+        if (op->work) (void)hipFree(op->work);
+        if (op->counters) (void)hipFree(op->counters);
         delete op;
         return rc;
     }
@@ -426,6 +483,8 @@ int miriam_op_destroy(miriam_op *op) {
         set_error("op referenced by a pending request");
         return MIRIAM_EBUSY;
     }
+    if (op->work) (void)hipFree(op->work);
+    if (op->counters) (void)hipFree(op->counters);
     delete op;
     return MIRIAM_OK;
 }

@@ -91,7 +91,8 @@ def _epi(bias, bn, residual):
     return flags
 
 
-def conv2d(x, w, y, stride=1, pad=0, bias=None, bn=None, residual=None, act="none", eps=1e-5, tile=0):
+def conv2d(x, w, y, stride=1, pad=0, bias=None, bn=None, residual=None, act="none", eps=1e-5, tile=0,
+           ksplit=0):
     """x [N,H,W,C], w [K,KH,KW,C], y [N,Ho,Wo,K]; bias [K] f32; bn [4,K] f32."""
     N, H, W, C = x.shape
     K, KH, KW, C2 = w.shape
@@ -99,17 +100,19 @@ def conv2d(x, w, y, stride=1, pad=0, bias=None, bn=None, residual=None, act="non
     return ElasticOp(L.OP_CONV2D, x.dtype, keep=(x, w, y, bias, bn, residual),
                      n=N, h=H, w=W, c=C, k=K, kh=KH, kw=KW, stride=stride, pad=pad, groups=1,
                      x=x, wt=w, y=y, bias=bias, bn=bn, residual=residual,
-                     flags=_epi(bias, bn, residual), act=L.ACT_CODE[act], eps=eps, tile=tile)
+                     flags=_epi(bias, bn, residual), act=L.ACT_CODE[act], eps=eps, tile=tile, ksplit=ksplit)
 
 
-def gemm(x, w, y, bias=None, residual=None, act="none", tile=0, ldx=0, ldw=0, ldy=0, m=None, n=None, k=None):
+def gemm(x, w, y, bias=None, residual=None, act="none", tile=0, ldx=0, ldw=0, ldy=0, m=None, n=None, k=None,
+         ksplit=0):
     """y[m][n] = act(x[m][:] . w[n][:] + bias + residual)."""
     M = m if m is not None else x.shape[0]
     Kk = k if k is not None else x.shape[-1]
     Nn = n if n is not None else w.shape[0]
     return ElasticOp(L.OP_GEMM, x.dtype, keep=(x, w, y, bias, residual),
                      m=M, nn=Nn, kk=Kk, ldx=ldx, ldw=ldw, ldy=ldy, x=x, wt=w, y=y, bias=bias,
-                     residual=residual, flags=_epi(bias, None, residual), act=L.ACT_CODE[act], tile=tile)
+                     residual=residual, flags=_epi(bias, None, residual), act=L.ACT_CODE[act], tile=tile,
+                     ksplit=ksplit)
 
 
 def bgemm(x, w, y, m, n, k, batch, batch_div, ldx, ldw, ldy, sx=(0, 0), sw=(0, 0), sy=(0, 0),

@@ -26,6 +26,7 @@ def default_config(**kw) -> L.Config:
     c.max_pt_frac = 0.1
     c.quantum_us = 50.0
     c.inflight_us = 0.0
+    c.busy_policy = 0
     c.log_launches = 0
     c.profile_reps = 3
     c.fake_n_cu = 8

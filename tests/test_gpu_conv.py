@@ -146,3 +146,56 @@ def test_conv_shapes_match_oracle(ops, orc, dtype, case):
                          bn=None if bn64 is None else tuple(bn64), residual=r64, act=act)
         err = rel_err(to_f64(y), ref)
         assert err <= RTOL[dtype], (tile, err)
+
+
+# ---------------------------------------------------------------- split K
+SPLIT_CASES = [
+    # N, H, W, C, K, KH, stride, pad, ksplit   (deep K over few output tiles)
+    (1, 7, 7, 512, 512, 3, 1, 1, 8),
+    (1, 14, 14, 256, 256, 3, 1, 1, 3),
+    (2, 7, 7, 64, 96, 3, 1, 1, 2),
+    (1, 7, 7, 512, 512, 3, 1, 1, 0),   # library choice
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("case", SPLIT_CASES)
+def test_conv_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, case):
+    N, H, W, C, K, KH, s, p, ks = case
+    seed = abs(hash(case)) % 1000
+    x, x64 = rand((N, H, W, C), dtype, seed=seed)
+    w, w64 = rand((K, KH, KH, C), dtype, seed=seed + 1, lo=-0.05, hi=0.05)
+    rng = np.random.default_rng(seed + 2)
+    bn64 = np.stack([rng.uniform(0.8, 1.2, K), rng.uniform(-0.1, 0.1, K),
+                     rng.uniform(-0.1, 0.1, K), rng.uniform(0.8, 1.2, K)]).astype(np.float32).astype(np.float64)
+    Ho, Wo = (H + 2 * p - KH) // s + 1, (W + 2 * p - KH) // s + 1
+    res, r64 = rand((N, Ho, Wo, K), dtype, seed=seed + 3)
+    y = empty((N, Ho, Wo, K), dtype)
+    op = ops.conv2d(x, w, y, stride=s, pad=p, bn=f32_dev(bn64), residual=res, act="relu", ksplit=ks)
+    if ks == 0:
+        # 1 x 7 x 7 x 512 output at 32x32 tiles: 32 output tiles, split to about 1.5 tiles per CU
+        assert op.T > 32 and op.T % 32 == 0
+    else:
+        assert op.T % ks == 0
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, stride=s, pad=p, bn=tuple(bn64), residual=r64, act="relu")
+    assert rel_err(to_f64(y), ref) <= RTOL[dtype]
+    ref_bits = bits(y)
+    # any shard plan, order, grid and block: the last slice to arrive reduces in fixed order
+    rng = np.random.default_rng(seed + 4)
+    for n in [1, 2, 3, 5, 8]:
+        if n > op.T:
+            continue
+        plan = orc.balanced_split(op.T, n)
+        order = rng.permutation(n)
+        for j in order:
+            b, l = plan[j]
+            op.launch(b, l, int(rng.choice([1, 3, 64, l])), int(rng.choice([64, 128, 256])))
+        torch.cuda.synchronize()
+        assert bits(y) == ref_bits, (n, order)
+    # repeated passes leave the arrival counters clean
+    for _ in range(3):
+        op.run()
+    torch.cuda.synchronize()
+    assert bits(y) == ref_bits
