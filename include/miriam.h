@@ -124,7 +124,19 @@ typedef struct miriam_op_info {
     int32_t max_wg_per_cu[3]; /* resident workgroups per CU for blocks 64, 128, 256 (0 if unknown) */
     double flops;             /* algorithmic floating-point operations of the whole op */
     double bytes;             /* algorithmic HBM bytes: inputs and weights read once, outputs written once */
+    int32_t path;             /* miriam_kernel_path: which kernel family serves the op */
+    int32_t ksplit;           /* K slices per output tile (1 = no split); num_tiles counts slices */
 } miriam_op_info;
+
+/* Kernel family behind an op (diagnostic; results do not depend on it beyond rounding
+ * order, which is fixed per op). */
+typedef enum miriam_kernel_path {
+    MIRIAM_PATH_OTHER = 0,       /* memory-bound operator kernels */
+    MIRIAM_PATH_STAGED = 1,      /* contraction, operands staged through registers */
+    MIRIAM_PATH_DMA = 2,         /* contraction, global->LDS pipeline, per-lane K decode */
+    MIRIAM_PATH_DMA_UNIFORM = 3, /* contraction, global->LDS pipeline, chunk-uniform filter taps */
+    MIRIAM_PATH_SKINNY = 4       /* small-batch fully connected, K split over logical waves */
+} miriam_kernel_path;
 
 /* ------------------------------------------------------------------ device */
 typedef struct miriam_device_desc {
@@ -228,8 +240,9 @@ typedef struct miriam_config {
     double max_blk_frac;     /* Eq. (5) MAX_blk as a fraction of the unsharded time (0.1) */
     double max_pt_frac;      /* Eq. (5) MAX_pt as a fraction of the unsharded time (0.1) */
     double quantum_us;       /* target duration of one normal shard */
-    double inflight_us;      /* normal work (estimated from the task profile) kept queued per
-                                normal stream; 0 = bounded by inflight_depth only */
+    double inflight_us;      /* normal work (estimated from the task profile) kept queued on the GPU,
+                                summed over the normal streams (each stream may always keep one
+                                shard in flight); 0 = bounded by inflight_depth only */
     int32_t busy_policy;     /* normal shards while a critical kernel runs: 0 = Eq. (2) + WIScore x OScore
                                 top fraction (the paper's rule), 1 = issue none until it completes,
                                 2 = smallest feasible footprint (grid = Eq. (2) limit / 4, block 64) */

@@ -508,11 +508,19 @@ Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
     return d;
 }
 
-// Issue shards for the normal requests of one stream while its in-flight budget lasts.
+// Estimated normal work queued on the GPU, over all normal streams.
+double queued_normal_us(const Coord &c) {
+    double t = 0.0;
+    for (size_t s = 1; s < c.inflight_us.size(); ++s) t += c.inflight_us[s];
+    return t;
+}
+
+// Issue shards for the normal requests of one stream while the in-flight budget lasts
+// (every stream may keep one shard in flight; beyond that the budget is shared).
 bool pump_normal(Coord &c, int s) {
     bool any = false;
     while (c.inflight[s] < c.cfg.inflight_depth &&
-           (c.cfg.inflight_us <= 0.0 || c.inflight[s] == 0 || c.inflight_us[s] < c.cfg.inflight_us)) {
+           (c.cfg.inflight_us <= 0.0 || c.inflight[s] == 0 || queued_normal_us(c) < c.cfg.inflight_us)) {
         Req *r = nullptr;
         for (Req *q : c.be_active[s])
             if (!q->launched_all) {

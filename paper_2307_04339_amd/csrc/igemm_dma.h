@@ -11,6 +11,13 @@
 // writes 1024 contiguous LDS bytes).  Padded taps and out-of-range rows load from
 // a zero-filled device block.
 //
+// UNI variant: when every K chunk lies inside one filter tap (C a multiple of the chunk,
+// which includes every GEMM with K a multiple of it), all lanes of a chunk share the tap
+// (kh, kw) and channel base, which live in scalar registers.  Each lane then keeps a
+// source pointer that is rebuilt only when the tap changes and otherwise advances by
+// one chunk (by nothing for padding lanes, which point at the zero block), so a load
+// costs one 64-bit add instead of a full index decode and bounds test.
+//
 // The arithmetic is exactly the one of igemm_kernel: same tile, same 2x2 logical
 // waves, same MFMA opcode and K order, same staged epilogue; only how operands
 // reach LDS differs.  Results are therefore bit-identical for every shard plan,
@@ -23,6 +30,20 @@ namespace miriam {
 
 // 16-byte zero source for lanes whose element lies in the padding or past a bound.
 static __device__ __attribute__((aligned(64))) uint32_t g_zero_src[16];
+
+// One 16-byte-per-lane global -> LDS load: lane i writes LDS bytes [lds + 16 i, lds + 16 i + 16).
+// Issued as inline assembly so the compiler does not treat every later LDS read as
+// dependent on it (it would otherwise wait for all outstanding loads before each read,
+// serialising the pipeline); the kernel orders these loads itself with wait_vmcnt and
+// barriers, and no compiler-visible vector loads are in flight while they are.
+// `lds` is a wave-uniform LDS byte address.
+__device__ __forceinline__ void lds_dma16(const void *src, uint32_t lds_addr) {
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(lds)
+                 : "memory", "m0");
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -61,7 +82,7 @@ struct DmaKernel {
     static_assert(KT % KSTEP == 0, "chunk must hold whole MFMA steps");
 };
 
-template <class T, int TM, int TN, int MS, int P>
+template <class T, int TM, int TN, int MS, int P, bool UNI>
 __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard sh) {
     typedef DmaKernel<T, TM, TN, MS, P> K_;
     typedef typename K_::MF MF;
@@ -74,6 +95,8 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
     __shared__ __attribute__((aligned(1024))) char smem_[K_::LDS_BYTES];
     char *const smem = smem_;
     float *const Cs = reinterpret_cast<float *>(smem_);
+    // LDS byte address of the ring (the DMA loads take LDS addresses, not generic pointers)
+    const uint32_t lds_ring = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem_;
 
     const int tid = threadIdx.x;
     const int pw = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -111,6 +134,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
         const T *a_base[NIA];
         int32_t a_h0[NIA], a_w0[NIA];
         int32_t a_kr0[NIA], a_ks0[NIA], a_kc0[NIA];
+        uint64_t a_org[NIA];  // UNI: byte address of tap (0, 0), channel 0 + this lane's piece
         bool a_ok[NIA];
 #pragma unroll
         for (int j = 0; j < NIA; ++j) {
@@ -126,10 +150,15 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
             a_w0[j] = (int32_t)q * a.stride - a.pad;
             // logical 16-byte piece of this slot, in the slice's first chunk
             const int32_t k = (int32_t)(slice * (uint32_t)a.cps) * KT + ((slot ^ ((row >> 1) & 7)) * VEC);
-            a_kc0[j] = k % C32;
-            const int32_t tap = k / C32;
-            a_ks0[j] = tap % KW32;
-            a_kr0[j] = tap / KW32;
+            if constexpr (UNI) {
+                const int64_t off = ((int64_t)a_h0[j] * a.W + a_w0[j]) * a.ldx + (slot ^ ((row >> 1) & 7)) * VEC;
+                a_org[j] = (uint64_t)(uintptr_t)a_base[j] + (uint64_t)(off * (int64_t)sizeof(T));
+            } else {
+                a_kc0[j] = k % C32;
+                const int32_t tap = k / C32;
+                a_ks0[j] = tap % KW32;
+                a_kr0[j] = tap / KW32;
+            }
         }
         const T *b_base[NIB];
         int32_t b_k0[NIB];
@@ -159,23 +188,75 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
                         for (int e = 0; e < MF::NACC; ++e) acc[s][i][jn][e] = 0.0f;
 
             int32_t kr[NIA], ks[NIA], kc[NIA];
+            if constexpr (!UNI) {
 #pragma unroll
-            for (int j = 0; j < NIA; ++j) {
-                kr[j] = a_kr0[j];
-                ks[j] = a_ks0[j];
-                kc[j] = a_kc0[j];
+                for (int j = 0; j < NIA; ++j) {
+                    kr[j] = a_kr0[j];
+                    ks[j] = a_ks0[j];
+                    kc[j] = a_kc0[j];
+                }
+            }
+            // UNI: the chunk's tap (ur, us) and channel base uc are wave-uniform; per-lane
+            // pointers and steps (elements per chunk: KT, or 0 for zero-block lanes)
+            int32_t ur = 0, us = 0, uc = 0;
+            bool retap = true;
+            const T *ap[NIA], *bp[NIB];
+            int32_t astep[NIA], bstep[NIB];
+            if constexpr (UNI) {
+                const int32_t k0 = c0 * KT, tap = k0 / C32;
+                uc = k0 - tap * C32;
+                ur = tap / KW32;
+                us = tap - ur * KW32;
+#pragma unroll
+                for (int j = 0; j < NIB; ++j) {
+                    bp[j] = b_ok[j] ? b_base[j] + k0 + b_k0[j] : zsrc;
+                    bstep[j] = b_ok[j] ? KT : 0;
+                }
             }
 
             // issue chunk ch into stage st (all lanes issue every instruction)
             auto issue = [&](int ch, int st) {
-                char *stage = smem + st * K_::STAGE;
+                const uint32_t stage = lds_ring + (uint32_t)(st * K_::STAGE);
+                if constexpr (UNI) {
+                    if (retap) {
+                        const int64_t toff = (((int64_t)ur * a.W + us) * a.ldx + uc) * (int64_t)sizeof(T);
+#pragma unroll
+                        for (int j = 0; j < NIA; ++j) {
+                            const uint32_t h = (uint32_t)(a_h0[j] + ur), w = (uint32_t)(a_w0[j] + us);
+                            const bool ok = a_ok[j] && h < (uint32_t)H32 && w < (uint32_t)W32;
+                            ap[j] = ok ? reinterpret_cast<const T *>((uintptr_t)(a_org[j] + (uint64_t)toff)) : zsrc;
+                            astep[j] = ok ? KT : 0;
+                        }
+                        retap = false;
+                    }
+#pragma unroll
+                    for (int j = 0; j < NIA; ++j) {
+                        lds_dma16(ap[j], stage + (uint32_t)((8 * (j * P + pw)) * 128));
+                        ap[j] += astep[j];
+                    }
+#pragma unroll
+                    for (int j = 0; j < NIB; ++j) {
+                        lds_dma16(bp[j], stage + (uint32_t)((TM + 8 * (j * P + pw)) * 128));
+                        bp[j] += bstep[j];
+                    }
+                    uc += KT;
+                    if (uc == C32) {
+                        uc = 0;
+                        retap = true;
+                        if (++us == KW32) {
+                            us = 0;
+                            ++ur;
+                        }
+                    }
+                    (void)ch;
+                    return;
+                }
 #pragma unroll
                 for (int j = 0; j < NIA; ++j) {
                     const int32_t h = a_h0[j] + kr[j], w = a_w0[j] + ks[j];
                     const bool ok = a_ok[j] && kr[j] < KH32 && h >= 0 && h < H32 && w >= 0 && w < W32;
                     const T *src = ok ? a_base[j] + ((int64_t)h * a.W + w) * a.ldx + kc[j] : zsrc;
-                    char *dst = stage + (8 * (j * P + pw)) * 128;
-                    __builtin_amdgcn_global_load_lds((const void *)(src), (__attribute__((address_space(3))) void *)(dst), 16, 0, 0);
+                    lds_dma16(src, stage + (uint32_t)((8 * (j * P + pw)) * 128));
                     kc[j] += KT;
                     while (kc[j] >= C32) {
                         kc[j] -= C32;
@@ -187,8 +268,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
                 for (int j = 0; j < NIB; ++j) {
                     const int64_t k = k0 + b_k0[j];
                     const T *src = (b_ok[j] && k < a.K) ? b_base[j] + k : zsrc;
-                    char *dst = stage + (TM + 8 * (j * P + pw)) * 128;
-                    __builtin_amdgcn_global_load_lds((const void *)(src), (__attribute__((address_space(3))) void *)(dst), 16, 0, 0);
+                    lds_dma16(src, stage + (uint32_t)((TM + 8 * (j * P + pw)) * 128));
                 }
             };
 
@@ -398,22 +478,22 @@ __global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard
     }
 }
 
-template <class T, int TM, int TN, int MS>
+template <class T, int TM, int TN, int MS, bool UNI>
 inline void igemm_dma_table(const void *out[3], int *lds) {
-    out[0] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 1>);
-    out[1] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 2>);
-    out[2] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 4>);
+    out[0] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 1, UNI>);
+    out[1] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 2, UNI>);
+    out[2] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 4, UNI>);
     *lds = DmaKernel<T, TM, TN, MS, 4>::LDS_BYTES;
 }
 
-template <class T>
+template <class T, bool UNI>
 inline int igemm_dma_table_cfg(int cfg, const void *out[3], int *lds) {
     switch (cfg) {
-    case CFG_32: igemm_dma_table<T, 32, 32, 16>(out, lds); return 0;
-    case CFG_64: igemm_dma_table<T, 64, 64, 32>(out, lds); return 0;
-    case CFG_128: igemm_dma_table<T, 128, 128, 32>(out, lds); return 0;
-    case CFG_128x64: igemm_dma_table<T, 128, 64, 32>(out, lds); return 0;
-    case CFG_256x128: igemm_dma_table<T, 256, 128, 32>(out, lds); return 0;
+    case CFG_32: igemm_dma_table<T, 32, 32, 16, UNI>(out, lds); return 0;
+    case CFG_64: igemm_dma_table<T, 64, 64, 32, UNI>(out, lds); return 0;
+    case CFG_128: igemm_dma_table<T, 128, 128, 32, UNI>(out, lds); return 0;
+    case CFG_128x64: igemm_dma_table<T, 128, 64, 32, UNI>(out, lds); return 0;
+    case CFG_256x128: igemm_dma_table<T, 256, 128, 32, UNI>(out, lds); return 0;
     default: return -1;
     }
 }

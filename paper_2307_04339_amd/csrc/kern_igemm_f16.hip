@@ -5,7 +5,8 @@
 namespace miriam {
 int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds) {
     switch (lay) {
-    case LAY_VEC: return igemm_dma_table_cfg<half_t>(cfg, out, lds);
+    case LAY_VEC: return igemm_dma_table_cfg<half_t, false>(cfg, out, lds);
+    case LAY_VEC_UNI: return igemm_dma_table_cfg<half_t, true>(cfg, out, lds);
     case LAY_SCALAR: return igemm_table_cfg<half_t, LAY_SCALAR>(cfg, out, lds);
     case LAY_VEC_NB: return igemm_table_cfg<half_t, LAY_VEC_NB>(cfg, out, lds);
     case LAY_SCALAR_NB: return igemm_table_cfg<half_t, LAY_SCALAR_NB>(cfg, out, lds);

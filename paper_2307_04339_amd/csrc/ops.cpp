@@ -104,11 +104,13 @@ static int device_cus() {
 // resident workgroups per CU stay busy through the tail.
 static int64_t wanted_tiles() { return (int64_t)device_cus() * 3 / 2; }
 
-// Contraction tile choice: the largest tile (128x128, 128x64, 64x64, 32x32) that
-// still yields the wanted number of tiles; 128x128 is skipped when N <= 64.
+// Contraction tile choice: the largest of 128x64, 64x64, 32x32 that still gives at
+// least three quarters of a tile per compute unit.  Measured on the pipelined kernel,
+// 128x64 beats 128x128 and 256x128 at every convolution size of the CNN workloads
+// (the wider tiles leave too few workgroups per compute unit to hide load latency),
+// and a smaller tile beats a larger one once the larger leaves CUs idle.
 static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
-    const int64_t want = wanted_tiles();
-    if (N > 64 && batch * cdiv(M, 128) * cdiv(N, 128) >= want) return CFG_128;
+    const int64_t want = (int64_t)device_cus() * 3 / 4;
     if (batch * cdiv(M, 128) * cdiv(N, 64) >= want) return CFG_128x64;
     if (batch * cdiv(M, 64) * cdiv(N, 64) >= want) return CFG_64;
     return CFG_32;
@@ -240,6 +242,8 @@ static int create_igemm(miriam_op *op) {
         op->tile_n = tile_n_of(cfg);
         if (nmaj) op->lay = (a_vec && b_vec) ? LAY_VEC_NB : LAY_SCALAR_NB;
         else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
+        // every 128-byte K chunk inside one filter tap: per-lane pointers advance per chunk
+        if (op->lay == LAY_VEC && a.C % (128 / es) == 0) op->lay = LAY_VEC_UNI;
         if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
             return einval("no kernel for this dtype / layout");
     }
@@ -460,6 +464,13 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
     for (int i = 0; i < 3; ++i) out->max_wg_per_cu[i] = op->max_wg_per_cu[i];
     out->flops = op->flops;
     out->bytes = op->bytes;
+    if (op->family == FAM_SKINNY) out->path = MIRIAM_PATH_SKINNY;
+    else if (op->family == FAM_IGEMM)
+        out->path = op->lay == LAY_VEC_UNI ? MIRIAM_PATH_DMA_UNIFORM
+                    : op->lay == LAY_VEC   ? MIRIAM_PATH_DMA
+                                           : MIRIAM_PATH_STAGED;
+    else out->path = MIRIAM_PATH_OTHER;
+    out->ksplit = op->family == FAM_IGEMM ? op->ig.ksplit : 1;
     return MIRIAM_OK;
 }
 

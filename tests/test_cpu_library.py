@@ -173,3 +173,31 @@ def test_gemm_tile_space(lib, M, N, K, tile, T):
     assert info.num_tiles == T
     assert info.flops == 2.0 * M * N * K
     lib.miriam_op_destroy(h)
+
+
+@pytest.mark.parametrize("kind,dtype,geo,addr,path", [
+    ("conv", "F16", dict(c=64), FAKE, "PATH_DMA_UNIFORM"),       # chunk = 64 channels = one tap
+    ("conv", "F16", dict(c=32), FAKE, "PATH_DMA"),               # chunks straddle taps
+    ("conv", "F32", dict(c=32), FAKE, "PATH_DMA_UNIFORM"),       # fp32 chunk is 32 elements
+    ("conv", "F16", dict(c=64), FAKE + 2, "PATH_STAGED"),        # operand not 16-byte aligned
+    ("conv", "F16", dict(c=3), FAKE, "PATH_STAGED"),             # rows not a 16-byte multiple
+    ("gemm", "BF16", dict(m=4, kk=512), FAKE, "PATH_SKINNY"),    # small-batch FC
+    ("gemm", "BF16", dict(m=64, kk=512), FAKE, "PATH_DMA_UNIFORM"),
+    ("gemm", "BF16", dict(m=64, kk=200), FAKE, "PATH_DMA"),      # K tail inside the last chunk
+    ("gemm", "F32", dict(m=4, kk=512), FAKE, "PATH_DMA_UNIFORM"),  # no fp32 skinny kernel
+])
+def test_kernel_path_selection(lib, kind, dtype, geo, addr, path):
+    from paper_2307_04339_amd import _lib as L
+    if kind == "conv":
+        d = dict(kind=L.OP_CONV2D, dtype=getattr(L, dtype), n=1, h=9, w=9, c=16, k=32, kh=3, kw=3,
+                 stride=1, pad=1, x=addr, wt=FAKE, y=FAKE)
+    else:
+        d = dict(kind=L.OP_GEMM, dtype=getattr(L, dtype), m=64, nn=96, kk=64, x=addr, wt=FAKE, y=FAKE)
+    d.update(geo)
+    rc, h = _create(lib, _desc(**d))
+    assert rc == 0, lib.miriam_last_error()
+    info = L.OpInfo()
+    assert lib.miriam_op_query(h, ctypes.byref(info)) == 0
+    assert info.path == getattr(L, path)
+    assert info.ksplit >= 1
+    lib.miriam_op_destroy(h)

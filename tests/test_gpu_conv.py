@@ -112,6 +112,8 @@ CASES = [
     (1, 14, 14, 256, 512, 1, 2, 0, "none", "bn"),     # 1x1 downsample
     (2, 7, 7, 96, 40, 1, 1, 0, "relu6", "bn_res"),    # residual, K not a tile multiple
     (1, 9, 9, 24, 144, 1, 1, 0, "relu6", "bn"),       # C = 24 (not a chunk multiple)
+    (2, 15, 15, 128, 64, 3, 2, 1, "relu", "bn"),      # two chunks per tap, stride 2, padding
+    (1, 12, 12, 64, 40, 5, 1, 2, "none", "bias"),     # 5x5 taps, one chunk per tap (16-bit)
 ]
 
 
