@@ -83,6 +83,39 @@ def time_layers(net, reps, flush):
     return out
 
 
+# HBM traffic of the dominant kernel, from rocprofv3 FETCH_SIZE / WRITE_SIZE runs committed under
+# profiles/ (each counter scaled by what it reads for a device copy of known size).  Used only
+# while the contraction-kernel sources still hash to the value the counters were taken with.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = ["igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h", "kern_igemm_f16.hip",
+                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "ops.cpp"]
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2307_04339_amd", "csrc", name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel, tile):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when
+    there is none for this workload / tile or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            entries = json.load(f)["entries"]
+    except (OSError, ValueError, KeyError):
+        return None
+    e = entries.get(f"{workload}:{kernel}")
+    if not e or list(e.get("tile", [])) != list(tile) or e.get("source_sha256") != kernel_source_hash():
+        return None
+    fetch = e["fetch_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_fetch_kib"] * 1024.0)
+    write = e["write_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_write_kib"] * 1024.0)
+    return round(fetch + write)
+
+
 def roofline_of(k, dtype):
     ai = k["flops"] / max(1.0, k["bytes"])
     ridge = PEAK_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
@@ -356,6 +389,8 @@ def main():
         kern["flops_per_launch"] = dom["flops"]
         kern["bytes_per_launch"] = dom["bytes"]
         layer = next(l for l in dom_net.layers if l.name == dom["name"])
+        kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
+        kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"])
         result["elastic_overhead"] = dict(kernel=kern["kernel"],
                                           **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load()))
         result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],

@@ -76,6 +76,8 @@ struct DmaKernel {
     static constexpr int LDC = TN + 4;
     static constexpr int C_BYTES = TM * LDC * 4;
     static constexpr int LDS_BYTES = S * STAGE > C_BYTES ? S * STAGE : C_BYTES;
+    // register budget: two resident 4-wave workgroups per CU wherever their LDS fits
+    static constexpr int WAVES_PER_SIMD = (P == 4 && 2 * (LDS_BYTES + 16) <= 160 * 1024) ? 2 : 1;
     static_assert(TM % (8 * P) == 0 && TN % (8 * P) == 0, "load instructions must divide evenly");
     static_assert((S - 2) * LPC < 64, "vmcnt range");
     static_assert(LW % SL == 0, "slots must divide logical waves");
@@ -83,7 +85,8 @@ struct DmaKernel {
 };
 
 template <class T, int TM, int TN, int MS, int P, bool UNI>
-__global__ __launch_bounds__(kWave * P) void igemm_dma_kernel(IgemmArgs a, Shard sh) {
+__global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_SIMD)) void igemm_dma_kernel(
+    IgemmArgs a, Shard sh) {
     typedef DmaKernel<T, TM, TN, MS, P> K_;
     typedef typename K_::MF MF;
     typedef typename MF::op_t op_t;

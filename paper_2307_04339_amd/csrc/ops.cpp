@@ -100,19 +100,16 @@ static int device_cus() {
     return n;
 }
 
-// Workgroups wanted per launch: one and a half per compute unit, so that two
-// resident workgroups per CU stay busy through the tail.
-static int64_t wanted_tiles() { return (int64_t)device_cus() * 3 / 2; }
-
-// Contraction tile choice: the largest of 128x64, 64x64, 32x32 that still gives at
-// least three quarters of a tile per compute unit.  Measured on the pipelined kernel,
-// 128x64 beats 128x128 and 256x128 at every convolution size of the CNN workloads
-// (the wider tiles leave too few workgroups per compute unit to hide load latency),
-// and a smaller tile beats a larger one once the larger leaves CUs idle.
+// Contraction tile choice, from per-layer sweeps of the pipelined kernel on the CNN
+// workloads: 128x128 when N > 64 and it still gives 1.5 tiles per compute unit (its
+// operands cost the fewest bytes per flop); otherwise the largest of 128x64, 64x64,
+// 32x32 that gives three quarters of a tile per compute unit (a smaller tile beats a
+// larger one once the larger leaves CUs idle).  256x128 never won: too few tiles.
 static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
-    const int64_t want = (int64_t)device_cus() * 3 / 4;
-    if (batch * cdiv(M, 128) * cdiv(N, 64) >= want) return CFG_128x64;
-    if (batch * cdiv(M, 64) * cdiv(N, 64) >= want) return CFG_64;
+    const int64_t cus = device_cus();
+    if (N > 64 && batch * cdiv(M, 128) * cdiv(N, 128) >= cus * 3 / 2) return CFG_128;
+    if (batch * cdiv(M, 128) * cdiv(N, 64) >= cus * 3 / 4) return CFG_128x64;
+    if (batch * cdiv(M, 64) * cdiv(N, 64) >= cus * 3 / 4) return CFG_64;
     return CFG_32;
 }
 
@@ -202,16 +199,14 @@ static int create_igemm(miriam_op *op) {
         op->T = batch * a.mT * a.nT;
         a.ksplit = 1;
         a.cps = (int32_t)cdiv(a.K, d.dtype == MIRIAM_F32 ? 32 : 64);  // K chunks of one 128-byte row
-        // few output tiles over a deep K (batch-1 layers): split K over workgroups with a
-        // fixed-order reduction (pipelined kernel only), up to 16 slices of >= 2 chunks,
-        // aiming at the wanted number of workgroups
-        const int64_t want = wanted_tiles();
+        // split K over workgroups with a fixed-order reduction (pipelined kernel only) when
+        // the caller asks for it
+        // (the library choice is no split: on the pipelined kernel a split measured slower
+        // than or equal to the unsplit launch on every CNN layer with few output tiles)
         const int64_t nch = a.cps;
         const bool vec_layout = (a_vec && b_vec && !nmaj);
-        const bool sparse = op->T < (int64_t)device_cus() / 2;  // under half a tile per compute unit
-        if (d.ksplit != 1 && vec_layout && (d.ksplit > 1 || (d.tile == 0 && sparse && nch >= 4))) {
-            int64_t ks = d.ksplit > 1 ? d.ksplit : std::min<int64_t>({16, cdiv(want, op->T), nch / 2});
-            ks = std::max<int64_t>(1, std::min<int64_t>(ks, nch));
+        if (d.ksplit > 1 && vec_layout) {
+            int64_t ks = std::min<int64_t>(d.ksplit, nch);
             if (ks > 1) {
                 const int64_t cps = cdiv(nch, ks);
                 ks = cdiv(nch, cps);  // no empty slices
