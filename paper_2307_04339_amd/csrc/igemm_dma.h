@@ -389,16 +389,24 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                     }
             }
             __syncthreads();
-            // ---- stage 2: + residual, activation, one rounding, coalesced row stores
+            // ---- stage 2: + residual, activation, one rounding, coalesced row stores.
+            // When this pass holds both column halves of its rows (always for 4-wave blocks),
+            // consecutive threads cover whole output rows of the tile, so every store
+            // instruction writes full rows (TN * sizeof(T) contiguous bytes each) rather
+            // than half rows whose other halves arrive later.
             {
                 constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
+                constexpr bool FULL = (SL * P) % 2 == 0;
+                constexpr int RV = FULL ? 2 * CV : CV;  // vectors per stored row segment
+                constexpr int ROWS = FULL ? (SL * P / 2) * SUBR : SL * P * SUBR;
                 const int lam0 = rd * SL * P;
-                for (int idx = tid; idx < SL * P * SUBR * CV; idx += NT) {
-                    const int sub = idx / (SUBR * CV);
-                    const int rem2 = idx - sub * (SUBR * CV);
-                    const int r = rem2 / CV, cv = rem2 - (rem2 / CV) * CV;
-                    const int lam = lam0 + sub;
-                    const int row = (lam >> 1) * SUBR + r, col = (lam & 1) * SUBC + cv * VEC;
+                for (int idx = tid; idx < ROWS * RV; idx += NT) {
+                    const int rr2 = idx / RV, cv = idx - (idx / RV) * RV;
+                    // FULL: row block (lam0 / 2 + rr2 / SUBR) and both halves; else sub-tile lam0 + rr2 / SUBR
+                    const int blk = rr2 / SUBR, r = rr2 - blk * SUBR;
+                    const int lam = FULL ? lam0 + 2 * blk : lam0 + blk;
+                    const int row = (lam >> 1) * SUBR + r;
+                    const int col = FULL ? cv * VEC : (lam & 1) * SUBC + cv * VEC;
                     const int64_t m = m0 + row, n = n0 + col;
                     if (m >= a.M) continue;
                     const float *cr = Cs + row * LDC + col;
