@@ -106,7 +106,9 @@ typedef struct miriam_op_desc {
                            per output tile (partials reduced in fixed order; the op then owns a device
                            workspace, and every pass over the op must cover its whole tile space) */
     int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128, 4 = 128x64,
-                           5 = 16-column split-K (GEMM, fp16/bf16, m <= 16), 6 = 256x128 */
+                           5 = 16-column split-K (GEMM, fp16/bf16, m <= 16), 6 = 256x128,
+                           7 = direct 3x3 stride-1 conv: 4x32 output pixels x 64 channels, the tile's
+                           input patch held in LDS (C a multiple of 64 fp16/bf16 or 32 fp32 channels) */
     float eps;          /* BN / LN epsilon */
     float scale;        /* SOFTMAX scale */
     const void *x, *wt, *bias, *bn, *residual; /* device pointers (wt = weights) */
@@ -135,7 +137,8 @@ typedef enum miriam_kernel_path {
     MIRIAM_PATH_STAGED = 1,      /* contraction, operands staged through registers */
     MIRIAM_PATH_DMA = 2,         /* contraction, global->LDS pipeline, per-lane K decode */
     MIRIAM_PATH_DMA_UNIFORM = 3, /* contraction, global->LDS pipeline, chunk-uniform filter taps */
-    MIRIAM_PATH_SKINNY = 4       /* small-batch fully connected, K split over logical waves */
+    MIRIAM_PATH_SKINNY = 4,      /* small-batch fully connected, K split over logical waves */
+    MIRIAM_PATH_HALO = 5         /* direct 3x3 stride-1 convolution, input patch of the tile in LDS */
 } miriam_kernel_path;
 
 /* ------------------------------------------------------------------ device */

@@ -57,7 +57,7 @@ class OpInfo(ctypes.Structure):
 
 
 # miriam_kernel_path
-PATH_OTHER, PATH_STAGED, PATH_DMA, PATH_DMA_UNIFORM, PATH_SKINNY = 0, 1, 2, 3, 4
+PATH_OTHER, PATH_STAGED, PATH_DMA, PATH_DMA_UNIFORM, PATH_SKINNY, PATH_HALO = 0, 1, 2, 3, 4, 5
 
 
 class DeviceDesc(ctypes.Structure):

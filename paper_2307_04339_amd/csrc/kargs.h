@@ -45,6 +45,7 @@ struct IgemmArgs {
     int64_t mT, nT;        // tiles along m and n
     int64_t bdiv, sx0, sx1, sw0, sw1, sy0, sy1;  // batch offsets
     int64_t img_x;         // elements between images of x
+    int64_t tY, tX;        // direct 3x3 kernel: tile rows and tile columns per output image
     int32_t vec_store;     // 1: output / residual rows allow 16-byte vector access
     int32_t ksplit;        // K slices per output tile (1 = none); tile id = output tile * ksplit + slice
     int32_t cps;           // K chunks per slice
@@ -80,7 +81,7 @@ struct RowArgs {
 
 enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3 };
 enum RowKind { ROW_SOFTMAX = 0, ROW_LAYERNORM = 1 };
-enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3, LAY_VEC_UNI = 4 };
-enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4, CFG_256x128 = 6 };
+enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3, LAY_VEC_UNI = 4, LAY_HALO = 5 };
+enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4, CFG_256x128 = 6, CFG_HALO = 7 };
 
 }  // namespace miriam

@@ -1,12 +1,13 @@
 // Kernel table of the elastic contraction kernel for f16 operands (one translation unit
 // per element type keeps the build parallel).
-#include "igemm_dma.h"
+#include "conv_halo.h"
 
 namespace miriam {
 int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds) {
     switch (lay) {
     case LAY_VEC: return igemm_dma_table_cfg<half_t, false>(cfg, out, lds);
     case LAY_VEC_UNI: return igemm_dma_table_cfg<half_t, true>(cfg, out, lds);
+    case LAY_HALO: return halo_table<half_t>(out, lds);
     case LAY_SCALAR: return igemm_table_cfg<half_t, LAY_SCALAR>(cfg, out, lds);
     case LAY_VEC_NB: return igemm_table_cfg<half_t, LAY_VEC_NB>(cfg, out, lds);
     case LAY_SCALAR_NB: return igemm_table_cfg<half_t, LAY_SCALAR_NB>(cfg, out, lds);

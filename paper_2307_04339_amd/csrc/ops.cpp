@@ -41,7 +41,7 @@ static int get_igemm_table(int dtype, int cfg, int lay, const void *out[3], int 
     }
 }
 
-static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : (cfg == CFG_256x128 ? 256 : 128)); }
+static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 : (cfg == CFG_256x128 ? 256 : 128)); }  // halo: 4 x 32 pixels
 static int tile_n_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 || cfg == CFG_128x64 ? 64 : 128); }
 constexpr int TILE_SKINNY = 5;  // descriptor tile code of the split-K skinny kernel
 
@@ -179,9 +179,37 @@ static int create_igemm(miriam_op *op) {
                   (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
     // fully connected layers at small batch: split-K skinny kernel
     const bool skinny_ok = d.kind == MIRIAM_OP_GEMM && d.dtype != MIRIAM_F32 && a.M <= 16 && a_vec && b_vec;
+    // direct 3x3 / stride-1 convolution with the input patch in LDS: C a whole number of
+    // 128-byte chunks, aligned rows.  The library picks it for layers with at most 64 output
+    // channels (one n tile) when it gives 1.5 tiles per CU and the 32-pixel tile columns waste
+    // at most a quarter of the output width; on wider layers the 128x128 / 128x64 implicit
+    // GEMM measured as fast or faster (VGG-16 b8: conv1_2 84 us vs 95 us at 128x64; conv3_2
+    // 64 us vs 54 us at 128x128)
+    const int64_t kt = 128 / es;
+    const bool halo_ok = d.kind == MIRIAM_OP_CONV2D && d.kh == 3 && d.kw == 3 && d.stride == 1 && a_vec && b_vec &&
+                         d.c % kt == 0 && d.ksplit <= 1;
+    const int64_t halo_tx = cdiv(a.Wo, 32), halo_ty = cdiv(a.Ho, 4);
+    const int64_t halo_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
     int cfg = d.tile;
+    if (cfg == 0 && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5)
+        cfg = CFG_HALO;
     if (cfg == 0) cfg = skinny_ok ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
-    if (cfg == TILE_SKINNY) {
+    if (cfg == CFG_HALO) {
+        if (!halo_ok) return einval("tile 7 (direct 3x3) needs a 3x3 stride-1 conv with C a multiple of the 128-byte chunk, 16-byte rows and no split K");
+        a.tX = halo_tx;
+        a.tY = halo_ty;
+        a.mT = halo_ty * halo_tx;
+        a.nT = cdiv(a.Nc, 64);
+        a.ksplit = 1;
+        a.cps = (int32_t)cdiv(a.K, kt);
+        op->T = d.n * a.mT * a.nT;
+        op->cfg = cfg;
+        op->tile_m = 128;
+        op->tile_n = 64;
+        op->lay = LAY_HALO;
+        if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
+            return einval("no direct 3x3 kernel for this dtype");
+    } else if (cfg == TILE_SKINNY) {
         if (!skinny_ok) return einval("skinny tile needs an fp16/bf16 GEMM with m <= 16 and 16-byte rows");
         op->family = FAM_SKINNY;
         a.mT = 1;
@@ -461,9 +489,10 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
     out->bytes = op->bytes;
     if (op->family == FAM_SKINNY) out->path = MIRIAM_PATH_SKINNY;
     else if (op->family == FAM_IGEMM)
-        out->path = op->lay == LAY_VEC_UNI ? MIRIAM_PATH_DMA_UNIFORM
-                    : op->lay == LAY_VEC   ? MIRIAM_PATH_DMA
-                                           : MIRIAM_PATH_STAGED;
+        out->path = op->lay == LAY_HALO      ? MIRIAM_PATH_HALO
+                    : op->lay == LAY_VEC_UNI ? MIRIAM_PATH_DMA_UNIFORM
+                    : op->lay == LAY_VEC     ? MIRIAM_PATH_DMA
+                                             : MIRIAM_PATH_STAGED;
     else out->path = MIRIAM_PATH_OTHER;
     out->ksplit = op->family == FAM_IGEMM ? op->ig.ksplit : 1;
     return MIRIAM_OK;

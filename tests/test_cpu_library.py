@@ -185,6 +185,10 @@ def test_gemm_tile_space(lib, M, N, K, tile, T):
     ("gemm", "BF16", dict(m=64, kk=512), FAKE, "PATH_DMA_UNIFORM"),
     ("gemm", "BF16", dict(m=64, kk=200), FAKE, "PATH_DMA"),      # K tail inside the last chunk
     ("gemm", "F32", dict(m=4, kk=512), FAKE, "PATH_DMA_UNIFORM"),  # no fp32 skinny kernel
+    ("conv", "F16", dict(c=64, tile=7), FAKE, "PATH_HALO"),      # direct 3x3 on request
+    ("conv", "F32", dict(c=32, tile=7), FAKE, "PATH_HALO"),      # fp32 chunk is 32 channels
+    ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=64), FAKE, "PATH_HALO"),   # chosen: 784 tiles, N = 64
+    ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=128), FAKE, "PATH_DMA_UNIFORM"),  # wider: implicit GEMM
 ])
 def test_kernel_path_selection(lib, kind, dtype, geo, addr, path):
     from paper_2307_04339_amd import _lib as L
@@ -201,3 +205,14 @@ def test_kernel_path_selection(lib, kind, dtype, geo, addr, path):
     assert info.path == getattr(L, path)
     assert info.ksplit >= 1
     lib.miriam_op_destroy(h)
+
+
+@pytest.mark.parametrize("geo", [dict(c=32), dict(c=64, stride=2), dict(c=64, kh=5, kw=5, pad=2),
+                                 dict(c=64, ksplit=2)])
+def test_direct3x3_rejects_ineligible_convs(lib, geo):
+    from paper_2307_04339_amd import _lib as L
+    d = dict(kind=L.OP_CONV2D, dtype=L.F16, n=1, h=9, w=9, c=16, k=32, kh=3, kw=3, stride=1, pad=1,
+             x=FAKE, wt=FAKE, y=FAKE, tile=7)
+    d.update(geo)
+    rc, _ = _create(lib, _desc(**d))
+    assert rc == L.EINVAL

@@ -46,7 +46,7 @@ def test_conv_cfg1_matches_oracle(ops, orc):
     assert err <= RTOL["f32"]
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3, 4])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 7])
 def test_conv_cfg1_bitwise_across_elastic_configs(ops, orc, tile):
     op, y, _ = _cfg1(ops, tile=tile)
     op.run()
@@ -71,8 +71,9 @@ def test_conv_cfg1_bitwise_across_elastic_configs(ops, orc, tile):
                     assert bits(y) == ref_bits, (tile, n, block, order, gmode)
 
 
-def test_conv_tile_map_matches_oracle(ops, orc):
-    op, y, _ = _cfg1(ops, tile=1)
+@pytest.mark.parametrize("tile", [1, 7])
+def test_conv_tile_map_matches_oracle(ops, orc, tile):
+    op, y, _ = _cfg1(ops, tile=tile)
     T = op.T
     for n, grids, block in [(1, [T], 256), (4, [5, 64, 1, 33], 128), (3, [7, 7, 7], 64),
                             (8, [256] * 8, 256)]:
@@ -202,3 +203,73 @@ def test_conv_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, case):
         op.run()
     torch.cuda.synchronize()
     assert bits(y) == ref_bits
+
+
+# ------------------------------------------------ direct 3x3 kernel (tile 7)
+HALO_CASES = [
+    # N, H, W, C, K, pad, act, epilogue
+    (2, 15, 37, 128, 64, 1, "relu", "bn"),       # ragged tile rows and columns, two 16-bit chunks
+    (1, 9, 70, 64, 96, 1, "none", "bias"),       # ragged n tile (96 = 64 + 32), three tile columns
+    (1, 30, 33, 64, 64, 0, "relu6", "bn_res"),   # no padding (28 x 31 output), residual
+    (3, 8, 32, 192, 40, 1, "none", "bn"),        # odd number of chunks, K < 64, batch 3
+]
+
+
+def _halo_inputs(case, dtype):
+    N, H, W, C, K, p, act, epi = case
+    seed = abs(hash(case)) % 1000
+    x, x64 = rand((N, H, W, C), dtype, seed=seed)
+    w, w64 = rand((K, 3, 3, C), dtype, seed=seed + 1, lo=-0.2, hi=0.2)
+    Ho, Wo = H + 2 * p - 2, W + 2 * p - 2
+    rng = np.random.default_rng(seed + 2)
+    bias = bn = res = None
+    b64 = bn64 = r64 = None
+    if "bias" in epi:
+        b64 = rng.uniform(-1, 1, K).astype(np.float32).astype(np.float64)
+        bias = f32_dev(b64)
+    if "bn" in epi:
+        bn64 = np.stack([rng.uniform(0.8, 1.2, K), rng.uniform(-0.1, 0.1, K), rng.uniform(-0.1, 0.1, K),
+                         rng.uniform(0.8, 1.2, K)]).astype(np.float32).astype(np.float64)
+        bn = f32_dev(bn64)
+    if "res" in epi:
+        res, r64 = rand((N, Ho, Wo, K), dtype, seed=seed + 3)
+    y = empty((N, Ho, Wo, K), dtype)
+    ref_args = dict(stride=1, pad=p, bias=b64, bn=None if bn64 is None else tuple(bn64), residual=r64, act=act)
+    return (x, w, y, dict(stride=1, pad=p, bias=bias, bn=bn, residual=res, act=act)), (x64, w64, ref_args)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("case", HALO_CASES)
+def test_conv_direct3x3_matches_oracle_and_is_elastic(ops, orc, dtype, case):
+    from paper_2307_04339_amd import _lib as L
+    (x, w, y, kw), (x64, w64, rargs) = _halo_inputs(case, dtype)
+    op = ops.conv2d(x, w, y, tile=7, **kw)
+    assert op.info.path == L.PATH_HALO
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, **rargs)
+    err = rel_err(to_f64(y), ref)
+    assert err <= RTOL[dtype], err
+    ref_bits = bits(y)
+    rng = np.random.default_rng(7)
+    for n in [2, 3, 5]:
+        if n > op.T:
+            continue
+        plan = orc.balanced_split(op.T, n)
+        for j in rng.permutation(n):
+            b, l = plan[j]
+            op.launch(b, l, int(rng.choice([1, 2, 7, l])), int(rng.choice([64, 128, 256])))
+        torch.cuda.synchronize()
+        assert bits(y) == ref_bits, n
+
+
+def test_conv_direct3x3_chosen_for_wide_layers(ops):
+    from paper_2307_04339_amd import _lib as L
+    # a 112 x 112 x 64 -> 64 layer at batch 8: 896 tiles, one n tile
+    x, _ = rand((8, 112, 112, 64), "f16", seed=0)
+    w, _ = rand((64, 3, 3, 64), "f16", seed=1, lo=-0.05, hi=0.05)
+    y = empty((8, 112, 112, 64), "f16")
+    assert ops.conv2d(x, w, y, stride=1, pad=1).info.path == L.PATH_HALO
+    # stride 2 keeps the implicit GEMM
+    y2 = empty((8, 56, 56, 64), "f16")
+    assert ops.conv2d(x, w, y2, stride=2, pad=1).info.path != L.PATH_HALO
