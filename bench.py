@@ -87,8 +87,8 @@ def time_layers(net, reps, flush):
 # profiles/ (each counter scaled by what it reads for a device copy of known size).  Used only
 # while the contraction-kernel sources still hash to the value the counters were taken with.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h", "kern_igemm_f16.hip",
-                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "ops.cpp"]
+KERNEL_SOURCES = ["conv_halo.h", "igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h", "kern_igemm_f16.hip",
+                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "kern_skinny.hip", "ops.cpp"]
 
 
 def kernel_source_hash():
