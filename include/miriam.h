@@ -311,6 +311,7 @@ typedef struct miriam_launch_record {
     int64_t shard_begin, shard_len, num_tiles;
     int64_t eq2_grid_limit; /* Eq. (2) grid limit in force (0 if none) */
     int64_t t_issue_ns;
+    double est_us;         /* the coordinator's estimate of the launch's duration (task profile) */
 } miriam_launch_record;
 
 /* Copy up to max_out of the oldest unread launch records; returns the count. */

@@ -87,6 +87,7 @@ class LaunchRecord(ctypes.Structure):
         ("criticality", ctypes.c_int32), ("grid", ctypes.c_int32), ("block", ctypes.c_int32),
         ("crit_busy", ctypes.c_int32), ("shard_begin", ctypes.c_int64), ("shard_len", ctypes.c_int64),
         ("num_tiles", ctypes.c_int64), ("eq2_grid_limit", ctypes.c_int64), ("t_issue_ns", ctypes.c_int64),
+        ("est_us", ctypes.c_double),
     ]
 
 

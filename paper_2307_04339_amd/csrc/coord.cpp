@@ -314,7 +314,7 @@ std::mutex g_life;  // serialises init / shutdown
 int64_t eq2_limit(int n_cu, int64_t n_rt) { return miriam_plan_eq2_grid_limit(n_cu, n_rt); }
 
 void log_launch(Coord &c, const Req *r, int op_index, int stream, int grid, int block, bool crit_busy,
-                int64_t b, int64_t l, int64_t T, int64_t limit) {
+                int64_t b, int64_t l, int64_t T, int64_t limit, double est_us) {
     if (!c.cfg.log_launches) return;
     miriam_launch_record rec;
     rec.ticket = r->ticket;
@@ -329,6 +329,7 @@ void log_launch(Coord &c, const Req *r, int op_index, int stream, int grid, int 
     rec.num_tiles = T;
     rec.eq2_grid_limit = limit;
     rec.t_issue_ns = mono_ns();
+    rec.est_us = est_us;
     std::lock_guard<std::mutex> lk(c.log_mu);
     if (c.log.size() - c.log_read < (1u << 22)) c.log.push_back(rec);
 }
@@ -346,7 +347,7 @@ int issue(Coord &c, Req *r, int oi, int64_t b, int64_t l, int grid, int block, i
     r->n_shards++;
     c.inflight[stream]++;
     c.inflight_us[stream] += est_us;
-    log_launch(c, r, oi, stream, grid, block, crit_busy, b, l, op->T, limit);
+    log_launch(c, r, oi, stream, grid, block, crit_busy, b, l, op->T, limit, est_us);
     std::lock_guard<std::mutex> lk(c.stat_mu);
     c.stats.launches++;
     return MIRIAM_OK;

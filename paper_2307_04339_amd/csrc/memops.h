@@ -18,11 +18,65 @@
 
 namespace miriam {
 
+// 16-byte zero source for window taps that fall in the padding.
+static __device__ __attribute__((aligned(64))) uint32_t g_pix_zero[16];
+
+// Per-channel epilogue parameters of V consecutive channels c0.. (16-byte loads when V is a
+// multiple of 4: C and c0 are then multiples of 4 and the parameter rows 16-byte aligned,
+// checked at creation).  Same values as chan_params, channel by channel.
+template <int V>
+__device__ __forceinline__ void chan_params_vec(const Epilogue &e, int64_t c0, ChanParams (&p)[V]) {
+    if constexpr (V % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            const int64_t c = c0 + 4 * q;
+            f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f}, g = {1.0f, 1.0f, 1.0f, 1.0f};
+            f32x4 be = {0.0f, 0.0f, 0.0f, 0.0f}, mu = {0.0f, 0.0f, 0.0f, 0.0f}, var = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (e.flags & EPI_BIAS) b = *reinterpret_cast<const f32x4 *>(e.bias + c);
+            if (e.flags & EPI_BN) {
+                g = *reinterpret_cast<const f32x4 *>(e.bn + c);
+                be = *reinterpret_cast<const f32x4 *>(e.bn + e.C + c);
+                mu = *reinterpret_cast<const f32x4 *>(e.bn + 2 * e.C + c);
+                var = *reinterpret_cast<const f32x4 *>(e.bn + 3 * e.C + c);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[4 * q + i] = ChanParams{0.0f, 0.0f, 1.0f, 0.0f};
+                if (e.flags & EPI_BIAS) p[4 * q + i].bias = b[i];
+                if (e.flags & EPI_BN) {
+                    p[4 * q + i].scale = g[i] / sqrtf(var[i] + e.eps);
+                    p[4 * q + i].mean = mu[i];
+                    p[4 * q + i].beta = be[i];
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) p[i] = chan_params(e, c0 + i);
+    }
+}
+
+template <class T, int V>
+__device__ __forceinline__ void ld_items(const T *p, T (&v)[V]) {
+    if constexpr (V * sizeof(T) == 16) {
+        Vec16<T> vv = ld_vec(p);
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[e] = vv.e[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[e] = p[e];
+    }
+}
+
 // One lane item: V consecutive channels of one output pixel.
+// Window taps are visited in row-major order (r, then s); padding taps are skipped.  The
+// taps go in batches of 9 whose loads are all issued before any is used, so a 3x3 window
+// costs one round of load latency, not nine.
 template <class T, int V, int KIND>
 __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
     const T *__restrict__ X = static_cast<const T *>(a.x);
     T *__restrict__ Y = static_cast<T *>(a.y);
+    const T *const zsrc = reinterpret_cast<const T *>(g_pix_zero);
     // item indices stay below 2^31 (checked at creation): 32-bit division
     const uint32_t CV = (uint32_t)(a.C / V), u32 = (uint32_t)u;
     const uint32_t pixu = u32 / CV;
@@ -31,58 +85,61 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
     float acc[V];
     if constexpr (KIND == PIX_EW) {
         // pixel == row of C channels; elementwise epilogue
-        const T *src = X + pix * a.C + c0;
-        const T *rs = static_cast<const T *>(a.res) + pix * a.C + c0;
+        T xv[V], rv[V];
+        ld_items<T, V>(X + pix * a.C + c0, xv);
+        if (a.epi.flags & EPI_RES) ld_items<T, V>(static_cast<const T *>(a.res) + pix * a.C + c0, rv);
+        ChanParams cp[V];
+        chan_params_vec<V>(a.epi, c0, cp);
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            const float r = (a.epi.flags & EPI_RES) ? ld_f(rs + e) : 0.0f;
-            acc[e] = epilogue_apply(a.epi, ld_f(src + e), c0 + e, r);
+            const float r = (a.epi.flags & EPI_RES) ? TypeOps<T>::to_f(rv[e]) : 0.0f;
+            acc[e] = epilogue_post(a.epi, epilogue_pre(a.epi, cp[e], TypeOps<T>::to_f(xv[e])), r);
         }
     } else {
         const uint32_t HoWo = (uint32_t)(a.Ho * a.Wo), Wo = (uint32_t)a.Wo;
-        const int64_t n = pixu / HoWo;
-        const uint32_t pq = pixu - (uint32_t)n * HoWo;
-        const int64_t p = pq / Wo, q = pq - (pq / Wo) * Wo;
-        const int64_t h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+        const uint32_t n = pixu / HoWo;
+        const uint32_t pq = pixu - n * HoWo;
+        const int32_t p = (int32_t)(pq / Wo), q = (int32_t)(pq - (pq / Wo) * Wo);
+        const int32_t h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+        const int32_t H32 = (int32_t)a.H, W32 = (int32_t)a.W;
+        const int taps = a.KH * a.KW;
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[e] = (KIND == PIX_MAX) ? -INFINITY : 0.0f;
         const T *Wt = static_cast<const T *>(a.w);
-        for (int r = 0; r < a.KH; ++r) {
-            const int64_t h = h0 + r;
-            if (h < 0 || h >= a.H) continue;
-            for (int s = 0; s < a.KW; ++s) {
-                const int64_t w = w0 + s;
-                if (w < 0 || w >= a.W) continue;
-                const T *xp = X + ((n * a.H + h) * a.W + w) * a.C + c0;
-                T xv[V];
-                if constexpr (V * sizeof(T) == 16) {
-                    Vec16<T> vv = ld_vec(xp);
+        const T *xn = X + (int64_t)n * a.H * a.W * a.C + c0;
+        int r = 0, s = 0;  // (r, s) of tap k0
+        constexpr int TB = 9;  // taps per batch
+        for (int k0 = 0; k0 < taps; k0 += TB) {
+            T xv[TB][V], wv[TB][V];
+            bool ok[TB];
+            int rj = r, sj = s;
 #pragma unroll
-                    for (int e = 0; e < V; ++e) xv[e] = vv.e[e];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < V; ++e) xv[e] = xp[e];
+            for (int j = 0; j < TB; ++j) {
+                const int32_t h = h0 + rj, w = w0 + sj;
+                ok[j] = k0 + j < taps && h >= 0 && h < H32 && w >= 0 && w < W32;
+                ld_items<T, V>(ok[j] ? xn + ((int64_t)h * a.W + w) * a.C : zsrc, xv[j]);
+                if constexpr (KIND == PIX_DW)
+                    ld_items<T, V>(ok[j] ? Wt + (int64_t)(k0 + j) * a.C + c0 : zsrc, wv[j]);
+                if (++sj == a.KW) {
+                    sj = 0;
+                    ++rj;
                 }
+            }
+            r = rj;
+            s = sj;
+#pragma unroll
+            for (int j = 0; j < TB; ++j) {
+                if (!ok[j]) continue;
                 if constexpr (KIND == PIX_DW) {
-                    const T *wp = Wt + ((int64_t)r * a.KW + s) * a.C + c0;
-                    T wv[V];
-                    if constexpr (V * sizeof(T) == 16) {
-                        Vec16<T> vv = ld_vec(wp);
-#pragma unroll
-                        for (int e = 0; e < V; ++e) wv[e] = vv.e[e];
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < V; ++e) wv[e] = wp[e];
-                    }
 #pragma unroll
                     for (int e = 0; e < V; ++e)
-                        acc[e] = __builtin_fmaf(TypeOps<T>::to_f(xv[e]), TypeOps<T>::to_f(wv[e]), acc[e]);
+                        acc[e] = __builtin_fmaf(TypeOps<T>::to_f(xv[j][e]), TypeOps<T>::to_f(wv[j][e]), acc[e]);
                 } else if constexpr (KIND == PIX_MAX) {
 #pragma unroll
-                    for (int e = 0; e < V; ++e) acc[e] = fmaxf(acc[e], TypeOps<T>::to_f(xv[e]));
+                    for (int e = 0; e < V; ++e) acc[e] = fmaxf(acc[e], TypeOps<T>::to_f(xv[j][e]));
                 } else {
 #pragma unroll
-                    for (int e = 0; e < V; ++e) acc[e] += TypeOps<T>::to_f(xv[e]);
+                    for (int e = 0; e < V; ++e) acc[e] += TypeOps<T>::to_f(xv[j][e]);
                 }
             }
         }
@@ -92,11 +149,14 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
             for (int e = 0; e < V; ++e) acc[e] *= inv;
         }
         if constexpr (KIND == PIX_DW) {
-            const T *rs = static_cast<const T *>(a.res) + pix * a.C + c0;
+            T rv[V];
+            if (a.epi.flags & EPI_RES) ld_items<T, V>(static_cast<const T *>(a.res) + pix * a.C + c0, rv);
+            ChanParams cp[V];
+            chan_params_vec<V>(a.epi, c0, cp);
 #pragma unroll
             for (int e = 0; e < V; ++e) {
-                const float r = (a.epi.flags & EPI_RES) ? ld_f(rs + e) : 0.0f;
-                acc[e] = epilogue_apply(a.epi, acc[e], c0 + e, r);
+                const float rr = (a.epi.flags & EPI_RES) ? TypeOps<T>::to_f(rv[e]) : 0.0f;
+                acc[e] = epilogue_post(a.epi, epilogue_pre(a.epi, cp[e], acc[e]), rr);
             }
         }
     }

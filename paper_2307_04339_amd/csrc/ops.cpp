@@ -312,7 +312,8 @@ static int create_pix(miriam_op *op) {
     if (rc) return rc;
     const bool vec = (a.C % V == 0) && aligned16(d.x) && aligned16(d.y) &&
                      (kind != PIX_DW || aligned16(d.wt)) &&
-                     (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
+                     (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual)) &&
+                     (!(d.flags & MIRIAM_EPI_BIAS) || aligned16(d.bias)) && (!(d.flags & MIRIAM_EPI_BN) || aligned16(d.bn));
     const int v = vec ? V : 1;
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.C);
