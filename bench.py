@@ -338,6 +338,8 @@ def main():
     ap.add_argument("--inflight-us", type=float, default=100.0)
     ap.add_argument("--busy-policy", type=int, default=0,
                     help="normal shards next to a running critical kernel: 0 paper rule, 1 none, 2 smallest")
+    ap.add_argument("--graphs", type=int, default=1, choices=(0, 1),
+                    help="1: whole-request launches replay each task's captured HIP graph")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
@@ -404,7 +406,7 @@ def main():
     torch.cuda.empty_cache()
 
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
-                busy_policy=args.busy_policy, profile_reps=3)
+                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
         if ph not in phases:
@@ -440,7 +442,8 @@ def main():
                    "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
-                   "inflight_us": args.inflight_us, "busy_policy": args.busy_policy},
+                   "inflight_us": args.inflight_us, "busy_policy": args.busy_policy,
+                   "graphs": args.graphs},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

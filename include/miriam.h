@@ -254,6 +254,12 @@ typedef struct miriam_config {
     /* FAKE backend only: simulated compute units, WG slots per CU, ns per tile, launch ns */
     int32_t fake_n_cu, fake_slots_per_cu;
     double fake_tile_ns, fake_launch_ns;
+    int32_t graphs;          /* 1 = capture each task's unsharded kernel sequence (grid = T, block 256
+                                per op) into a HIP graph when the task is created, and run every
+                                whole-request launch (critical requests; all requests under
+                                SEQUENTIAL and MULTISTREAM) as one replay of it with one completion
+                                event; 0 = launch op by op.  Normal elastic shards are launched
+                                individually either way.  FAKE backend: ignored. */
 } miriam_config;
 
 typedef struct miriam_completion {
@@ -275,6 +281,8 @@ typedef struct miriam_stats {
     int64_t decisions;        /* shard decisions taken */
     double decision_ns_total; /* host time spent deciding */
     int64_t completed;        /* requests completed */
+    int64_t graph_launches;   /* whole requests run as one replay of their task's captured graph
+                                 (each also counts its ops in `launches`) */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */

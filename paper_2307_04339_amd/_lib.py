@@ -78,6 +78,7 @@ class Config(ctypes.Structure):
         ("log_launches", ctypes.c_int32), ("profile_reps", ctypes.c_int32),
         ("fake_n_cu", ctypes.c_int32), ("fake_slots_per_cu", ctypes.c_int32),
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),
+        ("graphs", ctypes.c_int32),
     ]
 
 
@@ -104,6 +105,7 @@ class Stats(ctypes.Structure):
         ("launches", ctypes.c_int64), ("shards_sized", ctypes.c_int64),
         ("eq2_violations", ctypes.c_int64), ("decisions", ctypes.c_int64),
         ("decision_ns_total", ctypes.c_double), ("completed", ctypes.c_int64),
+        ("graph_launches", ctypes.c_int64),
     ]
 
 

@@ -50,8 +50,26 @@ struct Backend {
     virtual void release(int ev) = 0;
     virtual double time_us(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int reps) = 0;
     virtual double launch_gap_us(const miriam_op *op, int reps) = 0;
+    // Record the unsharded launch sequence of `ops` (grid = T, block 256 each) as one
+    // replayable unit; nullptr where the backend has none (then requests launch per op).
+    virtual void *capture(const std::vector<miriam_op *> &ops) { (void)ops; return nullptr; }
+    virtual int launch_captured(void *unit, int stream) { (void)unit; (void)stream; return MIRIAM_ESTATE; }
     virtual void stop() = 0;
 };
+
+// An instantiated HIP graph of one task's unsharded kernel sequence.
+struct CritGraph {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+};
+
+void free_captured(void *unit) {
+    CritGraph *cg = static_cast<CritGraph *>(unit);
+    if (!cg) return;
+    if (cg->exec) (void)hipGraphExecDestroy(cg->exec);
+    if (cg->graph) (void)hipGraphDestroy(cg->graph);
+    delete cg;
+}
 
 struct HipBackend : Backend {
     int dev = 0;
@@ -59,6 +77,8 @@ struct HipBackend : Backend {
     std::vector<hipEvent_t> events;
     std::vector<int> free_ev;
     hipStream_t prof = nullptr;
+    hipStream_t cap = nullptr;  // capture stream for task graphs (never executes work)
+    std::mutex cap_mu;
 
     int start(int n) override {
         hipError_t e = hipGetDevice(&dev);
@@ -71,6 +91,38 @@ struct HipBackend : Backend {
         }
         e = hipStreamCreateWithFlags(&prof, hipStreamNonBlocking);
         if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+        e = hipStreamCreateWithFlags(&cap, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+        return MIRIAM_OK;
+    }
+    void *capture(const std::vector<miriam_op *> &ops) override {
+        // thread-local capture: the dispatcher thread keeps launching on its own streams meanwhile
+        std::lock_guard<std::mutex> lk(cap_mu);
+        CritGraph *cg = new (std::nothrow) CritGraph();
+        if (!cg) return nullptr;
+        if (hipStreamBeginCapture(cap, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+            delete cg;
+            return nullptr;
+        }
+        bool ok = true;
+        for (const miriam_op *op : ops) {
+            const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
+            if (op_launch(op, 0, op->T, grid, 256, cap, nullptr, nullptr, nullptr) != MIRIAM_OK) {
+                ok = false;
+                break;
+            }
+        }
+        hipError_t e = hipStreamEndCapture(cap, &cg->graph);
+        if (!ok || e != hipSuccess || !cg->graph ||
+            hipGraphInstantiate(&cg->exec, cg->graph, nullptr, nullptr, 0) != hipSuccess) {
+            free_captured(cg);
+            return nullptr;
+        }
+        return cg;
+    }
+    int launch_captured(void *unit, int stream) override {
+        hipError_t e = hipGraphLaunch(static_cast<CritGraph *>(unit)->exec, streams[stream]);
+        if (e != hipSuccess) return hip_fail(e, "hipGraphLaunch");
         return MIRIAM_OK;
     }
     int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) override {
@@ -82,8 +134,11 @@ struct HipBackend : Backend {
             id = free_ev.back();
             free_ev.pop_back();
         } else {
+            // completion markers only: no timing, and a device-scope release (the host polls
+            // them and never reads kernel output through them; later device work, copies
+            // included, sees the writes), which spares a cache writeback per recorded event
             hipEvent_t ev;
-            hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventReleaseToDevice);
             if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
             events.push_back(ev);
             id = (int)events.size() - 1;
@@ -160,10 +215,12 @@ struct HipBackend : Backend {
             (void)hipStreamSynchronize(prof);
             (void)hipStreamDestroy(prof);
         }
+        if (cap) (void)hipStreamDestroy(cap);
         events.clear();
         free_ev.clear();
         streams.clear();
         prof = nullptr;
+        cap = nullptr;
     }
 };
 
@@ -240,13 +297,16 @@ struct miriam_task {
     std::vector<OpProf> prof;
     int id = 0;
     std::atomic<int> pending{0};
+    void *graph = nullptr;        // captured unsharded sequence (HIP graph), or nullptr
+    std::vector<double> end_us;   // profiled end of op i within one unsharded run
+    ~miriam_task() { free_captured(graph); }
 };
 
 namespace {
 
 struct Shot {  // one launch in flight
     int ev;
-    int op;
+    int op;         // op index, or -1 for the task's whole captured sequence
     double est_us;  // estimated duration (task profile), counted against cfg.inflight_us
 };
 
@@ -261,6 +321,9 @@ struct Req {
     size_t op = 0;       // next op to launch
     int64_t cursor = 0;  // next tile of that op
     bool launched_all = false;
+    int64_t est_gpu_start = 0;  // estimated start on the GPU of a captured sequence (after the
+                                // requests ahead of it on the same stream)
+    int64_t est_gpu_end = 0;
     std::deque<Shot> shots;
 };
 
@@ -380,8 +443,40 @@ void finish(Coord &c, Req *r) {
     c.cv_done.notify_all();
 }
 
-// Launch every op of a request unsharded (grid = T, block 256) on `stream`.
+// Launch every op of a request unsharded (grid = T, block 256) on `stream`: one replay of
+// the task's captured sequence where there is one (one host call and one completion event
+// instead of one launch and one event per op), else op by op.
 void launch_whole(Coord &c, Req *r, int stream) {
+    miriam_task *t = r->task;
+    const std::deque<Req *> &ahead = stream == 0 ? c.crit_active : c.be_active[stream];
+    const int64_t now = mono_ns();
+    r->est_gpu_start = std::max(now, ahead.empty() ? now : ahead.back()->est_gpu_end);
+    r->est_gpu_end = r->est_gpu_start + (int64_t)(1000.0 * (t->end_us.empty() ? 0.0 : t->end_us.back()));
+    if (t->graph && c.cfg.graphs) {
+        int rc = c.be->launch_captured(t->graph, stream);
+        int ev = rc == MIRIAM_OK ? c.be->record(stream) : rc;
+        if (ev < 0) {
+            r->status = ev;
+        } else {
+            const double total = t->end_us.empty() ? 0.0 : t->end_us.back();
+            r->t_start = now;
+            r->shots.push_back({ev, -1, total});
+            r->n_shards += (int)t->ops.size();
+            c.inflight[stream]++;
+            c.inflight_us[stream] += total;
+            for (size_t i = 0; i < t->ops.size(); ++i) {
+                const miriam_op *op = t->ops[i];
+                log_launch(c, r, (int)i, stream, (int)std::min<int64_t>(op->T, INT32_MAX), 256, false, 0, op->T,
+                           op->T, 0, t->prof[i].t_unsh_us);
+            }
+            std::lock_guard<std::mutex> lk(c.stat_mu);
+            c.stats.launches += (int64_t)t->ops.size();
+            c.stats.graph_launches++;
+        }
+        r->op = t->ops.size();
+        r->launched_all = true;
+        return;
+    }
     for (size_t i = 0; i < r->task->ops.size(); ++i) {
         const miriam_op *op = r->task->ops[i];
         const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
@@ -423,11 +518,27 @@ bool retire(Coord &c, std::deque<Req *> &active, int stream) {
 }
 
 // Op index of the critical kernel running now, or -1 if no critical work is in flight.
+// A captured sequence runs as one launch; its running op is inferred from the time since its
+// estimated start against the task profile (the op with the most tiles, the smallest Eq. (2)
+// grid limit, where the task has no profile).
 int current_critical_op(Coord &c, const miriam_op **op) {
     if (c.crit_active.empty()) return -1;
     Req *r = c.crit_active.front();
     if (r->shots.empty()) return -1;
-    const int oi = r->shots.front().op;
+    int oi = r->shots.front().op;
+    if (oi < 0) {
+        const miriam_task *t = r->task;
+        const int n = (int)t->ops.size();
+        if (t->end_us.empty() || !(t->end_us.back() > 0.0)) {
+            oi = 0;
+            for (int i = 1; i < n; ++i)
+                if (t->ops[i]->T > t->ops[oi]->T) oi = i;
+        } else {
+            const double el = 1e-3 * (double)(mono_ns() - r->est_gpu_start);
+            oi = 0;
+            while (oi < n - 1 && t->end_us[oi] <= el) ++oi;
+        }
+    }
     *op = r->task->ops[oi];
     return oi;
 }
@@ -715,6 +826,9 @@ void profile_task(Coord &c, miriam_task *t) {
         p.n_max = 1 + (int64_t)std::floor(budget / std::max(1e-3, c.t_launch_us));
         p.n_max = std::max<int64_t>(1, std::min<int64_t>(p.n_max, op->T));
     }
+    t->end_us.assign(t->ops.size(), 0.0);
+    double acc = 0.0;
+    for (size_t i = 0; i < t->ops.size(); ++i) t->end_us[i] = (acc += std::max(0.0, t->prof[i].t_unsh_us));
 }
 
 }  // namespace
@@ -733,7 +847,8 @@ int miriam_init(const miriam_config *cfg) {
     if (cfg->policy < 0 || cfg->policy > 2 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
-        cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2) {
+        cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
+        cfg->graphs > 1) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -801,6 +916,7 @@ int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out) {
     t->prof.resize(n_ops);
     t->id = g->next_task_id++;
     profile_task(*g, t);
+    if (g->cfg.graphs) t->graph = g->be->capture(t->ops);  // nullptr: launched op by op
     *out = t;
     return MIRIAM_OK;
 }

@@ -1,0 +1,65 @@
+"""The coordinator on the GPU: under every policy, with whole-request launches
+replayed from captured HIP graphs or issued op by op, the networks' outputs are
+bitwise identical to one eager forward pass, on every replay, with eager device
+work between replays; a captured request is one launch that still accounts for
+each of its ops, and normal shards sized next to it keep the Eq. (2) limit."""
+import pytest
+import torch
+
+from gpu_util import bits, gpu_available
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X")]
+
+
+def _nan_outputs(net):
+    for l in net.layers:
+        l.t["y"].fill_(float("nan"))
+
+
+@pytest.mark.parametrize("graphs", [0, 1])
+@pytest.mark.parametrize("policy", ["elastic", "sequential", "multistream"])
+def test_coordinator_outputs_match_eager(policy, graphs):
+    from paper_2307_04339_amd import models
+    from paper_2307_04339_amd.runtime import Coordinator
+    crit = models.resnet18(batch=1, dtype="f16")
+    be = models.mobilenetv2(batch=4, dtype="bf16")
+    for n in (crit, be):
+        n.forward()
+    torch.cuda.synchronize()
+    ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
+    co = Coordinator(policy=policy, graphs=graphs, profile_reps=1, log_launches=1, n_be_streams=1,
+                     inflight_depth=2, quantum_us=20.0)
+    try:
+        ct = co.task(crit.ops())
+        bt = co.task(be.ops())
+        reps = 3
+        for rep in range(reps):
+            _nan_outputs(crit)
+            _nan_outputs(be)
+            junk = torch.randn(1 << 20, device="cuda")
+            float((junk * 2.0).sum())  # eager device work between replays
+            torch.cuda.synchronize()
+            tb = co.submit(bt, False)
+            tc = co.submit(ct, True)
+            tb2 = co.submit(bt, False)
+            co.drain(60000)
+            recs = {r.ticket: r for r in co.poll()}
+            assert set(recs) == {tb, tc, tb2}
+            assert all(r.status == 0 for r in recs.values())
+            assert recs[tc].n_shards == len(crit.layers)
+            torch.cuda.synchronize()
+            for n in (crit, be):
+                for l, r in zip(n.layers, ref[n.name]):
+                    assert bits(l.t["y"]) == r, (policy, graphs, rep, n.name, l.name)
+        st = co.stats()
+        log = co.launch_log()
+        crit_recs = [r for r in log if r.criticality == 1]
+        assert len(crit_recs) == reps * len(crit.layers)
+        assert all(r.shard_begin == 0 and r.shard_len == r.num_tiles and r.block == 256 for r in crit_recs)
+        assert st.launches == len(log)
+        assert st.eq2_violations == 0
+        whole = reps * (3 if policy != "elastic" else 1)  # requests launched unsharded
+        assert st.graph_launches == (whole if graphs else 0)
+    finally:
+        co.shutdown()
