@@ -340,6 +340,9 @@ def main():
                     help="normal shards next to a running critical kernel: 0 paper rule, 1 none, 2 smallest")
     ap.add_argument("--graphs", type=int, default=1, choices=(0, 1),
                     help="1: whole-request launches replay each task's captured HIP graph")
+    ap.add_argument("--release-guard", type=int, default=-1, choices=(-1, 0, 1),
+                    help="1: hold normal shards that would still run at the next timed critical "
+                         "release; -1: on for periodic arrivals (release times known ahead), off for Poisson")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
@@ -405,8 +408,9 @@ def main():
     del flush
     torch.cuda.empty_cache()
 
+    guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
-                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs)
+                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
         if ph not in phases:
@@ -443,7 +447,7 @@ def main():
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
                    "inflight_us": args.inflight_us, "busy_policy": args.busy_policy,
-                   "graphs": args.graphs},
+                   "graphs": args.graphs, "release_guard": guard},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

@@ -260,6 +260,10 @@ typedef struct miriam_config {
                                 SEQUENTIAL and MULTISTREAM) as one replay of it with one completion
                                 event; 0 = launch op by op.  Normal elastic shards are launched
                                 individually either way.  FAKE backend: ignored. */
+    int32_t release_guard;   /* 1 = while no critical work runs, issue a normal shard only if the
+                                normal work queued on the GPU plus that shard (estimated from the
+                                task profiles) ends before the next timed critical release already
+                                submitted; 0 = ignore future releases */
 } miriam_config;
 
 typedef struct miriam_completion {

@@ -78,7 +78,7 @@ class Config(ctypes.Structure):
         ("log_launches", ctypes.c_int32), ("profile_reps", ctypes.c_int32),
         ("fake_n_cu", ctypes.c_int32), ("fake_slots_per_cu", ctypes.c_int32),
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),
-        ("graphs", ctypes.c_int32),
+        ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32),
     ]
 
 

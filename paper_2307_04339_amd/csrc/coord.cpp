@@ -23,6 +23,7 @@
 #include <cstring>
 #include <ctime>
 #include <deque>
+#include <functional>
 #include <mutex>
 #include <new>
 #include <queue>
@@ -355,6 +356,7 @@ struct Coord {
 
     // dispatcher-owned state
     std::priority_queue<Req *, std::vector<Req *>, ReleaseLater> timed;
+    std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> crit_timed;  // their releases
     std::vector<Req *> crit_ready;                 // released critical requests
     std::vector<std::deque<Req *>> norm_ready;     // per stream, FIFO
     std::deque<Req *> crit_active;                 // launched critical requests, stream 0
@@ -650,6 +652,9 @@ bool pump_normal(Coord &c, int s) {
         const bool busy = current_critical_op(c, &crit_op) >= 0;
         if (busy && c.cfg.busy_policy == 1) break;  // ablation: hold normal work back
         Decision d = decide(c, r, busy ? crit_op : nullptr);
+        if (!busy && c.cfg.release_guard && !c.crit_timed.empty() &&
+            t0 + (int64_t)(1000.0 * (queued_normal_us(c) + d.est_us)) > c.crit_timed.top())
+            break;  // the GPU would still hold this shard when the next critical request is released
         const int64_t t1 = mono_ns();
         const int oi = (int)r->op;
         int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit, d.est_us);
@@ -696,7 +701,10 @@ void dispatcher(Coord *cp) {
     for (;;) {
         {
             std::unique_lock<std::mutex> lk(c.mu);
-            for (Req *r : c.inbox) c.timed.push(r);
+            for (Req *r : c.inbox) {
+                c.timed.push(r);
+                if (r->crit) c.crit_timed.push(r->release);
+            }
             c.inbox.clear();
             if (c.stopping && c.outstanding == 0) break;
         }
@@ -707,6 +715,7 @@ void dispatcher(Coord *cp) {
             if (r->crit) c.crit_ready.push_back(r);
             else c.norm_ready[r->stream].push_back(r);
         }
+        while (!c.crit_timed.empty() && c.crit_timed.top() <= now) c.crit_timed.pop();
         bool progress = false;
         // retire finished work
         progress |= retire(c, c.crit_active, 0);
@@ -848,7 +857,7 @@ int miriam_init(const miriam_config *cfg) {
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
-        cfg->graphs > 1) {
+        cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }

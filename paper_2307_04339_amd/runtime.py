@@ -34,6 +34,7 @@ def default_config(**kw) -> L.Config:
     c.fake_tile_ns = 1000.0
     c.fake_launch_ns = 2000.0
     c.graphs = 1
+    c.release_guard = 0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

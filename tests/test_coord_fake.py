@@ -221,3 +221,32 @@ def test_bad_configs_rejected(L):
                 dict(busy_policy=3)]:
         c = default_config(**dict(dict(backend="fake"), **bad))
         assert lib.miriam_init(ctypes.byref(c)) == L.EINVAL, bad
+
+
+@pytest.mark.parametrize("guard", [0, 1])
+def test_release_guard_keeps_normal_work_clear_of_timed_releases(L, guard):
+    co = _coord(release_guard=guard, busy_policy=1, inflight_depth=4, quantum_us=100.0)
+    try:
+        be = co.task(_net(L, [20000, 20000]))
+        cr = co.task(_net(L, [4]))
+        now = co.now_ns()
+        rels = [now + 4_000_000 + k * 2_000_000 for k in range(3)]
+        for _ in range(3):
+            co.submit(be, False)
+        tks = [co.submit(cr, True, release_ns=r) for r in rels]
+        got = {r.ticket: r for r in _collect(co, 6)}
+        assert len(got) == 6 and all(r.status == 0 for r in got.values())
+        log = [r for r in co.launch_log() if r.criticality == 0]
+        assert log
+        late = 0
+        for rel in rels:
+            before = [r for r in log if r.t_issue_ns < rel]
+            assert before  # normal work runs up to each release
+            # a shard issued before a release is estimated to end by it (launch and logging slack)
+            late += sum(1 for r in before if r.t_issue_ns + 1000.0 * r.est_us > rel + 20_000)
+        if guard:
+            assert late == 0
+        for tk, rel in zip(tks, rels):
+            assert got[tk].t_start_ns >= rel
+    finally:
+        co.shutdown()
