@@ -343,6 +343,12 @@ def main():
     ap.add_argument("--release-guard", type=int, default=-1, choices=(-1, 0, 1),
                     help="1: hold normal shards that would still run at the next timed critical "
                          "release; -1: on for periodic arrivals (release times known ahead), off for Poisson")
+    ap.add_argument("--warm-critical", type=int, default=-1, choices=(-1, 0, 1),
+                    help="1: warm the critical task's parameters in the caches ahead of each release "
+                         "(needs the release guard); -1: follow the release guard")
+    ap.add_argument("--arm-lead-us", type=float, default=-1.0,
+                    help="queue each timed critical request behind a gate this long before its release "
+                         "(0 = launch at the release); -1: 500 with the release guard, else 0")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
@@ -409,8 +415,11 @@ def main():
     torch.cuda.empty_cache()
 
     guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
+    warm = args.warm_critical if args.warm_critical >= 0 else guard
+    arm = args.arm_lead_us if args.arm_lead_us >= 0 else (500.0 if guard else 0.0)
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
-                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard)
+                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
+                warm_critical=warm, arm_lead_us=arm)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
         if ph not in phases:
@@ -447,7 +456,8 @@ def main():
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
                    "inflight_us": args.inflight_us, "busy_policy": args.busy_policy,
-                   "graphs": args.graphs, "release_guard": guard},
+                   "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
+                   "arm_lead_us": arm},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

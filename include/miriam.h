@@ -264,6 +264,21 @@ typedef struct miriam_config {
                                 normal work queued on the GPU plus that shard (estimated from the
                                 task profiles) ends before the next timed critical release already
                                 submitted; 0 = ignore future releases */
+    int32_t warm_critical;   /* with release_guard: when normal work is first held for a critical
+                                release, queue a kernel that reads the critical task's parameters
+                                (weights, bias, normalisation vectors) behind the normal work in
+                                flight (on the normal stream with the most), so the request finds
+                                them in the caches;
+                                the guard reserves its estimated time.  The task then owns a small
+                                device table of its parameter ranges. */
+    int32_t graph_chunk;     /* with graphs: most kernels per captured graph (a task's sequence is
+                                captured as consecutive graphs launched back to back); 0 = one
+                                graph per task */
+    double arm_lead_us;      /* ELASTIC: this long before a timed critical release, queue the request's
+                                kernels on the critical stream behind a one-wave gate kernel that
+                                waits for a flag the dispatcher raises at the release (the gate gives
+                                up 2 ms after the release at the latest); 0 = launch at the release.
+                                Critical work released in between waits behind the gate. */
 } miriam_config;
 
 typedef struct miriam_completion {
@@ -287,6 +302,8 @@ typedef struct miriam_stats {
     int64_t completed;        /* requests completed */
     int64_t graph_launches;   /* whole requests run as one replay of their task's captured graph
                                  (each also counts its ops in `launches`) */
+    int64_t warm_launches;    /* cache-warming kernels queued ahead of critical releases */
+    int64_t armed_releases;   /* critical requests queued behind a gate ahead of their release */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */

@@ -78,7 +78,8 @@ class Config(ctypes.Structure):
         ("log_launches", ctypes.c_int32), ("profile_reps", ctypes.c_int32),
         ("fake_n_cu", ctypes.c_int32), ("fake_slots_per_cu", ctypes.c_int32),
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),
-        ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32),
+        ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32), ("warm_critical", ctypes.c_int32),
+        ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
     ]
 
 
@@ -105,7 +106,8 @@ class Stats(ctypes.Structure):
         ("launches", ctypes.c_int64), ("shards_sized", ctypes.c_int64),
         ("eq2_violations", ctypes.c_int64), ("decisions", ctypes.c_int64),
         ("decision_ns_total", ctypes.c_double), ("completed", ctypes.c_int64),
-        ("graph_launches", ctypes.c_int64),
+        ("graph_launches", ctypes.c_int64), ("warm_launches", ctypes.c_int64),
+        ("armed_releases", ctypes.c_int64),
     ]
 
 

@@ -53,8 +53,24 @@ struct Backend {
     virtual double launch_gap_us(const miriam_op *op, int reps) = 0;
     // Record the unsharded launch sequence of `ops` (grid = T, block 256 each) as one
     // replayable unit; nullptr where the backend has none (then requests launch per op).
-    virtual void *capture(const std::vector<miriam_op *> &ops) { (void)ops; return nullptr; }
+    virtual void *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) {
+        (void)ops; (void)i0; (void)i1;
+        return nullptr;
+    }
     virtual int launch_captured(void *unit, int stream) { (void)unit; (void)stream; return MIRIAM_ESTATE; }
+    // Run the cache-warming kernel over a device table of ranges on `stream`, after the
+    // recorded events `waits` (work already queued on other streams) have completed.
+    virtual int warm(const WarmRange *table, int n, int grid, int *sink, int stream, const std::vector<int> &waits) {
+        (void)table; (void)n; (void)grid; (void)sink; (void)stream; (void)waits;
+        return MIRIAM_OK;
+    }
+    // Queue a gate on `stream`: the stream's later work waits until open_gates(>= seq) or
+    // until limit_ns have passed.  A simulated device models the gate as ending at release_ns.
+    virtual int gate(uint64_t seq, int64_t release_ns, int64_t limit_ns, int stream) {
+        (void)seq; (void)release_ns; (void)limit_ns; (void)stream;
+        return MIRIAM_ESTATE;
+    }
+    virtual void open_gates(uint64_t seq) { (void)seq; }
     virtual void stop() = 0;
 };
 
@@ -80,6 +96,9 @@ struct HipBackend : Backend {
     hipStream_t prof = nullptr;
     hipStream_t cap = nullptr;  // capture stream for task graphs (never executes work)
     std::mutex cap_mu;
+    uint64_t *gate_host = nullptr;  // gate flag in coherent host memory, and its device address
+    uint64_t *gate_dev = nullptr;
+    int wall_khz = 0;               // device wall-clock rate
 
     int start(int n) override {
         hipError_t e = hipGetDevice(&dev);
@@ -94,9 +113,27 @@ struct HipBackend : Backend {
         if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
         e = hipStreamCreateWithFlags(&cap, hipStreamNonBlocking);
         if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+        e = hipHostMalloc(reinterpret_cast<void **>(&gate_host), 64, hipHostMallocCoherent | hipHostMallocMapped);
+        if (e != hipSuccess) {
+            gate_host = nullptr;
+            return hip_fail(e, "hipHostMalloc (gate flag)");
+        }
+        __atomic_store_n(gate_host, (uint64_t)0, __ATOMIC_RELEASE);
+        e = hipHostGetDevicePointer(reinterpret_cast<void **>(&gate_dev), gate_host, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer (gate flag)");
+        e = hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, dev);
+        if (e != hipSuccess || wall_khz <= 0) return hip_fail(e, "wall clock rate");
         return MIRIAM_OK;
     }
-    void *capture(const std::vector<miriam_op *> &ops) override {
+    int gate(uint64_t seq, int64_t release_ns, int64_t limit_ns, int stream) override {
+        (void)release_ns;
+        const uint64_t ticks = (uint64_t)std::max<int64_t>(0, limit_ns) * (uint64_t)wall_khz / 1000000u;
+        return gate_launch(gate_dev, seq, ticks, streams[stream]);
+    }
+    void open_gates(uint64_t seq) override {
+        if (gate_host) __atomic_store_n(gate_host, seq, __ATOMIC_RELEASE);
+    }
+    void *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) override {
         // thread-local capture: the dispatcher thread keeps launching on its own streams meanwhile
         std::lock_guard<std::mutex> lk(cap_mu);
         CritGraph *cg = new (std::nothrow) CritGraph();
@@ -106,7 +143,8 @@ struct HipBackend : Backend {
             return nullptr;
         }
         bool ok = true;
-        for (const miriam_op *op : ops) {
+        for (size_t i = i0; i < i1; ++i) {
+            const miriam_op *op = ops[i];
             const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
             if (op_launch(op, 0, op->T, grid, 256, cap, nullptr, nullptr, nullptr) != MIRIAM_OK) {
                 ok = false;
@@ -120,6 +158,13 @@ struct HipBackend : Backend {
             return nullptr;
         }
         return cg;
+    }
+    int warm(const WarmRange *table, int n, int grid, int *sink, int stream, const std::vector<int> &waits) override {
+        for (int ev : waits) {
+            hipError_t e = hipStreamWaitEvent(streams[stream], events[ev], 0);
+            if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        }
+        return warm_launch(table, n, grid, sink, streams[stream]);
     }
     int launch_captured(void *unit, int stream) override {
         hipError_t e = hipGraphLaunch(static_cast<CritGraph *>(unit)->exec, streams[stream]);
@@ -209,6 +254,7 @@ struct HipBackend : Backend {
         return best;
     }
     void stop() override {
+        open_gates(UINT64_MAX);
         for (hipStream_t s : streams) (void)hipStreamSynchronize(s);
         for (hipEvent_t e : events) (void)hipEventDestroy(e);
         for (hipStream_t s : streams) (void)hipStreamDestroy(s);
@@ -217,6 +263,8 @@ struct HipBackend : Backend {
             (void)hipStreamDestroy(prof);
         }
         if (cap) (void)hipStreamDestroy(cap);
+        if (gate_host) (void)hipHostFree(gate_host);
+        gate_host = gate_dev = nullptr;
         events.clear();
         free_ev.clear();
         streams.clear();
@@ -275,6 +323,10 @@ struct FakeBackend : Backend {
         return duration(op, l, grid) / 1000.0;
     }
     double launch_gap_us(const miriam_op *, int) override { return launch_ns / 1000.0; }
+    int gate(uint64_t, int64_t release_ns, int64_t, int stream) override {
+        busy_until[stream] = std::max(std::max(busy_until[stream], mono_ns()), release_ns);
+        return MIRIAM_OK;
+    }
     void stop() override {}
 };
 
@@ -298,9 +350,18 @@ struct miriam_task {
     std::vector<OpProf> prof;
     int id = 0;
     std::atomic<int> pending{0};
-    void *graph = nullptr;        // captured unsharded sequence (HIP graph), or nullptr
+    std::vector<void *> graphs;   // captured unsharded sequence (HIP graphs of consecutive ops), or empty
     std::vector<double> end_us;   // profiled end of op i within one unsharded run
-    ~miriam_task() { free_captured(graph); }
+    // parameter lines touched before a release (cache warming): device table of ranges and a
+    // sink word (HIP backend), their line count and estimated duration
+    void *warm_dev = nullptr;
+    int warm_n = 0, warm_grid = 0;
+    int64_t warm_lines = 0;
+    double warm_us = 0.0;
+    ~miriam_task() {
+        for (void *gph : graphs) free_captured(gph);
+        if (warm_dev) (void)hipFree(warm_dev);
+    }
 };
 
 namespace {
@@ -325,6 +386,7 @@ struct Req {
     int64_t est_gpu_start = 0;  // estimated start on the GPU of a captured sequence (after the
                                 // requests ahead of it on the same stream)
     int64_t est_gpu_end = 0;
+    uint64_t gate = 0;  // armed: the gate its kernels wait behind (opened at the release)
     std::deque<Shot> shots;
 };
 
@@ -356,7 +418,11 @@ struct Coord {
 
     // dispatcher-owned state
     std::priority_queue<Req *, std::vector<Req *>, ReleaseLater> timed;
-    std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> crit_timed;  // their releases
+    std::priority_queue<Req *, std::vector<Req *>, ReleaseLater> crit_timed;  // the critical ones among them
+    uint64_t warmed_ticket = 0;                    // critical request whose parameters were last warmed
+    Req *armed = nullptr;                          // timed critical request queued behind a gate
+    uint64_t gate_seq = 0;
+    std::vector<int> last_ev;                      // event of the latest launch per stream
     std::vector<Req *> crit_ready;                 // released critical requests
     std::vector<std::deque<Req *>> norm_ready;     // per stream, FIFO
     std::deque<Req *> crit_active;                 // launched critical requests, stream 0
@@ -409,6 +475,7 @@ int issue(Coord &c, Req *r, int oi, int64_t b, int64_t l, int grid, int block, i
     if (ev < 0) return ev;
     if (r->t_start == 0) r->t_start = mono_ns();
     r->shots.push_back({ev, oi, est_us});
+    c.last_ev[stream] = ev;
     r->n_shards++;
     c.inflight[stream]++;
     c.inflight_us[stream] += est_us;
@@ -454,8 +521,9 @@ void launch_whole(Coord &c, Req *r, int stream) {
     const int64_t now = mono_ns();
     r->est_gpu_start = std::max(now, ahead.empty() ? now : ahead.back()->est_gpu_end);
     r->est_gpu_end = r->est_gpu_start + (int64_t)(1000.0 * (t->end_us.empty() ? 0.0 : t->end_us.back()));
-    if (t->graph && c.cfg.graphs) {
-        int rc = c.be->launch_captured(t->graph, stream);
+    if (!t->graphs.empty() && c.cfg.graphs) {
+        int rc = MIRIAM_OK;
+        for (size_t k = 0; k < t->graphs.size() && rc == MIRIAM_OK; ++k) rc = c.be->launch_captured(t->graphs[k], stream);
         int ev = rc == MIRIAM_OK ? c.be->record(stream) : rc;
         if (ev < 0) {
             r->status = ev;
@@ -463,6 +531,7 @@ void launch_whole(Coord &c, Req *r, int stream) {
             const double total = t->end_us.empty() ? 0.0 : t->end_us.back();
             r->t_start = now;
             r->shots.push_back({ev, -1, total});
+            c.last_ev[stream] = ev;
             r->n_shards += (int)t->ops.size();
             c.inflight[stream]++;
             c.inflight_us[stream] += total;
@@ -629,6 +698,22 @@ double queued_normal_us(const Coord &c) {
     return t;
 }
 
+// Queue the cache-warming kernel over critical request nx's parameters on the normal stream
+// with the most work queued, so that it runs once that work has drained.
+void warm_for(Coord &c, const Req *nx) {
+    c.warmed_ticket = nx->ticket;
+    const miriam_task *t = nx->task;
+    if (t->warm_n < 1) return;
+    int s = 1;
+    for (int k = 2; k < c.n_streams; ++k)
+        if (c.inflight_us[k] > c.inflight_us[s]) s = k;
+    char *base = static_cast<char *>(t->warm_dev);
+    int rc = c.be->warm(reinterpret_cast<const WarmRange *>(base), t->warm_n, t->warm_grid,
+                        base ? reinterpret_cast<int *>(base + sizeof(WarmRange) * t->warm_n) : nullptr, s, {});
+    std::lock_guard<std::mutex> lk(c.stat_mu);
+    if (rc == MIRIAM_OK) c.stats.warm_launches++;
+}
+
 // Issue shards for the normal requests of one stream while the in-flight budget lasts
 // (every stream may keep one shard in flight; beyond that the budget is shared).
 bool pump_normal(Coord &c, int s) {
@@ -652,9 +737,18 @@ bool pump_normal(Coord &c, int s) {
         const bool busy = current_critical_op(c, &crit_op) >= 0;
         if (busy && c.cfg.busy_policy == 1) break;  // ablation: hold normal work back
         Decision d = decide(c, r, busy ? crit_op : nullptr);
-        if (!busy && c.cfg.release_guard && !c.crit_timed.empty() &&
-            t0 + (int64_t)(1000.0 * (queued_normal_us(c) + d.est_us)) > c.crit_timed.top())
-            break;  // the GPU would still hold this shard when the next critical request is released
+        if (!busy && c.cfg.release_guard && !c.crit_timed.empty()) {
+            const Req *nx = c.crit_timed.top();
+            const double warm_us = c.cfg.warm_critical ? nx->task->warm_us : 0.0;
+            if (c.warmed_ticket == nx->ticket ||
+                t0 + (int64_t)(1000.0 * (queued_normal_us(c) + d.est_us + warm_us)) > nx->release) {
+                // the GPU would still hold this shard when the next critical request is released:
+                // hold normal work from here to that release, and warm the request's parameters
+                // once the normal work already queued has drained
+                if (c.cfg.warm_critical && c.warmed_ticket != nx->ticket) warm_for(c, nx);
+                break;
+            }
+        }
         const int64_t t1 = mono_ns();
         const int oi = (int)r->op;
         int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit, d.est_us);
@@ -690,6 +784,31 @@ bool all_idle(Coord &c) {
     return true;
 }
 
+// The gate of an armed request gives up this long after the release at the latest.
+constexpr int64_t kGateSlackNs = 2000000;
+
+// Queue timed critical request nx on the critical stream ahead of its release, behind a gate
+// that the dispatcher opens at the release: the launch calls then cost the request nothing.
+// Work released on the critical stream in the meantime waits behind the gate.
+bool arm(Coord &c, Req *nx) {
+    const int64_t now = mono_ns();
+    const uint64_t seq = c.gate_seq + 1;
+    if (c.be->gate(seq, nx->release, nx->release - now + kGateSlackNs, 0) != MIRIAM_OK) {
+        c.cfg.arm_lead_us = 0.0;  // no gates on this backend: launch at the release
+        return false;
+    }
+    c.gate_seq = seq;
+    nx->gate = seq;
+    launch_whole(c, nx, 0);
+    nx->t_start = 0;  // set when the gate opens
+    nx->est_gpu_start = std::max(nx->est_gpu_start, nx->release);
+    nx->est_gpu_end = nx->est_gpu_start + (int64_t)(1000.0 * (nx->task->end_us.empty() ? 0.0 : nx->task->end_us.back()));
+    c.armed = nx;
+    std::lock_guard<std::mutex> lk(c.stat_mu);
+    c.stats.armed_releases++;
+    return true;
+}
+
 // The dispatcher sleeps only until this long before a timed release; the rest is spun.
 constexpr int64_t kWakeEarlyNs = 300000;
 
@@ -703,7 +822,7 @@ void dispatcher(Coord *cp) {
             std::unique_lock<std::mutex> lk(c.mu);
             for (Req *r : c.inbox) {
                 c.timed.push(r);
-                if (r->crit) c.crit_timed.push(r->release);
+                if (r->crit) c.crit_timed.push(r);
             }
             c.inbox.clear();
             if (c.stopping && c.outstanding == 0) break;
@@ -712,11 +831,23 @@ void dispatcher(Coord *cp) {
         while (!c.timed.empty() && c.timed.top()->release <= now) {
             Req *r = c.timed.top();
             c.timed.pop();
-            if (r->crit) c.crit_ready.push_back(r);
-            else c.norm_ready[r->stream].push_back(r);
+            if (r == c.armed) {  // its kernels are queued: open the gate
+                c.be->open_gates(r->gate);
+                r->t_start = mono_ns();
+                c.crit_active.push_back(r);
+                c.armed = nullptr;
+            } else if (r->crit) {
+                c.crit_ready.push_back(r);
+            } else {
+                c.norm_ready[r->stream].push_back(r);
+            }
         }
-        while (!c.crit_timed.empty() && c.crit_timed.top() <= now) c.crit_timed.pop();
+        while (!c.crit_timed.empty() && c.crit_timed.top()->release <= now) c.crit_timed.pop();
         bool progress = false;
+        if (c.cfg.arm_lead_us > 0.0 && c.cfg.policy == MIRIAM_POLICY_ELASTIC && !c.armed && !c.crit_timed.empty()) {
+            Req *nx = c.crit_timed.top();
+            if (nx->release > now && nx->release - now <= (int64_t)(1000.0 * c.cfg.arm_lead_us)) progress |= arm(c, nx);
+        }
         // retire finished work
         progress |= retire(c, c.crit_active, 0);
         for (int s = 1; s < c.n_streams; ++s) progress |= retire(c, c.be_active[s], s);
@@ -787,7 +918,8 @@ void dispatcher(Coord *cp) {
                     // sleep until shortly before the next timed release, then spin to it
                     int64_t wait_ns = 2000000;
                     if (!c.timed.empty()) wait_ns = std::min<int64_t>(wait_ns, c.timed.top()->release - mono_ns());
-                    if (wait_ns > kWakeEarlyNs) c.cv.wait_for(lk, std::chrono::nanoseconds(wait_ns - kWakeEarlyNs));
+                    const int64_t early = std::max<int64_t>(kWakeEarlyNs, (int64_t)(1000.0 * c.cfg.arm_lead_us) + 100000);
+                    if (wait_ns > early) c.cv.wait_for(lk, std::chrono::nanoseconds(wait_ns - early));
                 }
             } else {
                 std::this_thread::yield();
@@ -840,6 +972,39 @@ void profile_task(Coord &c, miriam_task *t) {
     for (size_t i = 0; i < t->ops.size(); ++i) t->end_us[i] = (acc += std::max(0.0, t->prof[i].t_unsh_us));
 }
 
+// Line table of the task's parameters (each distinct range once) for cache warming; its
+// duration is estimated at 4 TB/s plus a launch.
+int build_warm(Coord &c, miriam_task *t) {
+    std::vector<WarmRange> tab;
+    std::vector<const void *> seen;
+    for (const miriam_op *op : t->ops) {
+        const void *p[3];
+        int64_t b[3];
+        const int n = op_param_ranges(op, p, b);
+        for (int i = 0; i < n; ++i) {
+            if (std::find(seen.begin(), seen.end(), p[i]) != seen.end()) continue;
+            seen.push_back(p[i]);
+            const uintptr_t a0 = reinterpret_cast<uintptr_t>(p[i]) & ~(uintptr_t)63;
+            const uintptr_t a1 = reinterpret_cast<uintptr_t>(p[i]) + (uintptr_t)b[i];
+            tab.push_back({reinterpret_cast<const char *>(a0), (int64_t)((a1 - a0 + 63) / 64)});
+            t->warm_lines += tab.back().lines;
+        }
+    }
+    t->warm_n = (int)tab.size();
+    t->warm_us = 3.0 + 64.0 * (double)t->warm_lines / 4.0e6;
+    t->warm_grid = (int)std::max<int64_t>(1, std::min<int64_t>(4 * c.n_cu, (t->warm_lines + 2047) / 2048));
+    if (c.cfg.backend != MIRIAM_BACKEND_HIP || tab.empty()) return MIRIAM_OK;
+    const size_t bytes = sizeof(WarmRange) * tab.size() + 64;
+    hipError_t e = hipMalloc(&t->warm_dev, bytes);
+    if (e != hipSuccess) {
+        t->warm_dev = nullptr;
+        return hip_fail(e, "hipMalloc (warm table)");
+    }
+    e = hipMemcpy(t->warm_dev, tab.data(), sizeof(WarmRange) * tab.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy (warm table)");
+    return MIRIAM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -857,7 +1022,8 @@ int miriam_init(const miriam_config *cfg) {
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
-        cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1) {
+        cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
+        cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0)) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -899,6 +1065,7 @@ int miriam_init(const miriam_config *cfg) {
     c->be_active.resize(c->n_streams);
     c->inflight.assign(c->n_streams, 0);
     c->inflight_us.assign(c->n_streams, 0.0);
+    c->last_ev.assign(c->n_streams, -1);
     g = c;
     c->th = std::thread(dispatcher, c);
     return MIRIAM_OK;
@@ -925,7 +1092,25 @@ int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out) {
     t->prof.resize(n_ops);
     t->id = g->next_task_id++;
     profile_task(*g, t);
-    if (g->cfg.graphs) t->graph = g->be->capture(t->ops);  // nullptr: launched op by op
+    if (g->cfg.graphs) {  // no graph: launched op by op
+        const size_t n = t->ops.size(), chunk = g->cfg.graph_chunk > 0 ? (size_t)g->cfg.graph_chunk : n;
+        for (size_t i0 = 0; i0 < n; i0 += chunk) {
+            void *gph = g->be->capture(t->ops, i0, std::min(n, i0 + chunk));
+            if (!gph) {
+                for (void *q : t->graphs) free_captured(q);
+                t->graphs.clear();
+                break;
+            }
+            t->graphs.push_back(gph);
+        }
+    }
+    if (g->cfg.warm_critical) {
+        int rc = build_warm(*g, t);
+        if (rc != MIRIAM_OK) {
+            delete t;
+            return rc;
+        }
+    }
     *out = t;
     return MIRIAM_OK;
 }

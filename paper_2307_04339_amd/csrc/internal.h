@@ -49,4 +49,23 @@ namespace miriam {
 // Launch helper used by the public entry points and by the coordinator.
 int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
               int32_t *owner_wg, int32_t *owner_iter, int32_t *count);
+
+// Read-only parameter ranges of an op (weights, bias, batch-norm and layer-norm vectors)
+// that every request reads again: up to 3 (pointer, bytes) pairs; returns the count.
+// Operands that change per request (activations, batched right operands) are not listed.
+int op_param_ranges(const miriam_op *op, const void *ptr[3], int64_t bytes[3]);
+
+// One range of whole 64-byte lines for the cache-warming kernel.
+struct WarmRange {
+    const char *line0;  // first line (address rounded down to 64 bytes)
+    int64_t lines;      // lines to touch
+};
+
+// Touch one word of every line of the `n` ranges of the device table `table` (grid x 256
+// threads) on stream `st`; `sink` is a device word the kernel may write (never read back).
+int warm_launch(const WarmRange *table, int n, int grid, int *sink, hipStream_t st);
+
+// One-wave kernel on `st` that returns once *flag (coherent host memory, device address)
+// reaches `seq` or `limit_ticks` ticks of the device wall clock have passed.
+int gate_launch(const uint64_t *flag, uint64_t seq, uint64_t limit_ticks, hipStream_t st);
 }  // namespace miriam

@@ -1,0 +1,56 @@
+// Kernels that prepare a timed critical release.
+//
+// warm_kernel: read one word of every 64-byte line of a list of device ranges, so that a
+// kernel launched after it finds those lines in the L2 and memory-side caches instead of
+// HBM.  The coordinator runs it over a critical task's parameters just before the task's
+// release, once the co-running work that evicted them has drained.
+//
+// gate_kernel: one wave that holds back the rest of its stream until the host raises a
+// flag in coherent host memory to at least `seq`, or until `limit` ticks of the constant
+// wall clock have passed (so it always exits).  The coordinator queues a critical
+// request's kernels behind a gate ahead of the release and raises the flag at the release,
+// which takes the host-side launch calls off the request's latency.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace miriam {
+
+__global__ __launch_bounds__(256) void warm_kernel(const WarmRange *table, int n, int *sink) {
+    const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t nt = (int64_t)gridDim.x * 256;
+    unsigned acc = 0;
+    for (int i = 0; i < n; ++i) {
+        const char *p = table[i].line0;
+        const int64_t lines = table[i].lines;
+        for (int64_t l = tid; l < lines; l += nt) acc += *reinterpret_cast<const unsigned *>(p + l * 64);
+    }
+    // keeps the loads: the sum is not known at compile time
+    if (acc == 0x9e3779b9u) sink[0] = (int)acc;
+}
+
+__global__ __launch_bounds__(64) void gate_kernel(const uint64_t *flag, uint64_t seq, uint64_t limit) {
+    if (threadIdx.x != 0) return;
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) < seq) {
+        if (wall_clock64() - t0 > limit) break;
+        __builtin_amdgcn_s_sleep(4);
+    }
+}
+
+int warm_launch(const WarmRange *table, int n, int grid, int *sink, hipStream_t st) {
+    if (n < 1 || grid < 1) return MIRIAM_OK;
+    void *args[3] = {&table, &n, &sink};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&warm_kernel), dim3(grid), dim3(256), args, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "warm kernel launch");
+    return MIRIAM_OK;
+}
+
+int gate_launch(const uint64_t *flag, uint64_t seq, uint64_t limit_ticks, hipStream_t st) {
+    void *args[3] = {&flag, &seq, &limit_ticks};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&gate_kernel), dim3(1), dim3(64), args, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "gate kernel launch");
+    return MIRIAM_OK;
+}
+
+}  // namespace miriam

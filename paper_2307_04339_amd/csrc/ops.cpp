@@ -399,6 +399,37 @@ int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hi
     return MIRIAM_OK;
 }
 
+int op_param_ranges(const miriam_op *op, const void *ptr[3], int64_t bytes[3]) {
+    const miriam_op_desc &d = op->d;
+    const int64_t es = esize(d.dtype);
+    int n = 0;
+    auto add = [&](const void *p, int64_t b) {
+        if (p && b > 0 && n < 3) {
+            ptr[n] = p;
+            bytes[n] = b;
+            ++n;
+        }
+    };
+    int64_t ch = 0;  // channels of the per-channel epilogue vectors
+    if (op->family == FAM_IGEMM || op->family == FAM_SKINNY) {
+        const IgemmArgs &a = op->ig;
+        const bool nmaj = d.kind == MIRIAM_OP_BGEMM && d.b_nmajor;
+        if (d.kind != MIRIAM_OP_BGEMM || (a.sw0 == 0 && a.sw1 == 0))  // weights shared by the batch
+            add(d.wt, es * (nmaj ? (a.K - 1) * a.ldw + a.Nc : (a.Nc - 1) * a.ldw + a.K));
+        ch = a.Nc;
+    } else if (op->family == FAM_PIX) {
+        if (d.kind == MIRIAM_OP_DWCONV) add(d.wt, es * d.kh * d.kw * d.c);
+        ch = d.c;
+    } else if (d.kind == MIRIAM_OP_LAYERNORM) {
+        add(d.wt, 4 * d.nn);
+        add(d.bias, 4 * d.nn);
+        return n;
+    }
+    if (d.flags & MIRIAM_EPI_BIAS) add(d.bias, 4 * ch);
+    if (d.flags & MIRIAM_EPI_BN) add(d.bn, 16 * ch);
+    return n;
+}
+
 }  // namespace miriam
 
 using namespace miriam;

@@ -35,6 +35,9 @@ def default_config(**kw) -> L.Config:
     c.fake_launch_ns = 2000.0
     c.graphs = 1
     c.release_guard = 0
+    c.warm_critical = 0
+    c.graph_chunk = 0
+    c.arm_lead_us = 0.0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

@@ -223,9 +223,9 @@ def test_bad_configs_rejected(L):
         assert lib.miriam_init(ctypes.byref(c)) == L.EINVAL, bad
 
 
-@pytest.mark.parametrize("guard", [0, 1])
-def test_release_guard_keeps_normal_work_clear_of_timed_releases(L, guard):
-    co = _coord(release_guard=guard, busy_policy=1, inflight_depth=4, quantum_us=100.0)
+@pytest.mark.parametrize("guard,warm", [(0, 0), (1, 0), (1, 1)])
+def test_release_guard_keeps_normal_work_clear_of_timed_releases(L, guard, warm):
+    co = _coord(release_guard=guard, warm_critical=warm, busy_policy=1, inflight_depth=4, quantum_us=100.0)
     try:
         be = co.task(_net(L, [20000, 20000]))
         cr = co.task(_net(L, [4]))
@@ -248,5 +248,38 @@ def test_release_guard_keeps_normal_work_clear_of_timed_releases(L, guard):
             assert late == 0
         for tk, rel in zip(tks, rels):
             assert got[tk].t_start_ns >= rel
+        # one warming pass ahead of each release that found normal work running
+        assert co.stats().warm_launches == (len(rels) if warm else 0)
+    finally:
+        co.shutdown()
+
+
+def test_armed_critical_requests_start_at_release(L):
+    """Timed critical requests armed ahead of their release (kernels queued behind a gate)
+    still start no earlier than the release, and critical work released while a gate is
+    closed completes after it."""
+    co = _coord(arm_lead_us=500.0, release_guard=1, busy_policy=1)
+    try:
+        be = co.task(_net(L, [2000, 2000]))
+        cr = co.task(_net(L, [4, 4]))
+        now = co.now_ns()
+        rels = [now + 3_000_000 + k * 1_500_000 for k in range(4)]
+        tks = [co.submit(cr, True, release_ns=r) for r in rels]
+        for _ in range(4):
+            co.submit(be, False)
+        got = {r.ticket: r for r in _collect(co, 8)}
+        assert len(got) == 8 and all(r.status == 0 for r in got.values())
+        for tk, rel in zip(tks, rels):
+            assert got[tk].t_start_ns >= rel and got[tk].t_end_ns >= rel
+        assert co.stats().armed_releases == len(rels)
+        # an immediate critical request while the next one is armed
+        rel = co.now_ns() + 2_000_000
+        a = co.submit(cr, True, release_ns=rel)
+        while co.stats().armed_releases < len(rels) + 1:
+            time.sleep(0.0001)
+        b = co.submit(cr, True)
+        got = {r.ticket: r for r in _collect(co, 2)}
+        assert got[a].status == 0 and got[b].status == 0
+        assert got[a].t_start_ns >= rel
     finally:
         co.shutdown()

@@ -63,3 +63,48 @@ def test_coordinator_outputs_match_eager(policy, graphs):
         assert st.graph_launches == (whole if graphs else 0)
     finally:
         co.shutdown()
+
+
+@pytest.mark.parametrize("arm_lead_us", [0.0, 500.0])
+def test_warmed_periodic_critical_requests_match_eager(arm_lead_us):
+    """Timed critical releases with normal work running: the release guard holds normal
+    shards and a cache-warming pass runs ahead of each release, and (arm_lead_us > 0) each
+    critical request is queued behind a gate before its release; outputs stay bitwise equal
+    and armed requests complete after their release."""
+    from paper_2307_04339_amd import models
+    from paper_2307_04339_amd.runtime import Coordinator
+    crit = models.resnet18(batch=1, dtype="f16")
+    be = models.vgg16(batch=2, dtype="f16")
+    for n in (crit, be):
+        n.forward()
+    torch.cuda.synchronize()
+    ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
+    co = Coordinator(policy="elastic", graphs=1, release_guard=1, warm_critical=1, busy_policy=1,
+                     profile_reps=1, n_be_streams=1, inflight_depth=4, inflight_us=100.0, quantum_us=40.0,
+                     arm_lead_us=arm_lead_us)
+    try:
+        ct = co.task(crit.ops())
+        bt = co.task(be.ops())
+        for rep in range(2):
+            _nan_outputs(crit)
+            _nan_outputs(be)
+            torch.cuda.synchronize()
+            t0 = co.now_ns() + 2_000_000
+            tks = [co.submit(ct, True, release_ns=t0 + k * 1_500_000) for k in range(4)]
+            btk = [co.submit(bt, False) for _ in range(6)]
+            co.drain(60000)
+            recs = {r.ticket: r for r in co.poll()}
+            assert set(recs) == set(tks) | set(btk)
+            assert all(r.status == 0 for r in recs.values())
+            for k, tk in enumerate(tks):
+                assert recs[tk].t_start_ns >= t0 + k * 1_500_000
+            torch.cuda.synchronize()
+            for n in (crit, be):
+                for l, r in zip(n.layers, ref[n.name]):
+                    assert bits(l.t["y"]) == r, (rep, n.name, l.name)
+        st = co.stats()
+        assert st.warm_launches >= 1
+        assert st.graph_launches == 8
+        assert st.armed_releases == (8 if arm_lead_us > 0 else 0)
+    finally:
+        co.shutdown()
