@@ -87,8 +87,10 @@ def time_layers(net, reps, flush):
 # profiles/ (each counter scaled by what it reads for a device copy of known size).  Used only
 # while the contraction-kernel sources still hash to the value the counters were taken with.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# device code of the contraction kernels; the host-side choice of kernel is checked through
+# the kernel path and tile recorded with the counters
 KERNEL_SOURCES = ["conv_halo.h", "igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h", "kern_igemm_f16.hip",
-                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "kern_skinny.hip", "ops.cpp"]
+                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "kern_skinny.hip"]
 
 
 def kernel_source_hash():
@@ -100,16 +102,17 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(workload, kernel, tile):
+def measured_traffic(workload, kernel, tile, path):
     """HBM bytes per launch of `kernel` from the committed counter summary, or None when
-    there is none for this workload / tile or the kernel sources changed since."""
+    there is none for this workload / kernel path / tile or the kernel sources changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             entries = json.load(f)["entries"]
     except (OSError, ValueError, KeyError):
         return None
     e = entries.get(f"{workload}:{kernel}")
-    if not e or list(e.get("tile", [])) != list(tile) or e.get("source_sha256") != kernel_source_hash():
+    if (not e or list(e.get("tile", [])) != list(tile) or e.get("path") != path
+            or e.get("source_sha256") != kernel_source_hash()):
         return None
     fetch = e["fetch_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_fetch_kib"] * 1024.0)
     write = e["write_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_write_kib"] * 1024.0)
@@ -334,8 +337,13 @@ def main():
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=sorted(CONFIGS))
     ap.add_argument("--reps", type=int, default=20, help="repetitions per kernel timing")
     ap.add_argument("--quantum-us", type=float, default=40.0)
-    ap.add_argument("--depth", type=int, default=4)
-    ap.add_argument("--inflight-us", type=float, default=100.0)
+    ap.add_argument("--depth", type=int, default=32)
+    ap.add_argument("--inflight-us", type=float, default=-1.0,
+                    help="normal work kept queued on the GPU (it bounds the wait of an unannounced critical "
+                         "release; 300 measured 2-6%% more best-effort throughput but slower critical kernels "
+                         "next to it); -1: 100")
+    ap.add_argument("--event-us", type=float, default=-1.0,
+                    help="estimated normal work between completion events; -1: a third of the in-flight budget")
     ap.add_argument("--busy-policy", type=int, default=0,
                     help="normal shards next to a running critical kernel: 0 paper rule, 1 none, 2 smallest")
     ap.add_argument("--graphs", type=int, default=1, choices=(0, 1),
@@ -349,6 +357,8 @@ def main():
     ap.add_argument("--arm-lead-us", type=float, default=-1.0,
                     help="queue each timed critical request behind a gate this long before its release "
                          "(0 = launch at the release); -1: 500 with the release guard, else 0")
+    ap.add_argument("--segments", type=int, default=0, choices=(0, 1),
+                    help="1: runs of short normal ops within one quantum go out as one captured unit")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
@@ -401,7 +411,7 @@ def main():
         kern["bytes_per_launch"] = dom["bytes"]
         layer = next(l for l in dom_net.layers if l.name == dom["name"])
         kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
-        kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"])
+        kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
         result["elastic_overhead"] = dict(kernel=kern["kernel"],
                                           **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load()))
         result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
@@ -417,9 +427,11 @@ def main():
     guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
     warm = args.warm_critical if args.warm_critical >= 0 else guard
     arm = args.arm_lead_us if args.arm_lead_us >= 0 else (500.0 if guard else 0.0)
-    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=args.inflight_us,
+    inflight_us = args.inflight_us if args.inflight_us >= 0 else 100.0
+    event_us = args.event_us if args.event_us >= 0 else inflight_us / 3.0
+    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=inflight_us, event_us=event_us,
                 busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
-                warm_critical=warm, arm_lead_us=arm)
+                warm_critical=warm, arm_lead_us=arm, segments=args.segments)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
         if ph not in phases:
@@ -455,9 +467,9 @@ def main():
                    "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
-                   "inflight_us": args.inflight_us, "busy_policy": args.busy_policy,
+                   "inflight_us": inflight_us, "event_us": round(event_us, 2), "busy_policy": args.busy_policy,
                    "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
-                   "arm_lead_us": arm},
+                   "arm_lead_us": arm, "segments": args.segments},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

@@ -279,6 +279,15 @@ typedef struct miriam_config {
                                 waits for a flag the dispatcher raises at the release (the gate gives
                                 up 2 ms after the release at the latest); 0 = launch at the release.
                                 Critical work released in between waits behind the gate. */
+    int32_t segments;        /* ELASTIC: runs of consecutive ops of a task whose profiled unsharded
+                                times sum to at most quantum_us are captured (at task creation) as
+                                units; a normal request issues such a run as one launch with one
+                                event while no critical kernel runs (ops launched unsharded).
+                                Longer ops are sharded as usual. */
+    double event_us;         /* ELASTIC: a normal launch records a completion event only once this
+                                much estimated work has gathered on its stream since the last event,
+                                and on each request's last launch (an event costs GPU time between
+                                kernels); 0 = an event per launch */
 } miriam_config;
 
 typedef struct miriam_completion {
@@ -304,6 +313,7 @@ typedef struct miriam_stats {
                                  (each also counts its ops in `launches`) */
     int64_t warm_launches;    /* cache-warming kernels queued ahead of critical releases */
     int64_t armed_releases;   /* critical requests queued behind a gate ahead of their release */
+    int64_t segment_launches; /* runs of short normal ops issued as one captured unit */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */
@@ -318,6 +328,14 @@ int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out);
  * broken by earliest deadline).  Thread-safe. */
 int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_t deadline_ns,
                   uint64_t *ticket_out);
+
+/* Diagnostic of the release gate used by armed critical requests (arm_lead_us): queue one
+ * gate kernel on `stream` (a hipStream_t; NULL = the null stream) behind a start event, with a
+ * fresh flag that the host raises open_after_us microseconds after the launch (open_after_us
+ * < 0: never) and a wall-clock limit of limit_us (1 .. 100000); wait for the stream and
+ * return in *held_us the time between the events around the gate.  The gate always ends:
+ * held_us is about min(open_after_us, limit_us).  Blocks the calling thread. */
+int miriam_gate_check(void *stream, int64_t limit_us, int64_t open_after_us, double *held_us);
 
 /* Non-blocking: move up to max_out completion records into out; returns the count. */
 int miriam_poll(miriam_completion *out, int max_out);

@@ -80,6 +80,7 @@ class Config(ctypes.Structure):
         ("fake_tile_ns", ctypes.c_double), ("fake_launch_ns", ctypes.c_double),
         ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32), ("warm_critical", ctypes.c_int32),
         ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
+        ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
     ]
 
 
@@ -107,7 +108,7 @@ class Stats(ctypes.Structure):
         ("eq2_violations", ctypes.c_int64), ("decisions", ctypes.c_int64),
         ("decision_ns_total", ctypes.c_double), ("completed", ctypes.c_int64),
         ("graph_launches", ctypes.c_int64), ("warm_launches", ctypes.c_int64),
-        ("armed_releases", ctypes.c_int64),
+        ("armed_releases", ctypes.c_int64), ("segment_launches", ctypes.c_int64),
     ]
 
 
@@ -146,6 +147,7 @@ SIGNATURES = {
     "miriam_shutdown": ([], _INT),
     "miriam_now_ns": ([], _I64),
     "miriam_launch_log": ([ctypes.POINTER(LaunchRecord), _INT], _INT),
+    "miriam_gate_check": ([_P, _I64, _I64, _DP], _INT),
 }
 
 _lib = None

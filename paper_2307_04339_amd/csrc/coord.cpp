@@ -42,6 +42,12 @@ static int64_t mono_ns() {
 }
 
 // ------------------------------------------------------------------ backends
+// Ops [i0, i1) of a task, each launched unsharded (grid = T, block 256), recorded once and
+// replayed as a unit.
+struct Captured {
+    virtual ~Captured() {}
+};
+
 struct Backend {
     virtual ~Backend() {}
     virtual int start(int n_streams) = 0;
@@ -53,11 +59,11 @@ struct Backend {
     virtual double launch_gap_us(const miriam_op *op, int reps) = 0;
     // Record the unsharded launch sequence of `ops` (grid = T, block 256 each) as one
     // replayable unit; nullptr where the backend has none (then requests launch per op).
-    virtual void *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) {
+    virtual Captured *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) {
         (void)ops; (void)i0; (void)i1;
         return nullptr;
     }
-    virtual int launch_captured(void *unit, int stream) { (void)unit; (void)stream; return MIRIAM_ESTATE; }
+    virtual int launch_captured(Captured *unit, int stream) { (void)unit; (void)stream; return MIRIAM_ESTATE; }
     // Run the cache-warming kernel over a device table of ranges on `stream`, after the
     // recorded events `waits` (work already queued on other streams) have completed.
     virtual int warm(const WarmRange *table, int n, int grid, int *sink, int stream, const std::vector<int> &waits) {
@@ -74,19 +80,15 @@ struct Backend {
     virtual void stop() = 0;
 };
 
-// An instantiated HIP graph of one task's unsharded kernel sequence.
-struct CritGraph {
+// An instantiated HIP graph.
+struct HipGraphUnit : Captured {
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
+    ~HipGraphUnit() override {
+        if (exec) (void)hipGraphExecDestroy(exec);
+        if (graph) (void)hipGraphDestroy(graph);
+    }
 };
-
-void free_captured(void *unit) {
-    CritGraph *cg = static_cast<CritGraph *>(unit);
-    if (!cg) return;
-    if (cg->exec) (void)hipGraphExecDestroy(cg->exec);
-    if (cg->graph) (void)hipGraphDestroy(cg->graph);
-    delete cg;
-}
 
 struct HipBackend : Backend {
     int dev = 0;
@@ -133,10 +135,10 @@ struct HipBackend : Backend {
     void open_gates(uint64_t seq) override {
         if (gate_host) __atomic_store_n(gate_host, seq, __ATOMIC_RELEASE);
     }
-    void *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) override {
+    Captured *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) override {
         // thread-local capture: the dispatcher thread keeps launching on its own streams meanwhile
         std::lock_guard<std::mutex> lk(cap_mu);
-        CritGraph *cg = new (std::nothrow) CritGraph();
+        HipGraphUnit *cg = new (std::nothrow) HipGraphUnit();
         if (!cg) return nullptr;
         if (hipStreamBeginCapture(cap, hipStreamCaptureModeThreadLocal) != hipSuccess) {
             delete cg;
@@ -154,7 +156,7 @@ struct HipBackend : Backend {
         hipError_t e = hipStreamEndCapture(cap, &cg->graph);
         if (!ok || e != hipSuccess || !cg->graph ||
             hipGraphInstantiate(&cg->exec, cg->graph, nullptr, nullptr, 0) != hipSuccess) {
-            free_captured(cg);
+            delete cg;
             return nullptr;
         }
         return cg;
@@ -166,8 +168,8 @@ struct HipBackend : Backend {
         }
         return warm_launch(table, n, grid, sink, streams[stream]);
     }
-    int launch_captured(void *unit, int stream) override {
-        hipError_t e = hipGraphLaunch(static_cast<CritGraph *>(unit)->exec, streams[stream]);
+    int launch_captured(Captured *unit, int stream) override {
+        hipError_t e = hipGraphLaunch(static_cast<HipGraphUnit *>(unit)->exec, streams[stream]);
         if (e != hipSuccess) return hip_fail(e, "hipGraphLaunch");
         return MIRIAM_OK;
     }
@@ -323,6 +325,20 @@ struct FakeBackend : Backend {
         return duration(op, l, grid) / 1000.0;
     }
     double launch_gap_us(const miriam_op *, int) override { return launch_ns / 1000.0; }
+    struct FakeUnit : Captured {
+        std::vector<const miriam_op *> ops;
+    };
+    Captured *capture(const std::vector<miriam_op *> &ops, size_t i0, size_t i1) override {
+        FakeUnit *u = new (std::nothrow) FakeUnit();
+        if (u) u->ops.assign(ops.begin() + i0, ops.begin() + i1);
+        return u;
+    }
+    int launch_captured(Captured *unit, int stream) override {
+        int64_t st = std::max(mono_ns(), busy_until[stream]);
+        for (const miriam_op *op : static_cast<FakeUnit *>(unit)->ops) st += duration(op, op->T, op->T);
+        busy_until[stream] = st;
+        return MIRIAM_OK;
+    }
     int gate(uint64_t, int64_t release_ns, int64_t, int stream) override {
         busy_until[stream] = std::max(std::max(busy_until[stream], mono_ns()), release_ns);
         return MIRIAM_OK;
@@ -350,7 +366,16 @@ struct miriam_task {
     std::vector<OpProf> prof;
     int id = 0;
     std::atomic<int> pending{0};
-    std::vector<void *> graphs;   // captured unsharded sequence (HIP graphs of consecutive ops), or empty
+    std::vector<Captured *> graphs;  // captured unsharded sequence (consecutive ops), or empty
+    // segments: runs of consecutive short ops (profiled unsharded time within one quantum in
+    // total) that a normal request issues as one captured unit while no critical kernel runs
+    struct Segment {
+        size_t i0, i1;
+        Captured *unit;
+        double est_us;
+    };
+    std::vector<Segment> segs;
+    std::vector<int> seg_at;      // per op: the segment that starts there, or -1
     std::vector<double> end_us;   // profiled end of op i within one unsharded run
     // parameter lines touched before a release (cache warming): device table of ranges and a
     // sink word (HIP backend), their line count and estimated duration
@@ -359,12 +384,17 @@ struct miriam_task {
     int64_t warm_lines = 0;
     double warm_us = 0.0;
     ~miriam_task() {
-        for (void *gph : graphs) free_captured(gph);
+        for (Captured *gph : graphs) delete gph;
+        for (Segment &sg : segs) delete sg.unit;
         if (warm_dev) (void)hipFree(warm_dev);
     }
 };
 
 namespace {
+
+// Shot::ev values other than an event id: no event recorded with this launch (it is known
+// complete once a later launch of the same stream is), or known complete (failure path).
+constexpr int kNoEvent = -1, kDone = -2;
 
 struct Shot {  // one launch in flight
     int ev;
@@ -423,6 +453,7 @@ struct Coord {
     Req *armed = nullptr;                          // timed critical request queued behind a gate
     uint64_t gate_seq = 0;
     std::vector<int> last_ev;                      // event of the latest launch per stream
+    std::vector<double> since_ev_us;               // estimated work launched since that event
     std::vector<Req *> crit_ready;                 // released critical requests
     std::vector<std::deque<Req *>> norm_ready;     // per stream, FIFO
     std::deque<Req *> crit_active;                 // launched critical requests, stream 0
@@ -467,15 +498,21 @@ void log_launch(Coord &c, const Req *r, int op_index, int stream, int grid, int 
 
 // Launch shard [b, b+l) of op `oi` of request r on `stream` and record its event.
 int issue(Coord &c, Req *r, int oi, int64_t b, int64_t l, int grid, int block, int stream, bool crit_busy,
-          int64_t limit, double est_us = 0.0) {
+          int64_t limit, double est_us = 0.0, bool with_event = true) {
     const miriam_op *op = r->task->ops[oi];
     int rc = c.be->launch(op, b, l, grid, block, stream);
     if (rc != MIRIAM_OK) return rc;
-    int ev = c.be->record(stream);
-    if (ev < 0) return ev;
+    int ev = kNoEvent;
+    if (with_event) {
+        ev = c.be->record(stream);
+        if (ev < 0) return ev;
+        c.last_ev[stream] = ev;
+        c.since_ev_us[stream] = 0.0;
+    } else {
+        c.since_ev_us[stream] += est_us;
+    }
     if (r->t_start == 0) r->t_start = mono_ns();
     r->shots.push_back({ev, oi, est_us});
-    c.last_ev[stream] = ev;
     r->n_shards++;
     c.inflight[stream]++;
     c.inflight_us[stream] += est_us;
@@ -567,14 +604,23 @@ bool retire(Coord &c, std::deque<Req *> &active, int stream) {
     while (!active.empty()) {
         Req *r = active.front();
         while (!r->shots.empty()) {
-            int q = c.be->query(r->shots.front().ev);
-            if (q == 0) break;
-            if (q < 0) r->status = q;
-            c.be->release(r->shots.front().ev);
-            c.inflight_us[stream] -= r->shots.front().est_us;
+            // the first launch with an event; the event-less ones before it end no later
+            size_t k = 0;
+            while (k < r->shots.size() && r->shots[k].ev == kNoEvent) ++k;
+            if (k == r->shots.size()) break;
+            const int ev = r->shots[k].ev;
+            if (ev != kDone) {
+                int q = c.be->query(ev);
+                if (q == 0) break;
+                if (q < 0) r->status = q;
+                c.be->release(ev);
+            }
+            for (size_t i = 0; i <= k; ++i) {
+                c.inflight_us[stream] -= r->shots.front().est_us;
+                r->shots.pop_front();
+                c.inflight[stream]--;
+            }
             if (c.inflight_us[stream] < 1e-9) c.inflight_us[stream] = 0.0;
-            r->shots.pop_front();
-            c.inflight[stream]--;
             any = true;
         }
         if (r->shots.empty() && r->launched_all) {
@@ -714,6 +760,77 @@ void warm_for(Coord &c, const Req *nx) {
     if (rc == MIRIAM_OK) c.stats.warm_launches++;
 }
 
+// Release guard: true if normal work estimated at est_us, issued now behind the normal work
+// already queued, would still be on the GPU at the next timed critical release (then normal
+// work is held up to that release, and the request's parameters are warmed once).
+bool guard_holds(Coord &c, int64_t t0, double est_us) {
+    if (!c.cfg.release_guard || c.crit_timed.empty()) return false;
+    const Req *nx = c.crit_timed.top();
+    const double warm_us = c.cfg.warm_critical ? nx->task->warm_us : 0.0;
+    if (c.warmed_ticket != nx->ticket &&
+        t0 + (int64_t)(1000.0 * (queued_normal_us(c) + est_us + warm_us)) <= nx->release)
+        return false;
+    if (c.cfg.warm_critical && c.warmed_ticket != nx->ticket) warm_for(c, nx);
+    return true;
+}
+
+// Launch segment sg of normal request r on `stream` and record its event.
+int issue_segment(Coord &c, Req *r, const miriam_task::Segment &sg, int stream, bool with_event) {
+    int rc = c.be->launch_captured(sg.unit, stream);
+    if (rc != MIRIAM_OK) return rc;
+    int ev = kNoEvent;
+    if (with_event) {
+        ev = c.be->record(stream);
+        if (ev < 0) return ev;
+        c.last_ev[stream] = ev;
+        c.since_ev_us[stream] = 0.0;
+    } else {
+        c.since_ev_us[stream] += sg.est_us;
+    }
+    if (r->t_start == 0) r->t_start = mono_ns();
+    r->shots.push_back({ev, (int)sg.i0, sg.est_us});
+    r->n_shards += (int)(sg.i1 - sg.i0);
+    c.inflight[stream]++;
+    c.inflight_us[stream] += sg.est_us;
+    for (size_t i = sg.i0; i < sg.i1; ++i) {
+        const miriam_op *op = r->task->ops[i];
+        log_launch(c, r, (int)i, stream, (int)std::min<int64_t>(op->T, INT32_MAX), 256, false, 0, op->T, op->T, 0,
+                   r->task->prof[i].t_unsh_us);
+    }
+    std::lock_guard<std::mutex> lk(c.stat_mu);
+    c.stats.launches += (int64_t)(sg.i1 - sg.i0);
+    c.stats.segment_launches++;
+    return MIRIAM_OK;
+}
+
+// Whether a normal launch of est_us records a completion event: always on the request's
+// last launch, else once event_us of estimated work has gathered since the stream's last event.
+// A launch that fills the stream's in-flight depth or the shared budget also records one, so
+// that the stream can always retire work and issue again.
+bool want_event(const Coord &c, int stream, double est_us, bool last_of_request) {
+    return last_of_request || c.cfg.event_us <= 0.0 || c.since_ev_us[stream] + est_us >= c.cfg.event_us ||
+           c.inflight[stream] + 1 >= c.cfg.inflight_depth ||
+           (c.cfg.inflight_us > 0.0 && queued_normal_us(c) + est_us >= c.cfg.inflight_us);
+}
+
+// Give request r's last launch an event (or, if recording fails, mark its launches complete)
+// so that retiring them does not wait for a later launch: after a failure ends the request,
+// and when normal work is held back.
+void seal(Coord &c, Req *r, int stream) {
+    if (r->shots.empty() || r->shots.back().ev != kNoEvent) return;
+    const int ev = c.be->record(stream);
+    r->shots.back().ev = ev >= 0 ? ev : kDone;
+    c.since_ev_us[stream] = 0.0;
+}
+
+void seal_stream(Coord &c, int stream) {
+    for (auto it = c.be_active[stream].rbegin(); it != c.be_active[stream].rend(); ++it)
+        if (!(*it)->shots.empty()) {
+            seal(c, *it, stream);
+            return;
+        }
+}
+
 // Issue shards for the normal requests of one stream while the in-flight budget lasts
 // (every stream may keep one shard in flight; beyond that the budget is shared).
 bool pump_normal(Coord &c, int s) {
@@ -735,23 +852,45 @@ bool pump_normal(Coord &c, int s) {
         const int64_t t0 = mono_ns();
         const miriam_op *crit_op = nullptr;
         const bool busy = current_critical_op(c, &crit_op) >= 0;
-        if (busy && c.cfg.busy_policy == 1) break;  // ablation: hold normal work back
-        Decision d = decide(c, r, busy ? crit_op : nullptr);
-        if (!busy && c.cfg.release_guard && !c.crit_timed.empty()) {
-            const Req *nx = c.crit_timed.top();
-            const double warm_us = c.cfg.warm_critical ? nx->task->warm_us : 0.0;
-            if (c.warmed_ticket == nx->ticket ||
-                t0 + (int64_t)(1000.0 * (queued_normal_us(c) + d.est_us + warm_us)) > nx->release) {
-                // the GPU would still hold this shard when the next critical request is released:
-                // hold normal work from here to that release, and warm the request's parameters
-                // once the normal work already queued has drained
-                if (c.cfg.warm_critical && c.warmed_ticket != nx->ticket) warm_for(c, nx);
+        if (busy && c.cfg.busy_policy == 1) {  // ablation: hold normal work back
+            seal_stream(c, s);
+            break;
+        }
+        miriam_task *t = r->task;
+        const int sid = (!busy && r->cursor == 0 && r->op < t->seg_at.size()) ? t->seg_at[r->op] : -1;
+        if (sid >= 0) {  // a run of short ops as one captured unit
+            const miriam_task::Segment &sg = t->segs[sid];
+            if (guard_holds(c, t0, sg.est_us)) {
+                seal_stream(c, s);
                 break;
             }
+            int rc = issue_segment(c, r, sg, s, want_event(c, s, sg.est_us, sg.i1 >= t->ops.size()));
+            {
+                std::lock_guard<std::mutex> lk(c.stat_mu);
+                c.stats.decisions++;
+                c.stats.decision_ns_total += (double)(mono_ns() - t0);
+            }
+            any = true;
+            if (rc != MIRIAM_OK) {
+                r->status = rc;
+                r->launched_all = true;
+                seal(c, r, s);
+                continue;
+            }
+            r->op = sg.i1;
+            if (r->op >= t->ops.size()) r->launched_all = true;
+            continue;
+        }
+        Decision d = decide(c, r, busy ? crit_op : nullptr);
+        if (!busy && guard_holds(c, t0, d.est_us)) {
+            seal_stream(c, s);
+            break;
         }
         const int64_t t1 = mono_ns();
         const int oi = (int)r->op;
-        int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit, d.est_us);
+        const bool last = r->cursor + d.len >= r->task->ops[oi]->T && r->op + 1 >= r->task->ops.size();
+        int rc = issue(c, r, oi, r->cursor, d.len, d.grid, d.block, s, busy, d.limit, d.est_us,
+                       want_event(c, s, d.est_us, last));
         {
             std::lock_guard<std::mutex> lk(c.stat_mu);
             c.stats.decisions++;
@@ -765,6 +904,7 @@ bool pump_normal(Coord &c, int s) {
         if (rc != MIRIAM_OK) {
             r->status = rc;
             r->launched_all = true;
+            seal(c, r, s);
             continue;
         }
         r->cursor += d.len;
@@ -972,6 +1112,29 @@ void profile_task(Coord &c, miriam_task *t) {
     for (size_t i = 0; i < t->ops.size(); ++i) t->end_us[i] = (acc += std::max(0.0, t->prof[i].t_unsh_us));
 }
 
+// Group runs of consecutive ops whose profiled unsharded times sum to at most one quantum
+// into segments of two or more ops, each captured as one unit.
+void build_segments(Coord &c, miriam_task *t) {
+    const size_t n = t->ops.size();
+    t->seg_at.assign(n, -1);
+    const double q = c.cfg.quantum_us;
+    size_t i = 0;
+    while (i < n) {
+        size_t j = i;
+        double sum = 0.0;
+        while (j < n && t->prof[j].t_unsh_us > 0.0 && sum + t->prof[j].t_unsh_us <= q) sum += t->prof[j++].t_unsh_us;
+        if (j - i >= 2) {
+            Captured *u = c.be->capture(t->ops, i, j);
+            if (!u) return;  // no capture on this backend: ops launched one by one
+            t->seg_at[i] = (int)t->segs.size();
+            t->segs.push_back({i, j, u, sum});
+            i = j;
+        } else {
+            i = std::max(j, i + 1);
+        }
+    }
+}
+
 // Line table of the task's parameters (each distinct range once) for cache warming; its
 // duration is estimated at 4 TB/s plus a launch.
 int build_warm(Coord &c, miriam_task *t) {
@@ -1011,6 +1174,46 @@ extern "C" {
 
 int64_t miriam_now_ns(void) { return mono_ns(); }
 
+int miriam_gate_check(void *stream, int64_t limit_us, int64_t open_after_us, double *held_us) {
+    if (!held_us || limit_us < 1 || limit_us > 100000) {
+        set_error("gate check: limit_us in [1, 100000] and held_us required");
+        return MIRIAM_EINVAL;
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int dev = 0, khz = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess || khz <= 0) return hip_fail(e, "wall clock rate");
+    uint64_t *host = nullptr, *devp = nullptr;
+    e = hipHostMalloc(reinterpret_cast<void **>(&host), 64, hipHostMallocCoherent | hipHostMallocMapped);
+    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc (gate flag)");
+    __atomic_store_n(host, (uint64_t)0, __ATOMIC_RELEASE);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    int rc = MIRIAM_OK;
+    if ((e = hipHostGetDevicePointer(reinterpret_cast<void **>(&devp), host, 0)) != hipSuccess ||
+        (e = hipEventCreate(&e0)) != hipSuccess || (e = hipEventCreate(&e1)) != hipSuccess ||
+        (e = hipEventRecord(e0, st)) != hipSuccess) {
+        rc = hip_fail(e, "gate check set-up");
+    } else {
+        rc = gate_launch(devp, 1, (uint64_t)limit_us * (uint64_t)khz / 1000u, st);
+        if (rc == MIRIAM_OK && (e = hipEventRecord(e1, st)) != hipSuccess) rc = hip_fail(e, "hipEventRecord");
+        if (rc == MIRIAM_OK && open_after_us >= 0) {
+            std::this_thread::sleep_for(std::chrono::microseconds(open_after_us));
+            __atomic_store_n(host, (uint64_t)1, __ATOMIC_RELEASE);
+        }
+        // the gate has a bounded wait, so this returns
+        if (rc == MIRIAM_OK && (e = hipEventSynchronize(e1)) != hipSuccess) rc = hip_fail(e, "hipEventSynchronize");
+        float ms = 0.0f;
+        if (rc == MIRIAM_OK && (e = hipEventElapsedTime(&ms, e0, e1)) != hipSuccess) rc = hip_fail(e, "hipEventElapsedTime");
+        *held_us = 1000.0 * ms;
+    }
+    if (rc != MIRIAM_OK) (void)hipStreamSynchronize(st);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    (void)hipHostFree(host);
+    return rc;
+}
+
 int miriam_init(const miriam_config *cfg) {
     std::lock_guard<std::mutex> life(g_life);
     if (g) return estate("already initialised");
@@ -1023,7 +1226,8 @@ int miriam_init(const miriam_config *cfg) {
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
         cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
-        cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0)) {
+        cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
+        cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0)) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -1066,6 +1270,7 @@ int miriam_init(const miriam_config *cfg) {
     c->inflight.assign(c->n_streams, 0);
     c->inflight_us.assign(c->n_streams, 0.0);
     c->last_ev.assign(c->n_streams, -1);
+    c->since_ev_us.assign(c->n_streams, 0.0);
     g = c;
     c->th = std::thread(dispatcher, c);
     return MIRIAM_OK;
@@ -1095,15 +1300,16 @@ int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out) {
     if (g->cfg.graphs) {  // no graph: launched op by op
         const size_t n = t->ops.size(), chunk = g->cfg.graph_chunk > 0 ? (size_t)g->cfg.graph_chunk : n;
         for (size_t i0 = 0; i0 < n; i0 += chunk) {
-            void *gph = g->be->capture(t->ops, i0, std::min(n, i0 + chunk));
+            Captured *gph = g->be->capture(t->ops, i0, std::min(n, i0 + chunk));
             if (!gph) {
-                for (void *q : t->graphs) free_captured(q);
+                for (Captured *q : t->graphs) delete q;
                 t->graphs.clear();
                 break;
             }
             t->graphs.push_back(gph);
         }
     }
+    if (g->cfg.segments) build_segments(*g, t);
     if (g->cfg.warm_critical) {
         int rc = build_warm(*g, t);
         if (rc != MIRIAM_OK) {

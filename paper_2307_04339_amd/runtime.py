@@ -38,6 +38,8 @@ def default_config(**kw) -> L.Config:
     c.warm_critical = 0
     c.graph_chunk = 0
     c.arm_lead_us = 0.0
+    c.segments = 0
+    c.event_us = 0.0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

@@ -65,12 +65,16 @@ def _collect(co, n, timeout=20.0):
     return got
 
 
-@pytest.mark.parametrize("policy", ["elastic", "sequential", "multistream"])
-def test_every_request_completes_once(L, policy):
-    co = _coord(policy=policy, n_be_streams=2, inflight_depth=2)
+@pytest.mark.parametrize("policy,segments,event_us", [("elastic", 0, 0.0), ("elastic", 1, 0.0), ("elastic", 1, 25.0),
+                                                      ("elastic", 0, 1e9), ("sequential", 0, 0.0),
+                                                      ("multistream", 0, 0.0)])
+def test_every_request_completes_once(L, policy, segments, event_us):
+    # event_us: normal launches carry a completion event only every event_us of estimated work
+    # (1e9: only each request's last launch)
+    co = _coord(policy=policy, n_be_streams=2, inflight_depth=2, segments=segments, event_us=event_us)
     try:
         crit = co.task(_net(L, [3, 5, 2]))
-        be1 = co.task(_net(L, [40, 17, 64]))
+        be1 = co.task(_net(L, [40, 17, 64] + [2] * 6 + [40]))
         be2 = co.task(_net(L, [9, 33]))
         tickets = []
         now = co.now_ns()
@@ -90,6 +94,8 @@ def test_every_request_completes_once(L, policy):
         assert st.completed == len(tickets)
         assert st.eq2_violations == 0
         assert st.launches == len(log)
+        # short ops (5 us each on the simulated device, quantum 10 us) run as captured pairs
+        assert (st.segment_launches > 0) == (segments == 1)
         _check_log(log, policy)
     finally:
         co.shutdown()

@@ -17,9 +17,10 @@ def _nan_outputs(net):
         l.t["y"].fill_(float("nan"))
 
 
-@pytest.mark.parametrize("graphs", [0, 1])
-@pytest.mark.parametrize("policy", ["elastic", "sequential", "multistream"])
-def test_coordinator_outputs_match_eager(policy, graphs):
+@pytest.mark.parametrize("policy,graphs,segments,event_us",
+                         [(p, g, 0, 0.0) for p in ("elastic", "sequential", "multistream") for g in (0, 1)]
+                         + [("elastic", 1, 1, 0.0), ("elastic", 1, 1, 30.0)])
+def test_coordinator_outputs_match_eager(policy, graphs, segments, event_us):
     from paper_2307_04339_amd import models
     from paper_2307_04339_amd.runtime import Coordinator
     crit = models.resnet18(batch=1, dtype="f16")
@@ -28,8 +29,9 @@ def test_coordinator_outputs_match_eager(policy, graphs):
         n.forward()
     torch.cuda.synchronize()
     ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
-    co = Coordinator(policy=policy, graphs=graphs, profile_reps=1, log_launches=1, n_be_streams=1,
-                     inflight_depth=2, quantum_us=20.0)
+    co = Coordinator(policy=policy, graphs=graphs, segments=segments, event_us=event_us, profile_reps=1,
+                     log_launches=1,
+                     n_be_streams=1, inflight_depth=2, quantum_us=20.0)
     try:
         ct = co.task(crit.ops())
         bt = co.task(be.ops())
@@ -61,6 +63,7 @@ def test_coordinator_outputs_match_eager(policy, graphs):
         assert st.eq2_violations == 0
         whole = reps * (3 if policy != "elastic" else 1)  # requests launched unsharded
         assert st.graph_launches == (whole if graphs else 0)
+        assert (st.segment_launches > 0) == (segments == 1)
     finally:
         co.shutdown()
 
@@ -108,3 +111,24 @@ def test_warmed_periodic_critical_requests_match_eager(arm_lead_us):
         assert st.armed_releases == (8 if arm_lead_us > 0 else 0)
     finally:
         co.shutdown()
+
+
+@pytest.mark.parametrize("limit_us,open_after_us", [(300, -1), (50000, 1000), (2000, 0)])
+def test_release_gate_ends_on_flag_or_limit(limit_us, open_after_us):
+    """The gate that holds an armed critical request ends when the host raises its flag, and
+    on its own wall-clock limit when the flag is never raised."""
+    import ctypes
+    from paper_2307_04339_amd import _lib as L
+    lib = L.load()
+    s = torch.cuda.Stream()
+    held = ctypes.c_double()
+    assert lib.miriam_gate_check(ctypes.c_void_p(s.cuda_stream), limit_us, open_after_us, ctypes.byref(held)) == 0, \
+        lib.miriam_last_error()
+    expect = limit_us if open_after_us < 0 else min(open_after_us, limit_us)
+    assert held.value >= 0.8 * expect, (held.value, expect)
+    assert held.value <= expect + 2000.0, (held.value, expect)
+    # the stream runs normally afterwards
+    with torch.cuda.stream(s):
+        x = torch.ones(1024, device="cuda") * 2.0
+    s.synchronize()
+    assert float(x.sum()) == 2048.0
