@@ -1136,7 +1136,7 @@ void build_segments(Coord &c, miriam_task *t) {
 }
 
 // Line table of the task's parameters (each distinct range once) for cache warming; its
-// duration is estimated at 4 TB/s plus a launch.
+// duration is estimated at 2 TB/s (whole 64-byte lines) plus a launch.
 int build_warm(Coord &c, miriam_task *t) {
     std::vector<WarmRange> tab;
     std::vector<const void *> seen;
@@ -1154,8 +1154,8 @@ int build_warm(Coord &c, miriam_task *t) {
         }
     }
     t->warm_n = (int)tab.size();
-    t->warm_us = 3.0 + 64.0 * (double)t->warm_lines / 4.0e6;
-    t->warm_grid = (int)std::max<int64_t>(1, std::min<int64_t>(4 * c.n_cu, (t->warm_lines + 2047) / 2048));
+    t->warm_us = 4.0 + 64.0 * (double)t->warm_lines / 2.0e6;
+    t->warm_grid = (int)std::max<int64_t>(1, std::min<int64_t>(16 * c.n_cu, (t->warm_lines + 1023) / 1024));
     if (c.cfg.backend != MIRIAM_BACKEND_HIP || tab.empty()) return MIRIAM_OK;
     const size_t bytes = sizeof(WarmRange) * tab.size() + 64;
     hipError_t e = hipMalloc(&t->warm_dev, bytes);
