@@ -108,7 +108,9 @@ typedef struct miriam_op_desc {
     int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128, 4 = 128x64,
                            5 = 16-column split-K (GEMM, fp16/bf16, m <= 16), 6 = 256x128,
                            7 = direct 3x3 stride-1 conv: 4x32 output pixels x 64 channels, the tile's
-                           input patch held in LDS (C a multiple of 64 fp16/bf16 or 32 fp32 channels) */
+                           input patch held in LDS (C a multiple of 64 fp16/bf16 or 32 fp32 channels),
+                           8 = direct 3x3 stride-1 conv with the weights resident in registers: same
+                           tile, fp16/bf16, C in {8, 16, 32, 64}, at most 64 output channels */
     float eps;          /* BN / LN epsilon */
     float scale;        /* SOFTMAX scale */
     const void *x, *wt, *bias, *bn, *residual; /* device pointers (wt = weights) */
@@ -128,6 +130,9 @@ typedef struct miriam_op_info {
     double bytes;             /* algorithmic HBM bytes: inputs and weights read once, outputs written once */
     int32_t path;             /* miriam_kernel_path: which kernel family serves the op */
     int32_t ksplit;           /* K slices per output tile (1 = no split); num_tiles counts slices */
+    int32_t full_grid;        /* grid of the op's whole-tile-space (unsharded) launch: num_tiles (one
+                                 workgroup per tile), or for kernels that keep operands resident
+                                 across tiles the workgroups that fit the device at once */
 } miriam_op_info;
 
 /* Kernel family behind an op (diagnostic; results do not depend on it beyond rounding
@@ -138,7 +143,9 @@ typedef enum miriam_kernel_path {
     MIRIAM_PATH_DMA = 2,         /* contraction, global->LDS pipeline, per-lane K decode */
     MIRIAM_PATH_DMA_UNIFORM = 3, /* contraction, global->LDS pipeline, chunk-uniform filter taps */
     MIRIAM_PATH_SKINNY = 4,      /* small-batch fully connected, K split over logical waves */
-    MIRIAM_PATH_HALO = 5         /* direct 3x3 stride-1 convolution, input patch of the tile in LDS */
+    MIRIAM_PATH_HALO = 5,        /* direct 3x3 stride-1 convolution, input patch of the tile in LDS */
+    MIRIAM_PATH_RESIDENT = 6     /* direct 3x3 stride-1 convolution, weights resident in registers
+                                    across the tiles of a workgroup, input patch streamed through LDS */
 } miriam_kernel_path;
 
 /* ------------------------------------------------------------------ device */

@@ -52,12 +52,12 @@ class OpInfo(ctypes.Structure):
         ("num_tiles", ctypes.c_int64), ("logical_block", ctypes.c_int32),
         ("lds_bytes", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
         ("max_wg_per_cu", ctypes.c_int32 * 3), ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
-        ("path", ctypes.c_int32), ("ksplit", ctypes.c_int32),
+        ("path", ctypes.c_int32), ("ksplit", ctypes.c_int32), ("full_grid", ctypes.c_int32),
     ]
 
 
 # miriam_kernel_path
-PATH_OTHER, PATH_STAGED, PATH_DMA, PATH_DMA_UNIFORM, PATH_SKINNY, PATH_HALO = 0, 1, 2, 3, 4, 5
+PATH_OTHER, PATH_STAGED, PATH_DMA, PATH_DMA_UNIFORM, PATH_SKINNY, PATH_HALO, PATH_RESIDENT = 0, 1, 2, 3, 4, 5, 6
 
 
 class DeviceDesc(ctypes.Structure):

@@ -147,7 +147,7 @@ struct HipBackend : Backend {
         bool ok = true;
         for (size_t i = i0; i < i1; ++i) {
             const miriam_op *op = ops[i];
-            const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
+            const int grid = op_full_grid(op);
             if (op_launch(op, 0, op->T, grid, 256, cap, nullptr, nullptr, nullptr) != MIRIAM_OK) {
                 ok = false;
                 break;
@@ -335,7 +335,7 @@ struct FakeBackend : Backend {
     }
     int launch_captured(Captured *unit, int stream) override {
         int64_t st = std::max(mono_ns(), busy_until[stream]);
-        for (const miriam_op *op : static_cast<FakeUnit *>(unit)->ops) st += duration(op, op->T, op->T);
+        for (const miriam_op *op : static_cast<FakeUnit *>(unit)->ops) st += duration(op, op->T, op_full_grid(op));
         busy_until[stream] = st;
         return MIRIAM_OK;
     }
@@ -574,7 +574,7 @@ void launch_whole(Coord &c, Req *r, int stream) {
             c.inflight_us[stream] += total;
             for (size_t i = 0; i < t->ops.size(); ++i) {
                 const miriam_op *op = t->ops[i];
-                log_launch(c, r, (int)i, stream, (int)std::min<int64_t>(op->T, INT32_MAX), 256, false, 0, op->T,
+                log_launch(c, r, (int)i, stream, op_full_grid(op), 256, false, 0, op->T,
                            op->T, 0, t->prof[i].t_unsh_us);
             }
             std::lock_guard<std::mutex> lk(c.stat_mu);
@@ -587,7 +587,7 @@ void launch_whole(Coord &c, Req *r, int stream) {
     }
     for (size_t i = 0; i < r->task->ops.size(); ++i) {
         const miriam_op *op = r->task->ops[i];
-        const int grid = (int)std::min<int64_t>(op->T, INT32_MAX);
+        const int grid = op_full_grid(op);
         int rc = issue(c, r, (int)i, 0, op->T, grid, 256, stream, false, 0);
         if (rc != MIRIAM_OK) {
             r->status = rc;
@@ -674,7 +674,7 @@ Decision decide(Coord &c, Req *r, const miriam_op *crit_op) {
     Decision d{0, 256, 0, 0, 0.0};
     int bi = 2;
     if (crit_op) {
-        const int64_t n_rt = crit_op->T;  // critical kernels run unsharded: one workgroup per tile
+        const int64_t n_rt = op_full_grid(crit_op);  // critical kernels run unsharded (whole-tile-space grid)
         const int64_t s_rt = 256;
         const int64_t gl = eq2_limit(c.n_cu, n_rt);
         const int64_t sl = miriam_plan_eq2_block_limit(c.l_threads, s_rt);
@@ -794,7 +794,7 @@ int issue_segment(Coord &c, Req *r, const miriam_task::Segment &sg, int stream, 
     c.inflight_us[stream] += sg.est_us;
     for (size_t i = sg.i0; i < sg.i1; ++i) {
         const miriam_op *op = r->task->ops[i];
-        log_launch(c, r, (int)i, stream, (int)std::min<int64_t>(op->T, INT32_MAX), 256, false, 0, op->T, op->T, 0,
+        log_launch(c, r, (int)i, stream, op_full_grid(op), 256, false, 0, op->T, op->T, 0,
                    r->task->prof[i].t_unsh_us);
     }
     std::lock_guard<std::mutex> lk(c.stat_mu);
@@ -1093,7 +1093,7 @@ void profile_task(Coord &c, miriam_task *t) {
             continue;
         }
         const int greps = std::max(1, reps);
-        p.t_unsh_us = c.be->time_us(op, 0, op->T, (int)std::min<int64_t>(op->T, INT32_MAX), 256, greps);
+        p.t_unsh_us = c.be->time_us(op, 0, op->T, op_full_grid(op), 256, greps);
         for (int k = 0; k < 3; ++k) {
             const int64_t gp = std::min<int64_t>(op->T, (int64_t)c.n_cu * p.cap[k]);
             p.t_pers_us[k] = c.be->time_us(op, 0, op->T, (int)gp, 64 << k, greps);

@@ -97,6 +97,31 @@ __device__ __forceinline__ float apply_act(float v, int act) {
     }
 }
 
+// Activation fixed at compile time, and a dispatch that runs f(std::integral_constant<int, A>)
+// once for the runtime activation, so element loops carry no per-element branch.
+template <int ACT>
+__device__ __forceinline__ float act_c(float v) {
+    if constexpr (ACT == ACT_RELU) return v > 0.0f ? v : 0.0f;
+    else if constexpr (ACT == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
+    else if constexpr (ACT == ACT_GELU) return gelu_erf(v);
+    else return v;
+}
+
+template <int A>
+struct ActTag {
+    static constexpr int value = A;
+};
+
+template <class F>
+__device__ __forceinline__ void with_act(int act, F &&f) {
+    switch (act) {
+    case ACT_RELU: f(ActTag<ACT_RELU>{}); break;
+    case ACT_RELU6: f(ActTag<ACT_RELU6>{}); break;
+    case ACT_GELU: f(ActTag<ACT_GELU>{}); break;
+    default: f(ActTag<ACT_NONE>{}); break;
+    }
+}
+
 // The fused epilogue  v = act(BN(acc + bias[c]) + res)  in fp32.  Split into the
 // per-channel affine part (applied where the accumulator lives) and the residual /
 // activation part (applied where the output is stored); same operations, same order.

@@ -24,6 +24,7 @@ int igemm_kernels_bf16(int cfg, int lay, const void *out[3], int *lds);
 int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int skinny_kernels(int dtype, const void *out[3]);
+int rw_kernels(int dtype, int64_t c, const void *out[3], int *lds);  // resident-weight direct 3x3
 
 }  // namespace miriam
 
@@ -36,6 +37,7 @@ struct miriam_op {
     int lds_bytes;
     const void *kern[3];    // kernels for physical blocks 64, 128, 256
     int max_wg_per_cu[3];
+    int64_t full_grid;      // grid of a whole-tile-space launch (T, or the resident capacity)
     double flops, bytes;
     miriam::IgemmArgs ig;
     miriam::PixArgs px;
@@ -46,6 +48,11 @@ struct miriam_op {
 };
 
 namespace miriam {
+// Grid of the op's whole-tile-space (unsharded) launch.
+inline int op_full_grid(const miriam_op *op) {
+    return (int)(op->full_grid < INT32_MAX ? op->full_grid : INT32_MAX);
+}
+
 // Launch helper used by the public entry points and by the coordinator.
 int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
               int32_t *owner_wg, int32_t *owner_iter, int32_t *count);

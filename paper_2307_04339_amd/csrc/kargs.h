@@ -81,7 +81,7 @@ struct RowArgs {
 
 enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3 };
 enum RowKind { ROW_SOFTMAX = 0, ROW_LAYERNORM = 1 };
-enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3, LAY_VEC_UNI = 4, LAY_HALO = 5 };
-enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4, CFG_256x128 = 6, CFG_HALO = 7 };
+enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3, LAY_VEC_UNI = 4, LAY_HALO = 5, LAY_RW = 6 };
+enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4, CFG_256x128 = 6, CFG_HALO = 7, CFG_RW = 8 };
 
 }  // namespace miriam

@@ -47,7 +47,10 @@ constexpr int TILE_SKINNY = 5;  // descriptor tile code of the split-K skinny ke
 
 // Fill the per-physical-block residency of the op's kernels.  Without a device
 // the figures stay 0 ("unknown"); the error state of the runtime is cleared.
+static int device_cus();
+
 static void query_occupancy(miriam_op *op) {
+    op->full_grid = op->T;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) {
         (void)hipGetLastError();
@@ -61,6 +64,10 @@ static void query_occupancy(miriam_op *op) {
         else
             (void)hipGetLastError();
     }
+    // kernels that keep operands resident across tiles run persistently: as many workgroups
+    // as fit the device at once (one per tile when that is fewer)
+    if (op->family == FAM_IGEMM && op->lay == LAY_RW && op->max_wg_per_cu[2] > 0)
+        op->full_grid = std::min<int64_t>(op->T, (int64_t)device_cus() * op->max_wg_per_cu[2]);
 }
 
 static Epilogue make_epi(const miriam_op_desc &d, int64_t C) {
@@ -190,11 +197,32 @@ static int create_igemm(miriam_op *op) {
                          d.c % kt == 0 && d.ksplit <= 1;
     const int64_t halo_tx = cdiv(a.Wo, 32), halo_ty = cdiv(a.Ho, 4);
     const int64_t halo_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
+    // same tile with the weights resident in registers: fp16/bf16, C in {8, 16, 32, 64} (a
+    // workgroup's filter slice fits its registers), at most 64 output channels.  Chosen over
+    // the LDS-patch kernel and the implicit GEMM wherever it applies with 1.5 tiles per CU.
+    const bool rw_ok = d.kind == MIRIAM_OP_CONV2D && d.dtype != MIRIAM_F32 && d.kh == 3 && d.kw == 3 &&
+                       d.stride == 1 && a_vec && b_vec && (d.c == 8 || d.c == 16 || d.c == 32 || d.c == 64) &&
+                       a.Nc <= 64 && d.ksplit <= 1;
     int cfg = d.tile;
+    if (cfg == 0 && rw_ok && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5) cfg = CFG_RW;
     if (cfg == 0 && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5)
         cfg = CFG_HALO;
     if (cfg == 0) cfg = skinny_ok ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
-    if (cfg == CFG_HALO) {
+    if (cfg == CFG_RW) {
+        if (!rw_ok) return einval("tile 8 (resident-weight direct 3x3) needs an fp16/bf16 3x3 stride-1 conv with C in {8,16,32,64}, at most 64 output channels, 16-byte rows and no split K");
+        a.tX = halo_tx;
+        a.tY = halo_ty;
+        a.mT = halo_ty * halo_tx;
+        a.nT = 1;
+        a.ksplit = 1;
+        a.cps = 1;
+        op->T = d.n * a.mT;
+        op->cfg = cfg;
+        op->tile_m = 128;
+        op->tile_n = 64;
+        op->lay = LAY_RW;
+        if (rw_kernels(d.dtype, d.c, op->kern, &op->lds_bytes) != 0) return einval("no resident-weight kernel for this dtype / C");
+    } else if (cfg == CFG_HALO) {
         if (!halo_ok) return einval("tile 7 (direct 3x3) needs a 3x3 stride-1 conv with C a multiple of the 128-byte chunk, 16-byte rows and no split K");
         a.tX = halo_tx;
         a.tY = halo_ty;
@@ -521,12 +549,14 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
     out->bytes = op->bytes;
     if (op->family == FAM_SKINNY) out->path = MIRIAM_PATH_SKINNY;
     else if (op->family == FAM_IGEMM)
-        out->path = op->lay == LAY_HALO      ? MIRIAM_PATH_HALO
+        out->path = op->lay == LAY_RW        ? MIRIAM_PATH_RESIDENT
+                    : op->lay == LAY_HALO    ? MIRIAM_PATH_HALO
                     : op->lay == LAY_VEC_UNI ? MIRIAM_PATH_DMA_UNIFORM
                     : op->lay == LAY_VEC     ? MIRIAM_PATH_DMA
                                              : MIRIAM_PATH_STAGED;
     else out->path = MIRIAM_PATH_OTHER;
     out->ksplit = op->family == FAM_IGEMM ? op->ig.ksplit : 1;
+    out->full_grid = op_full_grid(op);
     return MIRIAM_OK;
 }
 

@@ -59,8 +59,9 @@ class ElasticOp:
             ctypes.c_void_p(count.data_ptr())), "miriam_elastic_launch_traced")
 
     def run(self, stream=None) -> None:
-        """Unsharded launch: one workgroup per tile, block 256."""
-        self.launch(0, self.T, self.T, 256, stream)
+        """Unsharded launch: the whole tile space at the op's full grid (one workgroup per
+        tile, or the resident capacity for kernels that keep operands across tiles), block 256."""
+        self.launch(0, self.T, int(self.info.full_grid), 256, stream)
 
     def run_plan(self, shards, grids, blocks, stream=None) -> None:
         for (b, l), g, bl in zip(shards, grids, blocks):

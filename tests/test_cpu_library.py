@@ -187,8 +187,13 @@ def test_gemm_tile_space(lib, M, N, K, tile, T):
     ("gemm", "F32", dict(m=4, kk=512), FAKE, "PATH_DMA_UNIFORM"),  # no fp32 skinny kernel
     ("conv", "F16", dict(c=64, tile=7), FAKE, "PATH_HALO"),      # direct 3x3 on request
     ("conv", "F32", dict(c=32, tile=7), FAKE, "PATH_HALO"),      # fp32 chunk is 32 channels
-    ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=64), FAKE, "PATH_HALO"),   # chosen: 784 tiles, N = 64
+    ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=64), FAKE, "PATH_RESIDENT"),  # chosen: 784 tiles, N = 64
+    ("conv", "F16", dict(n=8, h=112, w=112, c=8, k=64), FAKE, "PATH_RESIDENT"),    # 8-channel image stem
+    ("conv", "F32", dict(n=8, h=112, w=112, c=64, k=64), FAKE, "PATH_HALO"),       # no fp32 resident kernel
+    ("conv", "F16", dict(n=8, h=112, w=112, c=128, k=64), FAKE, "PATH_HALO"),      # C too wide for registers
     ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=128), FAKE, "PATH_DMA_UNIFORM"),  # wider: implicit GEMM
+    ("conv", "F16", dict(c=64, tile=8), FAKE, "PATH_RESIDENT"),  # resident weights on request
+    ("conv", "BF16", dict(c=8, k=20, tile=8), FAKE, "PATH_RESIDENT"),
 ])
 def test_kernel_path_selection(lib, kind, dtype, geo, addr, path):
     from paper_2307_04339_amd import _lib as L
@@ -216,3 +221,29 @@ def test_direct3x3_rejects_ineligible_convs(lib, geo):
     d.update(geo)
     rc, _ = _create(lib, _desc(**d))
     assert rc == L.EINVAL
+
+
+@pytest.mark.parametrize("geo", [dict(c=24), dict(c=128), dict(c=64, k=96), dict(c=64, stride=2),
+                                 dict(c=64, kh=5, kw=5, pad=2), dict(c=64, ksplit=2), dict(c=64, dtype=0)])
+def test_resident3x3_rejects_ineligible_convs(lib, geo):
+    from paper_2307_04339_amd import _lib as L
+    d = dict(kind=L.OP_CONV2D, dtype=L.F16, n=1, h=9, w=9, c=16, k=32, kh=3, kw=3, stride=1, pad=1,
+             x=FAKE, wt=FAKE, y=FAKE, tile=8)
+    d.update(geo)
+    rc, _ = _create(lib, _desc(**d))
+    assert rc == L.EINVAL
+
+
+def test_resident3x3_tile_space_and_full_grid(lib):
+    from paper_2307_04339_amd import _lib as L
+    # 2 x 15 x 37 output: 4 tile rows x 2 tile columns per image; without a device the
+    # whole-tile-space grid stays one workgroup per tile
+    rc, h = _create(lib, _desc(kind=L.OP_CONV2D, dtype=L.F16, n=2, h=15, w=37, c=64, k=64, kh=3, kw=3,
+                               stride=1, pad=1, x=FAKE, wt=FAKE, y=FAKE, tile=8))
+    assert rc == 0, lib.miriam_last_error()
+    info = L.OpInfo()
+    assert lib.miriam_op_query(h, ctypes.byref(info)) == 0
+    assert info.num_tiles == 2 * 4 * 2
+    assert (info.tile_m, info.tile_n) == (128, 64)
+    assert info.full_grid == info.num_tiles
+    lib.miriam_op_destroy(h)

@@ -265,11 +265,96 @@ def test_conv_direct3x3_matches_oracle_and_is_elastic(ops, orc, dtype, case):
 
 def test_conv_direct3x3_chosen_for_wide_layers(ops):
     from paper_2307_04339_amd import _lib as L
-    # a 112 x 112 x 64 -> 64 layer at batch 8: 896 tiles, one n tile
+    # a 112 x 112 x 64 -> 64 layer at batch 8: 896 tiles, one n tile; fp16 keeps the weights
+    # in registers, fp32 streams them through the LDS-patch kernel
     x, _ = rand((8, 112, 112, 64), "f16", seed=0)
     w, _ = rand((64, 3, 3, 64), "f16", seed=1, lo=-0.05, hi=0.05)
     y = empty((8, 112, 112, 64), "f16")
-    assert ops.conv2d(x, w, y, stride=1, pad=1).info.path == L.PATH_HALO
+    op = ops.conv2d(x, w, y, stride=1, pad=1)
+    assert op.info.path == L.PATH_RESIDENT
+    assert 1 <= op.info.full_grid <= op.T
+    xf, _ = rand((8, 112, 112, 64), "f32", seed=0)
+    wf, _ = rand((64, 3, 3, 64), "f32", seed=1, lo=-0.05, hi=0.05)
+    yf = empty((8, 112, 112, 64), "f32")
+    assert ops.conv2d(xf, wf, yf, stride=1, pad=1).info.path == L.PATH_HALO
     # stride 2 keeps the implicit GEMM
     y2 = empty((8, 56, 56, 64), "f16")
-    assert ops.conv2d(x, w, y2, stride=2, pad=1).info.path != L.PATH_HALO
+    assert ops.conv2d(x, w, y2, stride=2, pad=1).info.path not in (L.PATH_HALO, L.PATH_RESIDENT)
+
+
+# ------------------------------------ direct 3x3 kernel, weights in registers (tile 8)
+RW_CASES = [
+    # N, H, W, C, K, pad, act, epilogue
+    (2, 15, 37, 64, 64, 1, "relu", "bn"),        # ragged tile rows and columns
+    (1, 9, 70, 8, 64, 1, "relu", "bias"),        # 8-channel input: two taps per MFMA step, K = 72
+    (1, 30, 33, 64, 64, 0, "relu6", "bn_res"),   # no padding (28 x 31 output), residual
+    (3, 8, 32, 16, 40, 1, "none", "bn"),         # C = 16, K < 64 (upper channel half partly idle)
+    (2, 11, 20, 32, 24, 1, "gelu", "bias"),      # C = 32, only the lower channel half
+    (1, 6, 40, 8, 20, 1, "relu", "bias_res"),    # K not a multiple of 8: element stores
+]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", RW_CASES)
+def test_conv_resident3x3_matches_oracle_and_is_elastic(ops, orc, dtype, case):
+    from paper_2307_04339_amd import _lib as L
+    (x, w, y, kw), (x64, w64, rargs) = _halo_inputs(case, dtype)
+    op = ops.conv2d(x, w, y, tile=8, **kw)
+    assert op.info.path == L.PATH_RESIDENT
+    op.launch(0, op.T, op.T, 256)  # one workgroup per tile
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, **rargs)
+    err = rel_err(to_f64(y), ref)
+    print(f"resident 3x3 {dtype} {case}: T={op.T} rel={err:.3e}")
+    assert err <= RTOL[dtype], err
+    ref_bits = bits(y)
+    y.fill_(float("nan"))
+    op.run()  # full grid
+    torch.cuda.synchronize()
+    assert bits(y) == ref_bits
+    rng = np.random.default_rng(7)
+    for n in [1, 2, 3, 5]:
+        if n > op.T:
+            continue
+        for block in [64, 128, 256]:
+            y.fill_(float("nan"))
+            plan = orc.balanced_split(op.T, n)
+            for j in rng.permutation(n):
+                b, l = plan[j]
+                op.launch(b, l, int(rng.choice([1, 2, 7, l])), block)
+            torch.cuda.synchronize()
+            assert bits(y) == ref_bits, (n, block)
+
+
+@pytest.mark.parametrize("C", [8, 64])
+def test_conv_resident3x3_integer_inputs_exact(ops, orc, C):
+    # integer operands in {-1, 0, 1}: |partial sums| <= 9 C <= 576, exact in fp32 and fp16
+    x, x64 = ints((2, 10, 45, C), "f16", seed=5, lo=-1, hi=1)
+    w, w64 = ints((64, 3, 3, C), "f16", seed=6, lo=-1, hi=1)
+    y = empty((2, 10, 45, 64), "f16")
+    op = ops.conv2d(x, w, y, stride=1, pad=1, tile=8)
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, stride=1, pad=1)
+    assert np.array_equal(to_f64(y), ref)
+
+
+def test_conv_resident3x3_tile_map_matches_oracle(ops, orc):
+    x, _ = rand((2, 21, 70, 64), "f16", seed=8)
+    w, _ = rand((64, 3, 3, 64), "f16", seed=9, lo=-0.1, hi=0.1)
+    y = empty((2, 21, 70, 64), "f16")
+    op = ops.conv2d(x, w, y, stride=1, pad=1, tile=8)
+    T = op.T
+    assert T == 2 * 6 * 3
+    for n, grids, block in [(1, [T], 256), (4, [5, 64, 1, 3], 128), (3, [7, 7, 7], 64), (2, [4, 2], 256)]:
+        plan = orc.balanced_split(T, n)
+        ow = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+        oi = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros((T,), dtype=torch.int32, device="cuda")
+        for (b, l), g in zip(plan, grids):
+            op.launch_traced(b, l, g, block, ow, oi, cnt)
+        torch.cuda.synchronize()
+        _, wg_ref, it_ref, cnt_ref = orc.owner_map(T, plan, grids)
+        assert np.array_equal(cnt.cpu().numpy(), cnt_ref)
+        assert np.array_equal(ow.cpu().numpy(), wg_ref)
+        assert np.array_equal(oi.cpu().numpy(), it_ref)
