@@ -106,13 +106,17 @@ __global__ __launch_bounds__(kWave * P, (P == 4 ? 2 : 1)) void halo_kernel(Igemm
     const int lrow = lane >> 3, slot = lane & 7;
 
     int iter = 0;
-    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+    // tile id = ((image * tY + tile row) * tX + tile column) * nT + n tile, advanced by the grid
+    // without division
+    TileDigits<4> td;
+    {
+        const uint32_t radix[4] = {nT32, tX32, tY32, 0u};
+        td.init((uint32_t)(sh.begin + rank), (uint32_t)G, radix);
+    }
+    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter, td.advance()) {
         trace_tile(sh, t, iter);
         // tile id -> (image, tile row, tile column, n tile), n fastest; ids < 2^31 (checked at creation)
-        const uint32_t t32 = (uint32_t)t;
-        const uint32_t sp = t32 / nT32, nt = t32 - sp * nT32;
-        const uint32_t r2 = sp / tX32, tx = sp - r2 * tX32;
-        const uint32_t img = r2 / tY32, ty = r2 - img * tY32;
+        const uint32_t nt = td.d[0], tx = td.d[1], ty = td.d[2], img = td.d[3];
         const int32_t oy0 = (int32_t)ty * TH, ox0 = (int32_t)tx * TW;
         const int64_t n0 = (int64_t)nt * TN;
 
@@ -243,23 +247,27 @@ __global__ __launch_bounds__(kWave * P, (P == 4 ? 2 : 1)) void halo_kernel(Igemm
                 const int lam = (rd * SL + sl) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
 #pragma unroll
-                for (int i = 0; i < BM; ++i)
+                for (int jn = 0; jn < BN; ++jn) {
+                    const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                    const int64_t n = n0 + col;
+                    float sc, shf;
+                    chan_affine(a.epi, n < a.Nc ? n : 0, sc, shf);
 #pragma unroll
-                    for (int jn = 0; jn < BN; ++jn) {
-                        const int col = wn * (TN / 2) + jn * MS + lane % MS;
-                        const int64_t n = n0 + col;
-                        const ChanParams cp = chan_params(a.epi, n < a.Nc ? n : 0);
+                    for (int i = 0; i < BM; ++i) {
+                        float *const cb = Cs + (wm * (TM / 2) + i * MS + (lane / MS) * 4) * LDC + col;
 #pragma unroll
                         for (int e = 0; e < MF::NACC; ++e) {
-                            const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
-                            const int row = wm * (TM / 2) + i * MS + rr;
-                            Cs[row * LDC + col] = epilogue_pre(a.epi, cp, acc[sl][i][jn][e]);
+                            const int rr = (e / 4) * (4 * (kWave / MS)) + (e % 4);
+                            cb[rr * LDC] = acc[sl][i][jn][e] * sc + shf;
                         }
                     }
+                }
             }
             __syncthreads();
             // ---- stage 2: + residual, activation, one rounding, 16-byte stores of whole tile rows
-            {
+            auto stage2 = [&](auto actc, auto resc) {
+                constexpr int ACT = decltype(actc)::value;
+                constexpr bool RES = decltype(resc)::value != 0;
                 constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
                 constexpr bool FULL = (SL * P) % 2 == 0;
                 constexpr int RV = FULL ? 2 * CV : CV;
@@ -277,22 +285,26 @@ __global__ __launch_bounds__(kWave * P, (P == 4 ? 2 : 1)) void halo_kernel(Igemm
                     const float *cr = Cs + row * LDC + col;
                     const int64_t off = m * a.ldy + n;
                     if (a.vec_store && n + VEC <= a.Nc) {
-                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
                         Vec16<T> o;
+                        if constexpr (RES) {
+                            const Vec16<T> rv = ld_vec(R + off);
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, cr[e], TypeOps<T>::to_f(rv.e[e])));
+                            for (int e = 0; e < VEC; ++e)
+                                o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e] + TypeOps<T>::to_f(rv.e[e])));
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        }
                         st_vec(Y + off, o);
                     } else {
 #pragma unroll
                         for (int e = 0; e < VEC; ++e)
-                            if (n + e < a.Nc) {
-                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
-                                st_f(Y + off + e, epilogue_post(a.epi, cr[e], res));
-                            }
+                            if (n + e < a.Nc) st_f(Y + off + e, act_c<ACT>(RES ? cr[e] + ld_f(R + off + e) : cr[e]));
                     }
                 }
-            }
+            };
+            if (a.epi.flags & EPI_RES) with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<1>{}); });
+            else with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<0>{}); });
             __syncthreads();
         }
     }

@@ -127,9 +127,7 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
     for (int rd = 0; rd < ROUNDS; ++rd) {
         const int wn = P == 4 ? (pw & 1) : (P == 2 ? pw : rd);
         const int64_t col = 32 * wn + xl;
-        const ChanParams cp = chan_params(a.epi, col < a.Nc ? col : 0);
-        esc[rd] = cp.scale;
-        esh[rd] = (a.epi.flags & EPI_BN) ? (cp.bias - cp.mean) * cp.scale + cp.beta : cp.bias;
+        chan_affine(a.epi, col < a.Nc ? col : 0, esc[rd], esh[rd]);
     }
 
     // tile id = (image * tY + tile row) * tX + tile column, kept as a mixed-radix cursor that

@@ -30,6 +30,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2, ACT_GELU = 3 };
 enum EpiFlag { EPI_BIAS = 1, EPI_BN = 2, EPI_RES = 4 };
 
+// n / d for n < 2^31 with the divisor's constants from make_fastdiv.
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
+    return (__umulhi(n, f.m) + n) >> f.s;
+}
+
 // Logical rank of physical workgroup g among G, dies dealt round-robin.
 __device__ __forceinline__ int64_t wg_rank(int64_t g, int64_t G) {
     const int64_t q = G / kDies, r = G % kDies;
@@ -151,6 +156,43 @@ __device__ __forceinline__ float epilogue_post(const Epilogue &e, float v, float
     if (e.flags & EPI_RES) v += res;
     return apply_act(v, e.act);
 }
+
+// Per-channel affine part folded into one multiply-add, v = acc * sc + sh (bias, then batch
+// norm); the residual and the activation follow.
+__device__ __forceinline__ void chan_affine(const Epilogue &e, int64_t c, float &sc, float &sh) {
+    const ChanParams p = chan_params(e, c);
+    sc = p.scale;
+    sh = (e.flags & EPI_BN) ? (p.bias - p.mean) * p.scale + p.beta : p.bias;
+}
+
+// Digits (least significant first) of a tile id in a mixed-radix tile space, advanced by a
+// fixed stride with carries instead of per-tile divisions; the top digit is unbounded.
+template <int L>
+struct TileDigits {
+    uint32_t d[L], r[L], g[L];
+    __device__ __forceinline__ void init(uint32_t t, uint32_t stride, const uint32_t (&radix)[L]) {
+#pragma unroll
+        for (int i = 0; i + 1 < L; ++i) {
+            r[i] = radix[i];
+            d[i] = t % r[i];
+            t /= r[i];
+            g[i] = stride % r[i];
+            stride /= r[i];
+        }
+        d[L - 1] = t;
+        g[L - 1] = stride;
+    }
+    __device__ __forceinline__ void advance() {
+        uint32_t c = 0;
+#pragma unroll
+        for (int i = 0; i + 1 < L; ++i) {
+            const uint32_t v = d[i] + g[i] + c;  // below 2 r[i]
+            c = v >= r[i] ? 1u : 0u;
+            d[i] = v - c * r[i];
+        }
+        d[L - 1] += g[L - 1] + c;
+    }
+};
 
 // Whole epilogue for one element of channel c.
 __device__ __forceinline__ float epilogue_apply(const Epilogue &e, float acc, int64_t c, float res) {

@@ -136,14 +136,16 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
     const int32_t C32 = (int32_t)a.C, KW32 = a.KW, KH32 = a.KH;
 
     int iter = 0;
-    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+    TileDigits<4> td;
+    {
+        const uint32_t radix[4] = {(uint32_t)a.nT, (uint32_t)a.mT, (uint32_t)a.bdiv, 0u};
+        td.init((uint32_t)(sh.begin + rank), (uint32_t)G, radix);
+    }
+    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter, td.advance()) {
         trace_tile(sh, t, iter);
-        // tile id -> (batch, m tile, n tile); every index here is below 2^31 (checked at creation)
-        const uint32_t per = (uint32_t)(a.mT * a.nT), t32 = (uint32_t)t;
-        const uint32_t bi = t32 / per;
-        const uint32_t rem = t32 - bi * per;
-        const uint32_t mt = rem / (uint32_t)a.nT, nt = rem - mt * (uint32_t)a.nT;
-        const uint32_t b0 = bi / (uint32_t)a.bdiv, b1 = bi - b0 * (uint32_t)a.bdiv;
+        // tile id = ((b0 * bdiv + b1) * mT + mt) * nT + nt; every index here is below 2^31
+        // (checked at creation); the digits advance by the grid without division
+        const uint32_t nt = td.d[0], mt = td.d[1], b1 = td.d[2], b0 = td.d[3];
         const T *Xb = X + b0 * a.sx0 + b1 * a.sx1;
         const T *Wb = Wt + b0 * a.sw0 + b1 * a.sw1;
         const int64_t yoff = b0 * a.sy0 + b1 * a.sy1;
@@ -160,9 +162,9 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
             const int64_t m = m0 + row;
             a_ok[j] = (v < TM * KPR) && (m < a.M);
             const uint32_t mm = a_ok[j] ? (uint32_t)m : 0u;
-            const uint32_t img = mm / HoWo32;
+            const uint32_t img = fdiv(mm, a.fd_howo);
             const uint32_t pq = mm - img * HoWo32;
-            const uint32_t p = pq / Wo32, q = pq - p * Wo32;
+            const uint32_t p = fdiv(pq, a.fd_wo), q = pq - p * Wo32;
             a_img[j] = (int64_t)img * a.img_x;
             a_h0[j] = (int32_t)p * a.stride - a.pad;
             a_w0[j] = (int32_t)q * a.stride - a.pad;
@@ -324,24 +326,28 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                 const int lam = (rd * SL + s) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
 #pragma unroll
-                for (int i = 0; i < BM; ++i)
+                for (int jn = 0; jn < BN; ++jn) {
+                    const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                    const int64_t n = n0 + col;
+                    float sc, shf;
+                    chan_affine(a.epi, n < a.Nc ? n : 0, sc, shf);
 #pragma unroll
-                    for (int jn = 0; jn < BN; ++jn) {
-                        const int col = wn * (TN / 2) + jn * MS + lane % MS;
-                        const int64_t n = n0 + col;
-                        const ChanParams cp = chan_params(a.epi, n < a.Nc ? n : 0);
+                    for (int i = 0; i < BM; ++i) {
+                        float *const cb = Cs + (wm * (TM / 2) + i * MS + (lane / MS) * 4) * LDC + col;
 #pragma unroll
                         for (int e = 0; e < MF::NACC; ++e) {
-                            const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
-                            const int row = wm * (TM / 2) + i * MS + rr;
-                            Cs[row * LDC + col] = epilogue_pre(a.epi, cp, acc[s][i][jn][e]);
+                            const int rr = (e / 4) * (4 * (kWave / MS)) + (e % 4);
+                            cb[rr * LDC] = acc[s][i][jn][e] * sc + shf;
                         }
                     }
+                }
             }
             __syncthreads();
             // ---- stage 2: + residual, activation, one rounding, coalesced row stores
             // (whole tile rows per store instruction when the pass holds both column halves)
-            {
+            auto stage2 = [&](auto actc, auto resc) {
+                constexpr int ACT = decltype(actc)::value;
+                constexpr bool RES = decltype(resc)::value != 0;
                 constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
                 constexpr bool FULL = (SL * P) % 2 == 0;
                 constexpr int RV = FULL ? 2 * CV : CV;
@@ -358,22 +364,26 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
                     const float *cr = Cs + row * LDC + col;
                     const int64_t off = yoff + m * a.ldy + n;
                     if (a.vec_store && n + VEC <= a.Nc) {
-                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
                         Vec16<T> o;
+                        if constexpr (RES) {
+                            const Vec16<T> rv = ld_vec(R + off);
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, cr[e], TypeOps<T>::to_f(rv.e[e])));
+                            for (int e = 0; e < VEC; ++e)
+                                o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e] + TypeOps<T>::to_f(rv.e[e])));
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        }
                         st_vec(Y + off, o);
                     } else {
 #pragma unroll
                         for (int e = 0; e < VEC; ++e)
-                            if (n + e < a.Nc) {
-                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
-                                st_f(Y + off + e, epilogue_post(a.epi, cr[e], res));
-                            }
+                            if (n + e < a.Nc) st_f(Y + off + e, act_c<ACT>(RES ? cr[e] + ld_f(R + off + e) : cr[e]));
                     }
                 }
-            }
+            };
+            if (a.epi.flags & EPI_RES) with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<1>{}); });
+            else with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<0>{}); });
             __syncthreads();
         }
     }

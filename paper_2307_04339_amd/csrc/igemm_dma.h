@@ -117,17 +117,19 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
     // this lane's place in every load instruction: row offset in the 8-row group, slot
     const int lrow = lane >> 3, slot = lane & 7;
 
+    const bool has_res = (a.epi.flags & EPI_RES) != 0;
+    // tile id = (((b0 * bdiv + b1) * mT + mt) * nT + nt) * ksplit + slice; indices < 2^31 (checked
+    // at creation); the digits advance by the grid without division
+    TileDigits<5> td;
+    {
+        const uint32_t radix[5] = {(uint32_t)a.ksplit, (uint32_t)a.nT, (uint32_t)a.mT, (uint32_t)a.bdiv, 0u};
+        td.init((uint32_t)(sh.begin + rank), (uint32_t)G, radix);
+    }
     int iter = 0;
-    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter, td.advance()) {
         trace_tile(sh, t, iter);
-        // tile id -> (output tile, K slice) -> (batch, m tile, n tile); indices < 2^31 (checked at creation)
-        const uint32_t kslices = (uint32_t)a.ksplit;
-        const uint32_t otile = (uint32_t)t / kslices, slice = (uint32_t)t - otile * kslices;
-        const uint32_t per = (uint32_t)(a.mT * a.nT), t32 = otile;
-        const uint32_t bi = t32 / per;
-        const uint32_t rem = t32 - bi * per;
-        const uint32_t mt = rem / (uint32_t)a.nT, nt = rem - mt * (uint32_t)a.nT;
-        const uint32_t b0 = bi / (uint32_t)a.bdiv, b1 = bi - b0 * (uint32_t)a.bdiv;
+        const uint32_t slice = td.d[0], nt = td.d[1], mt = td.d[2], b1 = td.d[3], b0 = td.d[4];
+        const uint32_t otile = ((b0 * (uint32_t)a.bdiv + b1) * (uint32_t)a.mT + mt) * (uint32_t)a.nT + nt;
         const T *Xb = X + b0 * a.sx0 + b1 * a.sx1;
         const T *Wb = Wt + b0 * a.sw0 + b1 * a.sw1;
         const int64_t yoff = b0 * a.sy0 + b1 * a.sy1;
@@ -145,9 +147,9 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             const int64_t m = m0 + row;
             a_ok[j] = m < a.M;
             const uint32_t mm = a_ok[j] ? (uint32_t)m : 0u;
-            const uint32_t img = mm / HoWo32;
+            const uint32_t img = fdiv(mm, a.fd_howo);
             const uint32_t pq = mm - img * HoWo32;
-            const uint32_t p = pq / Wo32, q = pq - p * Wo32;
+            const uint32_t p = fdiv(pq, a.fd_wo), q = pq - p * Wo32;
             a_base[j] = Xb + (int64_t)img * a.img_x;
             a_h0[j] = (int32_t)p * a.stride - a.pad;
             a_w0[j] = (int32_t)q * a.stride - a.pad;
@@ -368,25 +370,27 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 continue;
             }
 
-            // ---- epilogue, stage 1: accumulators (+ bias, BN) -> LDS as fp32
+            // ---- epilogue, stage 1: accumulators * sc + sh (bias, BN) -> LDS as fp32
 #pragma unroll
             for (int s = 0; s < SL; ++s) {
                 const int lam = (rd * SL + s) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
 #pragma unroll
-                for (int i = 0; i < BM; ++i)
+                for (int jn = 0; jn < BN; ++jn) {
+                    const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                    const int64_t n = n0 + col;
+                    float sc, shf;
+                    chan_affine(a.epi, n < a.Nc ? n : 0, sc, shf);
 #pragma unroll
-                    for (int jn = 0; jn < BN; ++jn) {
-                        const int col = wn * (TN / 2) + jn * MS + lane % MS;
-                        const int64_t n = n0 + col;
-                        const ChanParams cp = chan_params(a.epi, n < a.Nc ? n : 0);
+                    for (int i = 0; i < BM; ++i) {
+                        float *const cb = Cs + (wm * (TM / 2) + i * MS + (lane / MS) * 4) * LDC + col;
 #pragma unroll
                         for (int e = 0; e < MF::NACC; ++e) {
-                            const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
-                            const int row = wm * (TM / 2) + i * MS + rr;
-                            Cs[row * LDC + col] = epilogue_pre(a.epi, cp, acc[s][i][jn][e]);
+                            const int rr = (e / 4) * (4 * (kWave / MS)) + (e % 4);
+                            cb[rr * LDC] = acc[s][i][jn][e] * sc + shf;
                         }
                     }
+                }
             }
             __syncthreads();
             // ---- stage 2: + residual, activation, one rounding, coalesced row stores.
@@ -394,7 +398,9 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             // consecutive threads cover whole output rows of the tile, so every store
             // instruction writes full rows (TN * sizeof(T) contiguous bytes each) rather
             // than half rows whose other halves arrive later.
-            {
+            auto stage2 = [&](auto actc, auto resc) {
+                constexpr int ACT = decltype(actc)::value;
+                constexpr bool RES = decltype(resc)::value != 0;
                 constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
                 constexpr bool FULL = (SL * P) % 2 == 0;
                 constexpr int RV = FULL ? 2 * CV : CV;  // vectors per stored row segment
@@ -412,22 +418,26 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                     const float *cr = Cs + row * LDC + col;
                     const int64_t off = yoff + m * a.ldy + n;
                     if (a.vec_store && n + VEC <= a.Nc) {
-                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
                         Vec16<T> o;
+                        if constexpr (RES) {
+                            const Vec16<T> rv = ld_vec(R + off);
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, cr[e], TypeOps<T>::to_f(rv.e[e])));
+                            for (int e = 0; e < VEC; ++e)
+                                o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e] + TypeOps<T>::to_f(rv.e[e])));
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        }
                         st_vec(Y + off, o);
                     } else {
 #pragma unroll
                         for (int e = 0; e < VEC; ++e)
-                            if (n + e < a.Nc) {
-                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
-                                st_f(Y + off + e, epilogue_post(a.epi, cr[e], res));
-                            }
+                            if (n + e < a.Nc) st_f(Y + off + e, act_c<ACT>(RES ? cr[e] + ld_f(R + off + e) : cr[e]));
                     }
                 }
-            }
+            };
+            if (has_res) with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<1>{}); });
+            else with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<0>{}); });
             __syncthreads();
         }
 
@@ -469,8 +479,9 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                         Vec16<T> o;
 #pragma unroll
                         for (int e = 0; e < VEC; ++e) {
-                            const float pre = epilogue_pre(a.epi, chan_params(a.epi, n + e), v[e]);
-                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, pre, TypeOps<T>::to_f(rv.e[e])));
+                            float sc, shf;
+                            chan_affine(a.epi, n + e, sc, shf);
+                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, v[e] * sc + shf, TypeOps<T>::to_f(rv.e[e])));
                         }
                         st_vec(Y + off, o);
                     } else {
@@ -478,8 +489,9 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                         for (int e = 0; e < VEC; ++e)
                             if (n + e < a.Nc) {
                                 const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
-                                const float pre = epilogue_pre(a.epi, chan_params(a.epi, n + e), v[e]);
-                                st_f(Y + off + e, epilogue_post(a.epi, pre, res));
+                                float sc, shf;
+                                chan_affine(a.epi, n + e, sc, shf);
+                                st_f(Y + off + e, epilogue_post(a.epi, v[e] * sc + shf, res));
                             }
                     }
                 }

@@ -11,6 +11,29 @@ constexpr int kLogicalBlock = 256;  // threads of the logical block
 constexpr int kWave = 64;           // wavefront size of CDNA
 constexpr int kDies = 8;            // XCDs of an MI355X; workgroups are dealt to them round-robin
 
+// Division of n < 2^31 by a divisor d >= 1 fixed per operator, as a multiply-high, an add and
+// a shift (unsigned division by invariant integers, Granlund and Montgomery 1994):
+//   l = ceil(log2 d),  m = floor(2^32 (2^l - d) / d) + 1,  n / d = (mulhi(n, m) + n) >> l.
+struct FastDiv {
+    uint32_t m;
+    uint32_t s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 32 && (1ull << l) < (uint64_t)d) ++l;
+    FastDiv f;
+    f.m = (uint32_t)((((1ull << l) - (uint64_t)d) << 32) / (uint64_t)d + 1ull);
+    f.s = l;
+    return f;
+}
+
+// Host evaluation of the same formula (used to check the constants).
+inline uint32_t fastdiv_host(uint32_t n, FastDiv f) {
+    const uint32_t hi = (uint32_t)(((uint64_t)n * (uint64_t)f.m) >> 32);
+    return (uint32_t)(((uint64_t)hi + (uint64_t)n) >> f.s);
+}
+
 // Shard description passed to every kernel.  The trace arrays are null except
 // in traced launches, where they record the tile -> (workgroup, iteration) map.
 struct Shard {
@@ -46,6 +69,7 @@ struct IgemmArgs {
     int64_t bdiv, sx0, sx1, sw0, sw1, sy0, sy1;  // batch offsets
     int64_t img_x;         // elements between images of x
     int64_t tY, tX;        // direct 3x3 kernel: tile rows and tile columns per output image
+    FastDiv fd_howo, fd_wo; // division by Ho * Wo and by Wo (output pixel -> image, row, column)
     int32_t vec_store;     // 1: output / residual rows allow 16-byte vector access
     int32_t ksplit;        // K slices per output tile (1 = none); tile id = output tile * ksplit + slice
     int32_t cps;           // K chunks per slice

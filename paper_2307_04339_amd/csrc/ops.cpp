@@ -181,6 +181,9 @@ static int create_igemm(miriam_op *op) {
     if (rc) return rc;
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.Nc);
+    if (a.Ho * a.Wo >= (int64_t)INT32_MAX) return einval("contraction: output image too large for 32-bit pixel indexing");
+    a.fd_howo = make_fastdiv((uint32_t)(a.Ho * a.Wo));
+    a.fd_wo = make_fastdiv((uint32_t)a.Wo);
 
     a.vec_store = (a.ldy % V == 0) && (a.sy0 % V == 0) && (a.sy1 % V == 0) && aligned16(d.y) &&
                   (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
