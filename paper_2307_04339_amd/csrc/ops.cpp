@@ -245,7 +245,36 @@ static int create_igemm(miriam_op *op) {
         op->family = FAM_SKINNY;
         a.mT = 1;
         a.nT = cdiv(a.Nc, 16);
-        op->T = a.nT;
+        // K slices: each slice keeps at least one 256-element group per logical wave.  The
+        // library choice splits until the op has about four tiles per CU, so a shard of a
+        // quarter of the op still fills the GPU.
+        const int64_t max_ks = std::max<int64_t>(1, cdiv(a.K, 256) / 4);
+        int64_t ks = d.ksplit > 1 ? std::min<int64_t>(d.ksplit, max_ks)
+                     : d.ksplit == 1 ? 1
+                                     : std::min<int64_t>(max_ks, cdiv(4 * (int64_t)device_cus(), a.nT));
+        ks = std::max<int64_t>(1, ks);
+        a.ksplit = 1;
+        if (ks > 1) {
+            const size_t wbytes = (size_t)a.nT * (size_t)ks * 16 * 16 * sizeof(float);
+            const size_t cbytes = (size_t)a.nT * sizeof(int32_t);
+            if (hipMalloc(&op->work, wbytes) == hipSuccess && hipMalloc(&op->counters, cbytes) == hipSuccess &&
+                hipMemset(op->counters, 0, cbytes) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
+                a.ksplit = (int32_t)ks;
+                a.work = static_cast<float *>(op->work);
+                a.counters = static_cast<int32_t *>(op->counters);
+            } else {
+                (void)hipGetLastError();
+                if (op->work) (void)hipFree(op->work);
+                if (op->counters) (void)hipFree(op->counters);
+                (void)hipGetLastError();
+                op->work = op->counters = nullptr;
+                if (d.ksplit > 1) {
+                    set_error("split-K workspace allocation failed");
+                    return MIRIAM_ENOMEM;
+                }
+            }
+        }
+        op->T = a.nT * a.ksplit;
         op->cfg = cfg;
         op->tile_m = op->tile_n = 16;
         op->lay = LAY_VEC;
@@ -558,7 +587,7 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
                     : op->lay == LAY_VEC     ? MIRIAM_PATH_DMA
                                              : MIRIAM_PATH_STAGED;
     else out->path = MIRIAM_PATH_OTHER;
-    out->ksplit = op->family == FAM_IGEMM ? op->ig.ksplit : 1;
+    out->ksplit = (op->family == FAM_IGEMM || op->family == FAM_SKINNY) ? op->ig.ksplit : 1;
     out->full_grid = op_full_grid(op);
     return MIRIAM_OK;
 }

@@ -79,6 +79,34 @@ def test_gemm_matches_oracle(ops, orc, dtype, case):
 
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("M,N,K,ksplit", [(4, 300, 4096, 4), (8, 1000, 8192, 0), (2, 64, 3328, 3),
+                                          (16, 200, 2048, 2)])
+def test_skinny_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, M, N, K, ksplit):
+    # K slices reduced in fixed order by the last-arriving slice; library choice (0) splits
+    # until the op has about four tiles per CU
+    seed = (M * 7 + N * 3 + K) % 991
+    x, x64 = rand((M, K), dtype, seed)
+    w, w64 = rand((N, K), dtype, seed + 1, -0.05, 0.05)
+    b64 = np.random.default_rng(seed + 2).uniform(-1, 1, N).astype(np.float32).astype(np.float64)
+    y = empty((M, N), dtype)
+    op = ops.gemm(x, w, y, bias=f32_dev(b64), act="relu", tile=5, ksplit=ksplit)
+    assert op.info.ksplit > 1
+    assert op.T == op.info.ksplit * ((N + 15) // 16)
+    op.run()
+    torch.cuda.synchronize()
+    ref = orc.linear(x64, w64, bias=b64, act="relu")
+    err = rel_err(to_f64(y), ref)
+    print(f"skinny split K {dtype} {M}x{N}x{K}: ksplit={op.info.ksplit} T={op.T} rel={err:.3e}")
+    assert err <= RTOL[dtype], err
+    _elastic_bitwise(op, y, orc, plans=(1, 2, 3, 8))
+    # two passes in a row: the arrival counters return to zero after each
+    op.run()
+    op.run()
+    torch.cuda.synchronize()
+    assert rel_err(to_f64(y), ref) <= RTOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("B,S", [(1, 128), (2, 96)])
 def test_attention_bgemm_matches_oracle(ops, orc, dtype, B, S):
     # packed QKV [B*S, 3*768]; scores[b,h] = Q_bh K_bh^T; ctx[b*S+i, h*64+j] = P_bh V_bh
