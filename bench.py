@@ -56,6 +56,20 @@ def pct(xs, q):
 
 
 # ----------------------------------------------------------- kernel timing
+class CacheFlush:
+    """Evicts the L2 caches and the Infinity Cache before a timed launch by reading a 512 MiB
+    buffer (twice the Infinity Cache).  A read pass leaves clean lines behind; a write pass
+    would leave dirty lines that the timed kernel then pays to write back."""
+
+    def __init__(self):
+        import torch
+        self.buf = torch.ones(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
+        self.sink = None
+
+    def __call__(self):
+        self.sink = self.buf.sum()
+
+
 def time_layers(net, reps, flush):
     """Average unsharded duration of every layer, HIP events on torch's current stream."""
     import torch
@@ -65,7 +79,7 @@ def time_layers(net, reps, flush):
         torch.cuda.synchronize()
         total = 0.0
         for _ in range(reps):
-            flush.zero_()
+            flush()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
@@ -89,8 +103,8 @@ def time_layers(net, reps, flush):
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # device code of the contraction kernels; the host-side choice of kernel is checked through
 # the kernel path and tile recorded with the counters
-KERNEL_SOURCES = ["conv_halo.h", "igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h", "kern_igemm_f16.hip",
-                  "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "kern_skinny.hip"]
+KERNEL_SOURCES = ["conv_halo.h", "conv_rw.h", "igemm_dma.h", "igemm.h", "elastic_common.h", "kargs.h",
+                  "kern_igemm_f16.hip", "kern_igemm_bf16.hip", "kern_igemm_f32.hip", "kern_rw.hip", "kern_skinny.hip"]
 
 
 def kernel_source_hash():
@@ -139,9 +153,11 @@ def shard_overhead(layer, reps, flush, n_cu, lib):
     cap = max(1, op.info.max_wg_per_cu[2])
 
     def timed(plan):
-        tot = 0.0
+        # median over the repetitions: a single host-side stall between two shard launches
+        # would otherwise dominate a 20-sample mean
+        ts = []
         for _ in range(reps):
-            flush.zero_()
+            flush()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
@@ -149,10 +165,10 @@ def shard_overhead(layer, reps, flush, n_cu, lib):
                 op.launch(b, l, g, bl)
             e1.record()
             e1.synchronize()
-            tot += e0.elapsed_time(e1)
-        return 1000.0 * tot / reps
+            ts.append(e0.elapsed_time(e1))
+        return 1000.0 * float(np.median(ts))
 
-    base = timed([(0, T, T, 256)])
+    base = timed([(0, T, int(op.info.full_grid), 256)])
     res = {"unsharded_us": round(base, 2)}
     for n in (1, 2, 4, 8):
         if n > T:
@@ -391,7 +407,7 @@ def main():
         n.forward()
     torch.cuda.synchronize()
     phases = set(args.phases.split(","))
-    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
+    flush = CacheFlush()
     result = {}
 
     kern = None

@@ -1341,6 +1341,7 @@ int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_
     r->stream = criticality ? 0 : 1 + task->id % (g->n_streams - 1);
     task->pending.fetch_add(1);
     for (miriam_op *op : task->ops) op->pending.fetch_add(1);
+    uint64_t ticket;
     {
         std::lock_guard<std::mutex> lk(g->mu);
         if (g->stopping) {
@@ -1349,12 +1350,13 @@ int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_
             delete r;
             return estate("coordinator is shutting down");
         }
-        r->ticket = g->next_ticket++;
+        // the dispatcher owns r once it is queued (it may finish and free it at any time)
+        ticket = r->ticket = g->next_ticket++;
         g->inbox.push_back(r);
         g->outstanding++;
     }
     g->cv.notify_one();
-    if (ticket_out) *ticket_out = r->ticket;
+    if (ticket_out) *ticket_out = ticket;
     return MIRIAM_OK;
 }
 

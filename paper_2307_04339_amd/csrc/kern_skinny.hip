@@ -23,7 +23,7 @@
 // [k0 + 32 j, k0 + 32 j + 32), k-group g of the lanes holding [k0 + 32 j + 8 g, +8),
 // so one load instruction reads 64 contiguous bytes of each of the 16 weight rows.
 // The next group's loads are issued before the current group's MFMAs, so two groups
-// (16 KB of weights per wave) are in flight.
+// (8 KB of weights per wave) are in flight.
 #include "elastic_common.h"
 #include "igemm.h"
 
@@ -35,7 +35,7 @@ template <class T, int P>
 __global__ __launch_bounds__(kWave * P) void skinny_kernel(IgemmArgs a, Shard sh) {
     typedef Mfma<T, 16> MF;
     typedef typename MF::op_t op_t;
-    constexpr int NJ = 8;              // MFMA steps per group
+    constexpr int NJ = 4;              // MFMA steps per group
     constexpr int GROUP = 32 * NJ;     // K consumed by one group
     __shared__ float part[kLogicalWaves][16][17];
 

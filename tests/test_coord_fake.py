@@ -101,6 +101,22 @@ def test_every_request_completes_once(L, policy, segments, event_us):
         co.shutdown()
 
 
+@pytest.mark.parametrize("policy", ["elastic", "sequential"])
+def test_submit_returns_the_ticket_of_its_request(L, policy):
+    # Requests that finish while submit is still returning (tiny ops, a fast simulated device,
+    # a submitting thread that can be descheduled) must still report their own ticket: the
+    # dispatcher owns and frees a request once it is queued.
+    co = _coord(policy=policy, n_be_streams=1, fake_tile_ns=1.0, fake_launch_ns=1.0, profile_reps=0)
+    try:
+        be = co.task(_net(L, [1]))
+        tickets = [co.submit(be, False) for _ in range(3000)]
+        recs = _collect(co, len(tickets), timeout=60.0)
+        assert len(set(tickets)) == len(tickets)
+        assert sorted(r.ticket for r in recs) == sorted(tickets)
+    finally:
+        co.shutdown()
+
+
 def _check_log(log, policy):
     by_req = {}
     for r in log:
