@@ -36,13 +36,14 @@ PEAK_HBM_GBS = 8000.0
 CONFIGS = {
     "corun-resnet18-vgg16-fp16": dict(
         dtype="f16", crit=("resnet18", dict(batch=1)), period_ms=20.0, arrival="periodic",
-        be=[("vgg16", dict(batch=8))]),
+        be=[("vgg16", dict(batch=8))], be_instances=3),
     "corun-encoder-mobilenetv2-bf16": dict(
         dtype="bf16", crit=("encoder", dict(batch=1, seq=128)), period_ms=10.0, arrival="periodic",
-        be=[("mobilenetv2", dict(batch=16))]),
+        be=[("mobilenetv2", dict(batch=16))], be_instances=3),
     "mix4-bf16": dict(
         dtype="bf16", crit=("resnet18", dict(batch=1)), period_ms=15.0, arrival="poisson",
-        be=[("vgg16", dict(batch=8)), ("encoder", dict(batch=4, seq=256)), ("mobilenetv2", dict(batch=32))]),
+        be=[("vgg16", dict(batch=8)), ("encoder", dict(batch=4, seq=256)), ("mobilenetv2", dict(batch=32))],
+        be_instances=1),
 }
 DEFAULT_CONFIG = "corun-resnet18-vgg16-fp16"
 
@@ -184,7 +185,8 @@ def shard_overhead(layer, reps, flush, n_cu, lib):
 
 
 # ----------------------------------------------------------------- co-run
-def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, seed, ccfg, with_be=True):
+def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, seed, ccfg, with_be=True,
+              be_inflight=2):
     import torch
     from paper_2307_04339_amd import synth
     from paper_2307_04339_amd.runtime import Coordinator
@@ -210,7 +212,7 @@ def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, se
         be_done = []   # (task index, t_end)
         be_ticket_task = {}
         for j, bt in enumerate(bts):
-            for _ in range(2):
+            for _ in range(be_inflight):
                 tk = co.submit(bt, False)
                 be_ticket_task[tk] = j
             be_out[j] = 2
@@ -375,6 +377,11 @@ def main():
                          "(0 = launch at the release); -1: 500 with the release guard, else 0")
     ap.add_argument("--segments", type=int, default=0, choices=(0, 1),
                     help="1: runs of short normal ops within one quantum go out as one captured unit")
+    ap.add_argument("--be-instances", type=int, default=0,
+                    help="instances of each best-effort network (shared weights, separate activation "
+                         "buffers), each its own closed-loop task and stream; Sequential still runs one "
+                         "request at a time.  0: the workload's default (3 for the two-task co-runs, 1 for "
+                         "the four-task mix, whose three networks already give three streams)")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
@@ -402,8 +409,14 @@ def main():
     cname, ckw = cfg["crit"]
     crit_net = models.BUILDERS[cname](dtype=dtype, **ckw)
     be_nets = [models.BUILDERS[n](dtype=dtype, **kw) for (n, kw) in cfg["be"]]
+    be_tasks = []  # every instance of every best-effort network
+    n_inst = args.be_instances if args.be_instances > 0 else cfg["be_instances"]
+    for first, (n, kw) in zip(be_nets, cfg["be"]):
+        be_tasks.append(first)
+        for _ in range(n_inst - 1):
+            be_tasks.append(models.BUILDERS[n](dtype=dtype, share=first, **kw))
     crit_net.forward()
-    for n in be_nets:
+    for n in be_tasks:
         n.forward()
     torch.cuda.synchronize()
     phases = set(args.phases.split(","))
@@ -455,7 +468,7 @@ def main():
         log(f"phase {ph} ...")
         policy = {"solo": "elastic", "elastic_pause": "elastic"}.get(ph, ph)
         pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else ccfg
-        runs[ph] = run_phase(policy, crit_net, be_nets, args.warmup, args.steps, cfg["period_ms"],
+        runs[ph] = run_phase(policy, crit_net, be_tasks, args.warmup, args.steps, cfg["period_ms"],
                              cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
         r = runs[ph]
         log(f"  p50 {r['p50_ms']:.3f} ms  p99 {r['p99_ms']:.3f} ms  be {r['be_img_s']:.1f} img/s "
@@ -482,6 +495,7 @@ def main():
         "config": {"workload": args.config,
                    "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
+                   "be_instances": n_inst,
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
                    "inflight_us": inflight_us, "event_us": round(event_us, 2), "busy_policy": args.busy_policy,
                    "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,

@@ -32,7 +32,10 @@ class Layer:
 
 
 class Net:
-    def __init__(self, name: str, dtype: str, batch: int, seed: int):
+    def __init__(self, name: str, dtype: str, batch: int, seed: int, share=None):
+        """share: a network built by the same builder with the same arguments whose read-only
+        tensors (weights, biases, BN / LN vectors, the input) this one reuses; activation
+        buffers are always its own, so the two can run requests concurrently."""
         self.name = name
         self.dtype = dtype
         self.batch = batch
@@ -41,6 +44,8 @@ class Net:
         self._n = 0
         self.input = None
         self.output = None
+        self._share = share
+        self._params: list = []
 
     # ----------------------------------------------------------- tensors
     def _dev(self, x64, dtype=None):
@@ -52,16 +57,29 @@ class Net:
             t = torch.from_numpy(np.ascontiguousarray(s))
         return t.cuda()
 
+    def _param(self, make, dtype=None):
+        """Read-only tensor: built from make() (a float64 array), or taken from the shared network."""
+        i = len(self._params)
+        if self._share is not None:
+            t = self._share._params[i]
+        else:
+            t = make() if callable(make) and not isinstance(make, np.ndarray) else make
+            t = self._dev(t, dtype) if isinstance(t, np.ndarray) else t
+        self._params.append(t)
+        return t
+
     def _u(self, shape, bound, name, dtype=None):
         sd = synth.tensor_seed(self.seed, self._n, name)
-        return self._dev(synth.uniform(shape, -bound, bound, sd), dtype)
+        return self._param(lambda: synth.uniform(shape, -bound, bound, sd), dtype)
 
     def _bn(self, C):
         sd = synth.tensor_seed(self.seed, self._n, "bn")
-        rng = np.random.default_rng(sd)
-        a = np.stack([rng.uniform(0.8, 1.2, C), rng.uniform(-0.1, 0.1, C),
-                      rng.uniform(-0.1, 0.1, C), rng.uniform(0.8, 1.2, C)])
-        return self._dev(a, "f32")
+
+        def make():
+            rng = np.random.default_rng(sd)
+            return np.stack([rng.uniform(0.8, 1.2, C), rng.uniform(-0.1, 0.1, C),
+                             rng.uniform(-0.1, 0.1, C), rng.uniform(0.8, 1.2, C)])
+        return self._param(make, "f32")
 
     def act_buf(self, shape):
         return torch.empty(shape, dtype=TORCH[self.dtype], device="cuda")
@@ -79,11 +97,14 @@ class Net:
         N, H, W, C = x.shape
         lc = logical_c or C
         fan = lc * k * k
-        w64 = synth.uniform((K, k, k, lc), -math.sqrt(6.0 / fan), math.sqrt(6.0 / fan),
-                            synth.tensor_seed(self.seed, self._n, "w"))
-        if lc != C:
-            w64 = np.concatenate([w64, np.zeros((K, k, k, C - lc))], axis=3)
-        w = self._dev(w64)
+        sd = synth.tensor_seed(self.seed, self._n, "w")
+
+        def make_w():
+            w64 = synth.uniform((K, k, k, lc), -math.sqrt(6.0 / fan), math.sqrt(6.0 / fan), sd)
+            if lc != C:
+                w64 = np.concatenate([w64, np.zeros((K, k, k, C - lc))], axis=3)
+            return w64
+        w = self._param(make_w)
         b = self._u((K,), 1.0 / math.sqrt(fan), "b", "f32") if bias else None
         bnp = self._bn(K) if bn else None
         Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
@@ -154,11 +175,11 @@ def image_input(batch, seed):
 
 
 
-def resnet18(batch=1, dtype="f16", seed=0, num_classes=1000) -> Net:
+def resnet18(batch=1, dtype="f16", seed=0, num_classes=1000, share=None) -> Net:
     """7x7/2 stem, 3x3/2 max pool, 4 stages of two 3x3 basic blocks (64/128/256/512),
     global average pool, FC 512 -> classes.  23 operators."""
-    net = Net("resnet18", dtype, batch, seed)
-    x = net._dev(image_input(batch, seed))
+    net = Net("resnet18", dtype, batch, seed, share)
+    x = net._param(lambda: image_input(batch, seed))
     net.input = x
     h = net.conv(x, 64, 7, 2, 3, name="stem", logical_c=3)
     h = net.pool(h, 3, 2, 1, "max", name="maxpool")
@@ -177,10 +198,10 @@ def resnet18(batch=1, dtype="f16", seed=0, num_classes=1000) -> Net:
     return net
 
 
-def vgg16(batch=8, dtype="f16", seed=1, num_classes=1000) -> Net:
+def vgg16(batch=8, dtype="f16", seed=1, num_classes=1000, share=None) -> Net:
     """13 3x3 convs (64..512, bias + ReLU), 5 2x2 max pools, FC 25088->4096->4096->classes."""
-    net = Net("vgg16", dtype, batch, seed)
-    x = net._dev(image_input(batch, seed))
+    net = Net("vgg16", dtype, batch, seed, share)
+    x = net._param(lambda: image_input(batch, seed))
     net.input = x
     h = x
     for si, (c, n) in enumerate([(64, 2), (128, 2), (256, 3), (512, 3), (512, 3)]):
@@ -195,11 +216,11 @@ def vgg16(batch=8, dtype="f16", seed=1, num_classes=1000) -> Net:
     return net
 
 
-def mobilenetv2(batch=16, dtype="bf16", seed=2, num_classes=1000) -> Net:
+def mobilenetv2(batch=16, dtype="bf16", seed=2, num_classes=1000, share=None) -> Net:
     """Stem 3x3/2 conv 3->32, inverted residual blocks (expansion 6, width 1.0),
     1x1 conv 320->1280, global average pool, FC 1280->classes."""
-    net = Net("mobilenetv2", dtype, batch, seed)
-    x = net._dev(image_input(batch, seed))
+    net = Net("mobilenetv2", dtype, batch, seed, share)
+    x = net._param(lambda: image_input(batch, seed))
     net.input = x
     h = net.conv(x, 32, 3, 2, 1, act="relu6", name="stem", logical_c=3)
     cin = 32
@@ -221,17 +242,17 @@ def mobilenetv2(batch=16, dtype="bf16", seed=2, num_classes=1000) -> Net:
     return net
 
 
-def encoder(batch=1, seq=128, layers=12, hidden=768, heads=12, ffn=3072, dtype="bf16", seed=3) -> Net:
+def encoder(batch=1, seq=128, layers=12, hidden=768, heads=12, ffn=3072, dtype="bf16", seed=3, share=None) -> Net:
     """Post-LN BERT-style encoder: per layer QKV projection, scores = Q K^T (per head),
     softmax(scores / sqrt(64)), context = P V, output projection + residual, LayerNorm,
     FFN (GELU) + residual, LayerNorm.  No attention mask."""
-    net = Net("encoder", dtype, batch, seed)
+    net = Net("encoder", dtype, batch, seed, share)
     M = batch * seq
     D = hidden // heads
-    x = net._dev(synth.uniform((M, hidden), -1, 1, synth.tensor_seed(seed, -1, "input")))
+    x = net._param(lambda: synth.uniform((M, hidden), -1, 1, synth.tensor_seed(seed, -1, "input")))
     net.input = x
-    ones = torch.ones(hidden, dtype=torch.float32, device="cuda")
-    zeros = torch.zeros(hidden, dtype=torch.float32, device="cuda")
+    ones = net._param(lambda: torch.ones(hidden, dtype=torch.float32, device="cuda"))
+    zeros = net._param(lambda: torch.zeros(hidden, dtype=torch.float32, device="cuda"))
     h = x
     for li in range(layers):
         bnd = 1.0 / math.sqrt(hidden)
