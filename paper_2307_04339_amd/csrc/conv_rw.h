@@ -1,24 +1,28 @@
-// Direct 3x3 / stride-1 convolution with the weights resident in registers, for
-// narrow layers (C <= 64 input channels, at most 64 output channels, fp16 / bf16).
+// Direct convolution with the weights resident in registers, for narrow layers (fp16 /
+// bf16, C <= 64 input channels): 3x3 stride 1 (at most 64 output channels), 3x3 stride 2
+// (8-channel images), and 1x1 stride 1 (any number of output channels).
 //
-// The tile is the one of the direct 3x3 kernel: 4 x 32 output pixels of one image
-// times 64 output channels (so the tile space, the shard plans and the tile map are
-// the same), split 2 x 2 over the 4 logical waves; logical wave (wm, wn) owns tile rows
-// 2wm, 2wm+1 and output channels 32wn .. 32wn+31.
+// The tile is 4 x 32 output pixels of one image times 64 output channels (for 3x3 stride 1
+// the tile of the LDS-patch kernel, so the tile space, the shard plans and the tile map
+// are the same), split 2 x 2 over the 4 logical waves; logical wave (wm, wn) owns tile
+// rows 2wm, 2wm+1 and output channels 32wn .. 32wn+31 of the tile's 64.  Tile id =
+// ((image * tY + tile row) * tX + tile column) * nT + n tile.
 //
 // With at most 64 input channels the whole filter slice of a logical wave, 32
-// channels x 9C K values, fits its registers as MFMA B operands (9C/4 VGPRs: 144 for
-// C = 64), so a workgroup loads its weights once and keeps them across every tile it
-// runs.  Only the input patch of a tile, the (4+2) x (32+2) pixels its nine taps touch,
-// streams through LDS: it is DMA'd (global_load_lds_dwordx4) into one of two buffers
-// while the previous tile computes.  A pixel occupies C/8 16-byte slots plus, for
-// C >= 16, one padding slot, so 32 consecutive pixels of a tap map to distinct bank
-// groups and every MFMA operand read is a ds_read_b128 with a compile-time offset.
+// channels x KS*KS*C K values, fits its registers as MFMA B operands (9C/4 VGPRs for
+// 3x3: 144 for C = 64), so with one n tile a workgroup loads its weights once and keeps
+// them across every tile it runs; 1x1 layers with several n tiles load the next tile's
+// (C/4 VGPRs) while the current one computes.  Only the input patch of a tile, the
+// ((4-1) ST + KS) x ((32-1) ST + KS) pixels its taps touch, streams through LDS: it is
+// DMA'd (global_load_lds_dwordx4) into one of two buffers while the previous tile
+// computes.  A pixel occupies C/8 16-byte slots, padded to an odd count, so the pixels
+// of a tap map to distinct bank groups and every MFMA operand read is a ds_read_b128 with
+// a compile-time offset.
 //
 // K order per output element (fixed, whatever the elastic configuration): MFMA step s
-// covers k = 16s .. 16s+15 with k = tap * C + c (tap = 3r + s in row-major order, c
-// fastest), the order of the [Cout][KH][KW][Cin] weight rows; when 9C is not a multiple
-// of 16 (C = 8) the last step's upper half is zero on both operands.
+// covers k = 16s .. 16s+15 with k = tap * C + c (tap = KS r + s in row-major order, c
+// fastest), the order of the [Cout][KH][KW][Cin] weight rows; when KS*KS*C is not a
+// multiple of 16 the last step's upper half is zero on both operands.
 //
 // Elastic block: a physical block of P waves runs logical wave lambda on wave
 // lambda mod P.  P = 2 runs both row halves of one channel half (same weights) at once;
@@ -31,23 +35,26 @@
 
 namespace miriam {
 
-template <class T, int C, int P>
+template <class T, int C, int P, int KS, int ST>
 struct RwKernel {
     typedef Mfma<T, 32> MF;
     static_assert(sizeof(T) == 2, "16-bit operands only");
-    static_assert(C == 8 || C == 16 || C == 32 || C == 64, "C must be 8, 16, 32 or 64");
+    static_assert(C % 8 == 0 && C >= 8 && C <= 64, "C must be a multiple of 8 up to 64");
+    // two MFMA operand halves share one tap unless one tap holds a single half (C = 8)
+    static_assert(KS == 1 || C == 8 || C % 16 == 0, "3x3 needs C = 8 or a multiple of 16");
+    static_assert((KS == 3 && (ST == 1 || ST == 2)) || (KS == 1 && ST == 1), "3x3 stride 1 or 2, 1x1 stride 1");
     static constexpr int TH = 4, TW = 32, TM = TH * TW, TN = 64;
     static constexpr int NT = kWave * P;
     static constexpr int VEC = 8;                         // 16-bit elements per 16 bytes
     static constexpr int NP = C / 8;                      // 16-byte pieces of a pixel
-    static constexpr int SP = NP == 1 ? 1 : NP + 1;       // LDS slots per pixel (odd stride)
+    static constexpr int SP = NP % 2 == 1 ? NP : NP + 1;  // LDS slots per pixel (odd stride)
     static constexpr int PS = SP * 16;                    // LDS bytes per patch pixel
-    static constexpr int PH = TH + 2, PW = TW + 2, PPIX = PH * PW;
+    static constexpr int PH = (TH - 1) * ST + KS, PW = (TW - 1) * ST + KS, PPIX = PH * PW;
     static constexpr int NSLOT = PPIX * SP;
     static constexpr int NINS = (NSLOT + kWave - 1) / kWave;  // DMA instructions per patch
     static constexpr int NJ = (NINS + P - 1) / P;             // per wave (the last may be idle)
     static constexpr int PATCH = NINS * kWave * 16;
-    static constexpr int KTOT = 9 * C;
+    static constexpr int KTOT = KS * KS * C;
     static constexpr int NS = (KTOT + 15) / 16;            // MFMA k-steps of 16
     static constexpr int LW = kLogicalWaves / P;
     static constexpr int SL = P == 4 ? 1 : 2;              // logical waves held at once
@@ -64,16 +71,16 @@ struct RwKernel {
     static_assert(TM * LDY * 2 <= CS, "staged output fits the staging area");
 };
 
-// patch pixel offset of filter tap `tap` (row-major 3x3)
-template <int PW>
+// patch pixel offset of filter tap `tap` (row-major KS x KS)
+template <int PW, int KS>
 __host__ __device__ constexpr int rw_toff(int tap) {
-    return (tap / 3) * PW + tap % 3;
+    return (tap / KS) * PW + tap % KS;
 }
 
-template <class T, int C, int P>
-__global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) void rw3x3_kernel(IgemmArgs a,
-                                                                                               Shard sh) {
-    typedef RwKernel<T, C, P> K_;
+template <class T, int C, int P, int KS, int ST>
+__global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SIMD)) void rw_conv_kernel(IgemmArgs a,
+                                                                                                     Shard sh) {
+    typedef RwKernel<T, C, P, KS, ST> K_;
     typedef typename K_::MF MF;
     typedef typename MF::op_t op_t;
     typedef typename MF::acc_t acc_t;
@@ -99,46 +106,42 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
     const int64_t end = sh.begin + sh.len;
     const int32_t H32 = (int32_t)a.H, W32 = (int32_t)a.W, Ho32 = (int32_t)a.Ho, Wo32 = (int32_t)a.Wo;
     const int32_t ldx32 = (int32_t)a.ldx;
-    const uint32_t tX32 = (uint32_t)a.tX, tY32 = (uint32_t)a.tY;
+    const uint32_t tX32 = (uint32_t)a.tX, tY32 = (uint32_t)a.tY, nT32 = (uint32_t)a.nT;
     const bool has_res = (a.epi.flags & EPI_RES) != 0;
 
     int64_t t = sh.begin + rank;
     if (t >= end) return;
 
-    // weights of channel half wn: step s holds k = 16s + 8hx .. +7 of output channel 32wn + xl
+    // weights of n tile nt, channel half wn: step s holds k = 16s + 8hx .. +7 of output
+    // channel 64 nt + 32 wn + xl
     op_t bw[NS];
-    auto load_weights = [&](int wn) {
-        const int64_t n = 32 * wn + xl;
+    auto load_weights = [&](op_t *dst, uint32_t nt, int wn) {
+        const int64_t n = 64 * (int64_t)nt + 32 * wn + xl;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int k = 16 * s + 8 * hx;
             op_t v = op_t{};
             if (n < a.Nc && k < KTOT) v = *reinterpret_cast<const op_t *>(Wt + n * a.ldw + k);
-            bw[s] = v;
+            dst[s] = v;
         }
     };
     // P = 4: logical wave pw; P = 2: channel half pw, both row halves; P = 1: both, in rounds
-    if constexpr (P != 1) load_weights(P == 4 ? (pw & 1) : pw);
+    const int wn_mine = P == 4 ? (pw & 1) : (P == 2 ? pw : 0);
 
-    // per-channel affine part of the epilogue folded into one multiply-add, v = acc * sc + sh,
-    // for this lane's channel in each round (bias, then batch norm)
-    float esc[ROUNDS], esh[ROUNDS];
-#pragma unroll
-    for (int rd = 0; rd < ROUNDS; ++rd) {
-        const int wn = P == 4 ? (pw & 1) : (P == 2 ? pw : rd);
-        const int64_t col = 32 * wn + xl;
-        chan_affine(a.epi, col < a.Nc ? col : 0, esc[rd], esh[rd]);
-    }
-
-    // tile id = (image * tY + tile row) * tX + tile column, kept as a mixed-radix cursor that
-    // advances by the grid (no division per tile)
+    // tile id = ((image * tY + tile row) * tX + tile column) * nT + n tile, kept as mixed-radix
+    // digits that advance by the grid (no division per tile)
     struct Cursor {
-        uint32_t img, ty, tx;
+        uint32_t img, ty, tx, nt;
     };
-    const uint32_t gx = (uint32_t)(G % tX32), g2 = (uint32_t)(G / tX32);
+    const uint32_t g0 = (uint32_t)G;
+    const uint32_t gn = g0 % nT32, g1 = g0 / nT32;
+    const uint32_t gx = g1 % tX32, g2 = g1 / tX32;
     const uint32_t gy = g2 % tY32, gi = g2 / tY32;
     auto advance = [&](Cursor c) {
-        c.tx += gx;
+        c.nt += gn;
+        const uint32_t cn = c.nt >= nT32 ? 1u : 0u;
+        c.nt -= cn * nT32;
+        c.tx += gx + cn;
         const uint32_t cx = c.tx >= tX32 ? 1u : 0u;
         c.tx -= cx * tX32;
         c.ty += gy + cx;
@@ -147,11 +150,23 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
         c.img += gi + cy;
         return c;
     };
+    const bool one_nt = nT32 == 1;
+    // per-channel affine part of the epilogue folded into one multiply-add, v = acc * sc + sh,
+    // for this lane's channel in each round (bias, then batch norm)
+    float esc[ROUNDS], esh[ROUNDS];
+    auto load_affine = [&](uint32_t nt) {
+#pragma unroll
+        for (int rd = 0; rd < ROUNDS; ++rd) {
+            const int wn = P == 1 ? rd : wn_mine;
+            const int64_t col = 64 * (int64_t)nt + 32 * wn + xl;
+            chan_affine(a.epi, col < a.Nc ? col : 0, esc[rd], esh[rd]);
+        }
+    };
 
     // DMA of the patch of tile `c` into buffer `buf`: instruction j writes slots 64j .. 64j+63
     auto issue_patch = [&](Cursor c, int buf) {
         const uint32_t tx = c.tx, ty = c.ty, img = c.img;
-        const int32_t iy0 = (int32_t)ty * K_::TH - a.pad, ix0 = (int32_t)tx * TW - a.pad;
+        const int32_t iy0 = (int32_t)ty * K_::TH * ST - a.pad, ix0 = (int32_t)tx * TW * ST - a.pad;
         const T *xb = X + (int64_t)img * a.img_x;
         const uint32_t base = lds0 + (uint32_t)(buf * BUF);
         // the lane index passes through an empty asm so this lane's slot decode is recomputed
@@ -176,9 +191,14 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
 
     Cursor cu;
     {
-        const uint32_t t32 = (uint32_t)t, r2 = t32 / tX32;
-        cu = Cursor{r2 / tY32, r2 % tY32, t32 % tX32};
+        const uint32_t t32 = (uint32_t)t, r1 = t32 / nT32, r2 = r1 / tX32;
+        cu = Cursor{r2 / tY32, r2 % tY32, r1 % tX32, t32 % nT32};
     }
+    // one n tile: weights and per-channel constants once for the workgroup's lifetime;
+    // several (1x1 only): for each tile, the next tile's weights load with its patch
+    op_t bw_next[KS == 1 ? NS : 1];
+    if constexpr (P != 1) load_weights(bw, cu.nt, wn_mine);
+    load_affine(cu.nt);
     issue_patch(cu, 0);
     int iter = 0;
     for (; t < end; t += G, ++iter) {
@@ -189,9 +209,23 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
         wait_vmcnt<0>();
         __syncthreads();
         const Cursor nx = advance(cu);
-        if (t + G < end) issue_patch(nx, cur ^ 1);
+        if constexpr (KS == 1 && P != 1) {
+            if (!one_nt && iter > 0) {
+                // the weights loaded with this tile's patch (complete: waited above)
+#pragma unroll
+                for (int s = 0; s < NS; ++s) bw[s] = bw_next[s];
+                load_affine(cu.nt);
+            }
+        }
+        if (t + G < end) {
+            issue_patch(nx, cur ^ 1);
+            if constexpr (KS == 1 && P != 1)
+                if (!one_nt) load_weights(bw_next, nx.nt, wn_mine);
+        }
 
-        const uint32_t tx = cu.tx, ty = cu.ty, img = cu.img;
+        const uint32_t tx = cu.tx, ty = cu.ty, img = cu.img, ntile = cu.nt;
+        if constexpr (P == 1)
+            if (!one_nt && iter > 0) load_affine(ntile);
         cu = nx;
         const int32_t oy0 = (int32_t)ty * K_::TH, ox0 = (int32_t)tx * TW;
         const char *patch = smem_ + cur * BUF;
@@ -202,8 +236,8 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
 #pragma unroll
         for (int rd = 0; rd < ROUNDS; ++rd) {
             acc_t acc[SL][2];
-            const int wn = P == 4 ? (pw & 1) : (P == 2 ? pw : rd);
-            if constexpr (P == 1) load_weights(wn);
+            const int wn = P == 1 ? rd : wn_mine;
+            if constexpr (P == 1) load_weights(bw, ntile, wn);
             // operand base of block i of slot sl: patch pixel (tile row y, column xl) + this lane's half
             const char *abase[SL][2];
 #pragma unroll
@@ -212,12 +246,10 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int y = 2 * wm + i;
-                    abase[sl][i] = patch + (y * PW + xl) * PS + (NP == 1 ? 0 : hx * 16);
+                    abase[sl][i] = patch + (y * ST * PW + xl * ST) * PS + (NP == 1 ? 0 : hx * 16);
                 }
             }
-            // C = 8: the two operand halves take taps 2s and 2s+1; the upper one is offset by
-            // (toff(2s+1) - toff(2s)) pixels, which is 1 or PW - 2
-            const int hoff1 = hx * PS, hoffw = hx * (PW - 2) * PS;
+            // one 8-channel tap per operand half (C = 8, 3x3): halves take taps 2s and 2s+1
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 op_t av[SL][2];
@@ -225,18 +257,20 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
                 for (int sl = 0; sl < SL; ++sl)
 #pragma unroll
                     for (int i = 0; i < 2; ++i) {
-                        if constexpr (NP == 1) {
+                        if constexpr (NP == 1 && KS == 3) {
                             const int t0 = 2 * s, t1 = 2 * s + 1;
-                            const int off0 = rw_toff<PW>(t0) * PS;
-                            const bool wide = t1 < 9 && (rw_toff<PW>(t1) - rw_toff<PW>(t0)) != 1;
-                            const char *p = abase[sl][i] + off0 + (wide ? hoffw : hoff1);
-                            op_t v = *reinterpret_cast<const op_t *>(p);
+                            const int off0 = rw_toff<PW, KS>(t0) * PS;
+                            const int d1 = t1 < 9 ? (rw_toff<PW, KS>(t1) - rw_toff<PW, KS>(t0)) * PS : PS;
+                            op_t v = *reinterpret_cast<const op_t *>(abase[sl][i] + off0 + hx * d1);
                             if (16 * s + 8 * hx >= KTOT) v = op_t{};
                             av[sl][i] = v;
                         } else {
-                            const int k0 = 16 * s, tap = k0 / C, c0 = k0 % C;
-                            const int off = rw_toff<PW>(tap) * PS + (c0 / 8) * 16;
-                            av[sl][i] = *reinterpret_cast<const op_t *>(abase[sl][i] + off);
+                            // both halves in one tap (channels c0 .. c0 + 15); 1x1: the one tap
+                            const int k0 = 16 * s, tap = KS == 1 ? 0 : k0 / C, c0 = KS == 1 ? k0 : k0 % C;
+                            const int off = rw_toff<PW, KS>(tap) * PS + (c0 / 8) * 16;
+                            op_t v = *reinterpret_cast<const op_t *>(abase[sl][i] + off);
+                            if (KTOT % 16 != 0 && 16 * s + 8 * hx >= KTOT) v = op_t{};
+                            av[sl][i] = v;
                         }
                     }
 #pragma unroll
@@ -293,7 +327,7 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
             for (int idx = tid; idx < TM * RV; idx += NT) {
                 const int row = idx / RV, cv = idx - (idx / RV) * RV;
                 const int32_t oy = oy0 + row / TW, ox = ox0 + row % TW;
-                const int64_t n = (int64_t)cv * VEC;
+                const int64_t n = 64 * (int64_t)ntile + (int64_t)cv * VEC;
                 if (oy >= Ho32 || ox >= Wo32 || n >= a.Nc) continue;
                 const int64_t off = (((int64_t)img * a.Ho + oy) * a.Wo + ox) * a.ldy + n;
                 const float *cr = Cs + row * LDC + cv * VEC;
@@ -318,7 +352,7 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
         for (int idx = tid; idx < TM * RV; idx += NT) {
             const int row = idx / RV, cv = idx - (idx / RV) * RV;
             const int32_t oy = oy0 + row / TW, ox = ox0 + row % TW;
-            const int64_t n = (int64_t)cv * VEC;
+            const int64_t n = 64 * (int64_t)ntile + (int64_t)cv * VEC;
             if (oy >= Ho32 || ox >= Wo32 || n >= a.Nc) continue;
             const int64_t off = (((int64_t)img * a.Ho + oy) * a.Wo + ox) * a.ldy + n;
             Vec16<T> o;
@@ -336,24 +370,42 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P>::WAVES_PER_SIMD)) voi
     }
 }
 
-template <class T, int C>
+template <class T, int C, int KS, int ST>
 inline void rw_table(const void *out[3], int *lds) {
-    out[0] = reinterpret_cast<const void *>(&rw3x3_kernel<T, C, 1>);
-    out[1] = reinterpret_cast<const void *>(&rw3x3_kernel<T, C, 2>);
-    out[2] = reinterpret_cast<const void *>(&rw3x3_kernel<T, C, 4>);
-    *lds = RwKernel<T, C, 4>::LDS_BYTES;
+    out[0] = reinterpret_cast<const void *>(&rw_conv_kernel<T, C, 1, KS, ST>);
+    out[1] = reinterpret_cast<const void *>(&rw_conv_kernel<T, C, 2, KS, ST>);
+    out[2] = reinterpret_cast<const void *>(&rw_conv_kernel<T, C, 4, KS, ST>);
+    *lds = RwKernel<T, C, 4, KS, ST>::LDS_BYTES;
 }
 
-// Kernel table of the resident-weight kernel for C input channels; -1 if C is not served.
+// Kernel table of the resident-weight kernel for a (kernel size, stride, C) it serves:
+// 3x3 stride 1 with C in {8, 16, 32, 64}, 3x3 stride 2 with C = 8, 1x1 with C in
+// {16, 24, 32, 64}; -1 otherwise.
 template <class T>
-inline int rw_table_c(int64_t c, const void *out[3], int *lds) {
-    switch (c) {
-    case 8: rw_table<T, 8>(out, lds); return 0;
-    case 16: rw_table<T, 16>(out, lds); return 0;
-    case 32: rw_table<T, 32>(out, lds); return 0;
-    case 64: rw_table<T, 64>(out, lds); return 0;
-    default: return -1;
+inline int rw_table_c(int64_t ks, int64_t st, int64_t c, const void *out[3], int *lds) {
+    if (ks == 3 && st == 1) {
+        switch (c) {
+        case 8: rw_table<T, 8, 3, 1>(out, lds); return 0;
+        case 16: rw_table<T, 16, 3, 1>(out, lds); return 0;
+        case 32: rw_table<T, 32, 3, 1>(out, lds); return 0;
+        case 64: rw_table<T, 64, 3, 1>(out, lds); return 0;
+        default: return -1;
+        }
     }
+    if (ks == 3 && st == 2 && c == 8) {
+        rw_table<T, 8, 3, 2>(out, lds);
+        return 0;
+    }
+    if (ks == 1 && st == 1) {
+        switch (c) {
+        case 16: rw_table<T, 16, 1, 1>(out, lds); return 0;
+        case 24: rw_table<T, 24, 1, 1>(out, lds); return 0;
+        case 32: rw_table<T, 32, 1, 1>(out, lds); return 0;
+        case 64: rw_table<T, 64, 1, 1>(out, lds); return 0;
+        default: return -1;
+        }
+    }
+    return -1;
 }
 
 }  // namespace miriam

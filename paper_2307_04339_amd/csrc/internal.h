@@ -24,7 +24,9 @@ int igemm_kernels_bf16(int cfg, int lay, const void *out[3], int *lds);
 int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int skinny_kernels(int dtype, const void *out[3]);
-int rw_kernels(int dtype, int64_t c, const void *out[3], int *lds);  // resident-weight direct 3x3
+// resident-weight direct convolution: (3x3, stride 1, C in {8,16,32,64}), (3x3, stride 2, C = 8),
+// (1x1, stride 1, C in {16,24,32,64})
+int rw_kernels(int dtype, int64_t ks, int64_t stride, int64_t c, const void *out[3], int *lds);
 
 }  // namespace miriam
 

@@ -87,6 +87,7 @@ struct PixArgs {
     int64_t N, H, W, C, Ho, Wo;
     int32_t KH, KW, stride, pad;
     int64_t items;     // lane items: N*Ho*Wo*(C/V)
+    FastDiv fd_cv, fd_howo, fd_wo;  // division by C/V, Ho*Wo and Wo (item -> pixel -> image, row, column)
     Epilogue epi;
 };
 

@@ -44,7 +44,7 @@ __device__ __forceinline__ void chan_params_vec(const Epilogue &e, int64_t c0, C
                 p[4 * q + i] = ChanParams{0.0f, 0.0f, 1.0f, 0.0f};
                 if (e.flags & EPI_BIAS) p[4 * q + i].bias = b[i];
                 if (e.flags & EPI_BN) {
-                    p[4 * q + i].scale = g[i] / sqrtf(var[i] + e.eps);
+                    p[4 * q + i].scale = g[i] * __builtin_amdgcn_rsqf(var[i] + e.eps);
                     p[4 * q + i].mean = mu[i];
                     p[4 * q + i].beta = be[i];
                 }
@@ -72,14 +72,14 @@ __device__ __forceinline__ void ld_items(const T *p, T (&v)[V]) {
 // Window taps are visited in row-major order (r, then s); padding taps are skipped.  The
 // taps go in batches of 9 whose loads are all issued before any is used, so a 3x3 window
 // costs one round of load latency, not nine.
-template <class T, int V, int KIND>
+template <class T, int V, int KIND, int ACT>
 __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
     const T *__restrict__ X = static_cast<const T *>(a.x);
     T *__restrict__ Y = static_cast<T *>(a.y);
     const T *const zsrc = reinterpret_cast<const T *>(g_pix_zero);
-    // item indices stay below 2^31 (checked at creation): 32-bit division
+    // item indices stay below 2^31 (checked at creation): division by precomputed constants
     const uint32_t CV = (uint32_t)(a.C / V), u32 = (uint32_t)u;
-    const uint32_t pixu = u32 / CV;
+    const uint32_t pixu = fdiv(u32, a.fd_cv);
     const int64_t pix = pixu;
     const int64_t c0 = (int64_t)(u32 - pixu * CV) * V;
     float acc[V];
@@ -92,14 +92,16 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
         chan_params_vec<V>(a.epi, c0, cp);
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            const float r = (a.epi.flags & EPI_RES) ? TypeOps<T>::to_f(rv[e]) : 0.0f;
-            acc[e] = epilogue_post(a.epi, epilogue_pre(a.epi, cp[e], TypeOps<T>::to_f(xv[e])), r);
+            float v = epilogue_pre(a.epi, cp[e], TypeOps<T>::to_f(xv[e]));
+            if (a.epi.flags & EPI_RES) v += TypeOps<T>::to_f(rv[e]);
+            acc[e] = act_c<ACT>(v);
         }
     } else {
         const uint32_t HoWo = (uint32_t)(a.Ho * a.Wo), Wo = (uint32_t)a.Wo;
-        const uint32_t n = pixu / HoWo;
+        const uint32_t n = fdiv(pixu, a.fd_howo);
         const uint32_t pq = pixu - n * HoWo;
-        const int32_t p = (int32_t)(pq / Wo), q = (int32_t)(pq - (pq / Wo) * Wo);
+        const uint32_t pu = fdiv(pq, a.fd_wo);
+        const int32_t p = (int32_t)pu, q = (int32_t)(pq - pu * Wo);
         const int32_t h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
         const int32_t H32 = (int32_t)a.H, W32 = (int32_t)a.W;
         const int taps = a.KH * a.KW;
@@ -155,8 +157,9 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
             chan_params_vec<V>(a.epi, c0, cp);
 #pragma unroll
             for (int e = 0; e < V; ++e) {
-                const float rr = (a.epi.flags & EPI_RES) ? TypeOps<T>::to_f(rv[e]) : 0.0f;
-                acc[e] = epilogue_post(a.epi, epilogue_pre(a.epi, cp[e], acc[e]), rr);
+                float v = epilogue_pre(a.epi, cp[e], acc[e]);
+                if (a.epi.flags & EPI_RES) v += TypeOps<T>::to_f(rv[e]);
+                acc[e] = act_c<ACT>(v);
             }
         }
     }
@@ -178,16 +181,20 @@ __global__ __launch_bounds__(kWave * P) void pix_kernel(PixArgs a, Shard sh) {
     const int lane = threadIdx.x % kWave;
     const int64_t G = gridDim.x;
     const int64_t rank = wg_rank(blockIdx.x, G);
-    int iter = 0;
-    for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
-        trace_tile(sh, t, iter);
+    // the activation is dispatched once for the launch, not per element
+    with_act(a.epi.act, [&](auto actc) {
+        constexpr int ACT = decltype(actc)::value;
+        int iter = 0;
+        for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
+            trace_tile(sh, t, iter);
 #pragma unroll
-        for (int s = 0; s < kLogicalWaves / P; ++s) {
-            const int lam = s * P + pw;
-            const int64_t u = t * kLogicalBlock + lam * kWave + lane;
-            if (u < a.items) pix_item<T, V, KIND>(a, u);
+            for (int s = 0; s < kLogicalWaves / P; ++s) {
+                const int lam = s * P + pw;
+                const int64_t u = t * kLogicalBlock + lam * kWave + lane;
+                if (u < a.items) pix_item<T, V, KIND, ACT>(a, u);
+            }
         }
-    }
+    });
 }
 
 // ------------------------------------------------------------------- rows

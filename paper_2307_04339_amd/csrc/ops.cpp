@@ -200,31 +200,39 @@ static int create_igemm(miriam_op *op) {
                          d.c % kt == 0 && d.ksplit <= 1;
     const int64_t halo_tx = cdiv(a.Wo, 32), halo_ty = cdiv(a.Ho, 4);
     const int64_t halo_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
-    // same tile with the weights resident in registers: fp16/bf16, C in {8, 16, 32, 64} (a
-    // workgroup's filter slice fits its registers), at most 64 output channels.  Chosen over
-    // the LDS-patch kernel and the implicit GEMM wherever it applies with 1.5 tiles per CU.
-    const bool rw_ok = d.kind == MIRIAM_OP_CONV2D && d.dtype != MIRIAM_F32 && d.kh == 3 && d.kw == 3 &&
-                       d.stride == 1 && a_vec && b_vec && (d.c == 8 || d.c == 16 || d.c == 32 || d.c == 64) &&
-                       a.Nc <= 64 && d.ksplit <= 1;
+    // 4x32-pixel x 64-channel tiles with the weights resident in registers (fp16/bf16, a
+    // workgroup's filter slice fits its registers): 3x3 stride 1 with C in {8, 16, 32, 64} and
+    // at most 64 output channels, 3x3 stride 2 on 8-channel images, 1x1 stride 1 with C in
+    // {16, 24, 32, 64} and any number of output channels.  Chosen over the LDS-patch kernel
+    // and the implicit GEMM wherever it applies with 1.5 tiles per CU.
+    const bool rw_shape = (d.kh == 3 && d.kw == 3 && d.stride == 1 && (d.c == 8 || d.c == 16 || d.c == 32 || d.c == 64) &&
+                           a.Nc <= 64) ||
+                          (d.kh == 3 && d.kw == 3 && d.stride == 2 && d.c == 8 && a.Nc <= 64) ||
+                          (d.kh == 1 && d.kw == 1 && d.stride == 1 && d.pad == 0 &&
+                           (d.c == 16 || d.c == 24 || d.c == 32 || d.c == 64));
+    const bool rw_ok = d.kind == MIRIAM_OP_CONV2D && d.dtype != MIRIAM_F32 && rw_shape && a_vec && b_vec &&
+                       d.ksplit <= 1 && a.img_x < (int64_t)INT32_MAX;
+    const int64_t rw_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
     int cfg = d.tile;
-    if (cfg == 0 && rw_ok && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5) cfg = CFG_RW;
+    if (cfg == 0 && rw_ok && rw_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5) cfg = CFG_RW;
     if (cfg == 0 && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5)
         cfg = CFG_HALO;
     if (cfg == 0) cfg = skinny_ok ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
     if (cfg == CFG_RW) {
-        if (!rw_ok) return einval("tile 8 (resident-weight direct 3x3) needs an fp16/bf16 3x3 stride-1 conv with C in {8,16,32,64}, at most 64 output channels, 16-byte rows and no split K");
+        if (!rw_ok) return einval("tile 8 (resident-weight direct conv) needs an fp16/bf16 conv that is 3x3 stride 1 with C in {8,16,32,64} and at most 64 output channels, 3x3 stride 2 with C = 8 and at most 64 output channels, or 1x1 stride 1 pad 0 with C in {16,24,32,64}; 16-byte rows; no split K");
         a.tX = halo_tx;
         a.tY = halo_ty;
         a.mT = halo_ty * halo_tx;
-        a.nT = 1;
+        a.nT = cdiv(a.Nc, 64);
         a.ksplit = 1;
         a.cps = 1;
-        op->T = d.n * a.mT;
+        op->T = d.n * a.mT * a.nT;
         op->cfg = cfg;
         op->tile_m = 128;
         op->tile_n = 64;
         op->lay = LAY_RW;
-        if (rw_kernels(d.dtype, d.c, op->kern, &op->lds_bytes) != 0) return einval("no resident-weight kernel for this dtype / C");
+        if (rw_kernels(d.dtype, d.kh, d.stride, d.c, op->kern, &op->lds_bytes) != 0)
+            return einval("no resident-weight kernel for this dtype / shape");
     } else if (cfg == CFG_HALO) {
         if (!halo_ok) return einval("tile 7 (direct 3x3) needs a 3x3 stride-1 conv with C a multiple of the 128-byte chunk, 16-byte rows and no split K");
         a.tX = halo_tx;
@@ -380,6 +388,9 @@ static int create_pix(miriam_op *op) {
     a.epi = make_epi(d, a.C);
     a.items = a.N * a.Ho * a.Wo * (a.C / v);
     if (a.items >= (int64_t)INT32_MAX) return einval("pixel op too large for 32-bit item indexing");
+    a.fd_cv = make_fastdiv((uint32_t)(a.C / v));
+    a.fd_howo = make_fastdiv((uint32_t)(a.Ho * a.Wo));
+    a.fd_wo = make_fastdiv((uint32_t)a.Wo);
     op->T = cdiv(a.items, 256);
     op->lds_bytes = 0;
     if (pix_kernels(d.dtype, kind, vec, op->kern) != 0) return einval("no kernel for this dtype");

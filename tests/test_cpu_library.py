@@ -194,6 +194,11 @@ def test_gemm_tile_space(lib, M, N, K, tile, T):
     ("conv", "BF16", dict(n=8, h=112, w=112, c=64, k=128), FAKE, "PATH_DMA_UNIFORM"),  # wider: implicit GEMM
     ("conv", "F16", dict(c=64, tile=8), FAKE, "PATH_RESIDENT"),  # resident weights on request
     ("conv", "BF16", dict(c=8, k=20, tile=8), FAKE, "PATH_RESIDENT"),
+    ("conv", "BF16", dict(n=16, h=224, w=224, c=8, k=32, stride=2), FAKE, "PATH_RESIDENT"),  # stem 3x3/2
+    ("conv", "BF16", dict(n=16, h=112, w=112, c=16, k=96, kh=1, kw=1, pad=0), FAKE, "PATH_RESIDENT"),  # 1x1
+    ("conv", "F16", dict(n=16, h=56, w=56, c=24, k=144, kh=1, kw=1, pad=0), FAKE, "PATH_RESIDENT"),
+    ("conv", "BF16", dict(n=16, h=56, w=56, c=96, k=24, kh=1, kw=1, pad=0), FAKE, "PATH_DMA"),  # C too wide
+    ("conv", "F16", dict(c=24, k=200, kh=1, kw=1, pad=0, tile=8), FAKE, "PATH_RESIDENT"),
 ])
 def test_kernel_path_selection(lib, kind, dtype, geo, addr, path):
     from paper_2307_04339_amd import _lib as L
@@ -224,7 +229,9 @@ def test_direct3x3_rejects_ineligible_convs(lib, geo):
 
 
 @pytest.mark.parametrize("geo", [dict(c=24), dict(c=128), dict(c=64, k=96), dict(c=64, stride=2),
-                                 dict(c=64, kh=5, kw=5, pad=2), dict(c=64, ksplit=2), dict(c=64, dtype=0)])
+                                 dict(c=64, kh=5, kw=5, pad=2), dict(c=64, ksplit=2), dict(c=64, dtype=0),
+                                 dict(c=16, stride=2), dict(c=8, k=96, stride=2), dict(c=8, kh=1, kw=1, pad=0),
+                                 dict(c=16, kh=1, kw=1, pad=1), dict(c=16, kh=1, kw=1, pad=0, stride=2)])
 def test_resident3x3_rejects_ineligible_convs(lib, geo):
     from paper_2307_04339_amd import _lib as L
     d = dict(kind=L.OP_CONV2D, dtype=L.F16, n=1, h=9, w=9, c=16, k=32, kh=3, kw=3, stride=1, pad=1,

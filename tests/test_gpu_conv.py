@@ -326,6 +326,68 @@ def test_conv_resident3x3_matches_oracle_and_is_elastic(ops, orc, dtype, case):
             assert bits(y) == ref_bits, (n, block)
 
 
+# 1x1 and 3x3 stride-2 shapes of the resident-weight kernel (N, H, W, C, K, ks, stride, pad, act, epi)
+RW_SHAPES = [
+    (2, 23, 70, 8, 32, 3, 2, 1, "relu6", "bn"),      # image stem: 3x3 / 2 on 8 channels, ragged
+    (1, 16, 33, 8, 64, 3, 2, 1, "relu", "bias"),     # even input size, full 64 channels
+    (2, 9, 40, 16, 96, 1, 1, 0, "relu6", "bn"),      # 1x1 expand, two n tiles (96 = 64 + 32)
+    (1, 12, 37, 24, 144, 1, 1, 0, "relu6", "bn"),    # 1x1, C = 24 (half-masked last step), 3 n tiles
+    (3, 7, 33, 32, 16, 1, 1, 0, "none", "bn_res"),   # 1x1 project with residual, one n tile
+    (1, 10, 20, 64, 200, 1, 1, 0, "gelu", "bias"),   # 1x1, 4 n tiles, ragged last one
+]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("case", RW_SHAPES)
+def test_conv_resident_shapes_match_oracle_and_are_elastic(ops, orc, dtype, case):
+    from paper_2307_04339_amd import _lib as L
+    N, H, W, C, K, ks, st, p, act, epi = case
+    seed = abs(hash(case)) % 1000
+    x, x64 = rand((N, H, W, C), dtype, seed=seed)
+    w, w64 = rand((K, ks, ks, C), dtype, seed=seed + 1, lo=-0.2, hi=0.2)
+    Ho, Wo = (H + 2 * p - ks) // st + 1, (W + 2 * p - ks) // st + 1
+    rng = np.random.default_rng(seed + 2)
+    bias = bn = res = None
+    b64 = bn64 = r64 = None
+    if "bias" in epi:
+        b64 = rng.uniform(-1, 1, K).astype(np.float32).astype(np.float64)
+        bias = f32_dev(b64)
+    if "bn" in epi:
+        bn64 = np.stack([rng.uniform(0.8, 1.2, K), rng.uniform(-0.1, 0.1, K), rng.uniform(-0.1, 0.1, K),
+                         rng.uniform(0.8, 1.2, K)]).astype(np.float32).astype(np.float64)
+        bn = f32_dev(bn64)
+    if "res" in epi:
+        res, r64 = rand((N, Ho, Wo, K), dtype, seed=seed + 3)
+    y = empty((N, Ho, Wo, K), dtype)
+    op = ops.conv2d(x, w, y, stride=st, pad=p, bias=bias, bn=bn, residual=res, act=act, tile=8)
+    assert op.info.path == L.PATH_RESIDENT
+    assert op.T == N * ((Ho + 3) // 4) * ((Wo + 31) // 32) * ((K + 63) // 64)
+    op.launch(0, op.T, op.T, 256)
+    torch.cuda.synchronize()
+    ref = orc.conv2d(x64, w64, stride=st, pad=p, bias=b64, bn=None if bn64 is None else tuple(bn64),
+                     residual=r64, act=act)
+    err = rel_err(to_f64(y), ref)
+    print(f"resident {ks}x{ks}/{st} {dtype} {case}: T={op.T} rel={err:.3e}")
+    assert err <= RTOL[dtype], err
+    ref_bits = bits(y)
+    y.fill_(float("nan"))
+    op.run()
+    torch.cuda.synchronize()
+    assert bits(y) == ref_bits
+    rng = np.random.default_rng(9)
+    for n in [1, 2, 5]:
+        if n > op.T:
+            continue
+        for block in [64, 128, 256]:
+            y.fill_(float("nan"))
+            plan = orc.balanced_split(op.T, n)
+            for j in rng.permutation(n):
+                b, l = plan[j]
+                op.launch(b, l, int(rng.choice([1, 3, 7, l])), block)
+            torch.cuda.synchronize()
+            assert bits(y) == ref_bits, (n, block)
+
+
 @pytest.mark.parametrize("C", [8, 64])
 def test_conv_resident3x3_integer_inputs_exact(ops, orc, C):
     # integer operands in {-1, 0, 1}: |partial sums| <= 9 C <= 576, exact in fp32 and fp16
