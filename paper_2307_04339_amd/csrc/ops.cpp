@@ -297,13 +297,17 @@ static int create_igemm(miriam_op *op) {
         a.ksplit = 1;
         a.cps = (int32_t)cdiv(a.K, d.dtype == MIRIAM_F32 ? 32 : 64);  // K chunks of one 128-byte row
         // split K over workgroups with a fixed-order reduction (pipelined kernel only) when
-        // the caller asks for it
-        // (the library choice is no split: on the pipelined kernel a split measured slower
-        // than or equal to the unsplit launch on every CNN layer with few output tiles)
+        // the caller asks for it, or by the library's choice for ops with at most a quarter of
+        // a tile per CU and at least 32 K chunks (a slice keeps 16 or more): ResNet-18 b1
+        // layer 4 as a 49 x 512 x 4608 product 21.0 -> 14.3 us with 4 slices; ops with more
+        // tiles measured slower split (encoder b1 QKV 9.9 -> 14.3 us with 2)
         const int64_t nch = a.cps;
         const bool vec_layout = (a_vec && b_vec && !nmaj);
-        if (d.ksplit > 1 && vec_layout) {
-            int64_t ks = std::min<int64_t>(d.ksplit, nch);
+        int64_t want_ks = d.ksplit;
+        if (d.ksplit == 0 && vec_layout && op->T * 4 <= (int64_t)device_cus() && nch >= 32)
+            want_ks = std::min<int64_t>(4, nch / 16);
+        if (want_ks > 1 && vec_layout) {
+            int64_t ks = std::min<int64_t>(want_ks, nch);
             if (ks > 1) {
                 const int64_t cps = cdiv(nch, ks);
                 ks = cdiv(nch, cps);  // no empty slices

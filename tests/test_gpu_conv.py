@@ -176,8 +176,9 @@ def test_conv_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, case):
     y = empty((N, Ho, Wo, K), dtype)
     op = ops.conv2d(x, w, y, stride=s, pad=p, bn=f32_dev(bn64), residual=res, act="relu", ksplit=ks)
     if ks == 0:
-        # library choice: 1 x 7 x 7 x 512 output at 32x32 tiles, not split
-        assert op.T == 32 and op.info.ksplit == 1
+        # library choice: 1 x 7 x 7 x 512 output at 32x32 tiles is 32 output tiles (under a
+        # quarter of a tile per CU) over 72 (fp16) or 144 (fp32) K chunks: 4 slices
+        assert op.info.ksplit == 4 and op.T == 32 * 4
     else:
         assert op.info.ksplit == ks
         assert op.T % ks == 0
