@@ -497,7 +497,8 @@ def main():
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "be_instances": n_inst,
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
-                   "inflight_us": inflight_us, "event_us": round(event_us, 2), "busy_policy": args.busy_policy,
+                   "inflight_us": inflight_us, "event_us": round(event_us, 2),
+                   "busy_policy": 1 if main_name == "elastic_pause" else args.busy_policy,
                    "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
                    "arm_lead_us": arm, "segments": args.segments},
     }
