@@ -382,7 +382,7 @@ def main():
                          "buffers), each its own closed-loop task and stream; Sequential still runs one "
                          "request at a time.  0: the workload's default (3 for the two-task co-runs, 1 for "
                          "the four-task mix, whose three networks already give three streams)")
-    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,elastic,elastic_pause")
+    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,ib,elastic,elastic_pause")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
                     help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
@@ -462,7 +462,7 @@ def main():
                 busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
                 warm_critical=warm, arm_lead_us=arm, segments=args.segments)
     runs = {}
-    for ph in ("solo", "sequential", "multistream", "elastic", "elastic_pause"):
+    for ph in ("solo", "sequential", "multistream", "ib", "elastic", "elastic_pause"):
         if ph not in phases:
             continue
         log(f"phase {ph} ...")
@@ -509,7 +509,7 @@ def main():
             "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
             "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
             "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
-        for other in ("elastic", "multistream", "sequential"):
+        for other in ("elastic", "multistream", "ib", "sequential"):
             if other in runs and other != main_name:
                 out["critical"][f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
     for ph, r in runs.items():

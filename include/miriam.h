@@ -241,7 +241,10 @@ int64_t miriam_plan_tree_head(int64_t T, int64_t cursor, int64_t max_len, int *d
 typedef enum {
     MIRIAM_POLICY_ELASTIC = 0,     /* Miriam: critical unsharded, normal as elastic shards */
     MIRIAM_POLICY_SEQUENTIAL = 1,  /* one request at a time, critical first (baseline) */
-    MIRIAM_POLICY_MULTISTREAM = 2  /* every task on its own stream, full kernels (baseline) */
+    MIRIAM_POLICY_MULTISTREAM = 2, /* every task on its own stream, full kernels (baseline) */
+    MIRIAM_POLICY_IB = 3           /* inter-stream barrier (baseline, §8.1.3): the tasks' full kernels
+                                      advance in groups of one kernel per task, each stream waiting
+                                      on the device for the previous group's kernels */
 } miriam_policy;
 
 typedef enum { MIRIAM_BACKEND_HIP = 0, MIRIAM_BACKEND_FAKE = 1 } miriam_backend;
@@ -326,6 +329,7 @@ typedef struct miriam_stats {
     int64_t warm_launches;    /* cache-warming kernels queued ahead of critical releases */
     int64_t armed_releases;   /* critical requests queued behind a gate ahead of their release */
     int64_t segment_launches; /* runs of short normal ops issued as one captured unit */
+    int64_t barrier_groups;   /* IB: kernel groups issued behind an inter-stream barrier */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */

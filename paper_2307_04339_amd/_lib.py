@@ -23,7 +23,7 @@ DTYPE_CODE = {"f32": F32, "f16": F16, "bf16": BF16}
 ACT_NONE, ACT_RELU, ACT_RELU6, ACT_GELU = 0, 1, 2, 3
 ACT_CODE = {"none": 0, "relu": 1, "relu6": 2, "gelu": 3}
 EPI_BIAS, EPI_BN, EPI_RESIDUAL = 1, 2, 4
-POLICY_ELASTIC, POLICY_SEQUENTIAL, POLICY_MULTISTREAM = 0, 1, 2
+POLICY_ELASTIC, POLICY_SEQUENTIAL, POLICY_MULTISTREAM, POLICY_IB = 0, 1, 2, 3
 BACKEND_HIP, BACKEND_FAKE = 0, 1
 
 
@@ -109,6 +109,7 @@ class Stats(ctypes.Structure):
         ("decision_ns_total", ctypes.c_double), ("completed", ctypes.c_int64),
         ("graph_launches", ctypes.c_int64), ("warm_launches", ctypes.c_int64),
         ("armed_releases", ctypes.c_int64), ("segment_launches", ctypes.c_int64),
+        ("barrier_groups", ctypes.c_int64),
     ]
 
 

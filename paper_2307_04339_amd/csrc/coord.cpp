@@ -14,7 +14,9 @@
 //
 // Baseline policies for comparison (§8.1.3): SEQUENTIAL runs one request at a
 // time on one stream, critical first; MULTISTREAM launches every request's
-// kernels unsharded on its task's stream.
+// kernels unsharded on its task's stream; IB (inter-stream barrier) advances the
+// tasks' unsharded kernels in lockstep groups, one kernel per task and stream,
+// each stream waiting on the device for the previous group's kernels.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -77,6 +79,11 @@ struct Backend {
         return MIRIAM_ESTATE;
     }
     virtual void open_gates(uint64_t seq) { (void)seq; }
+    // Make later work on `stream` wait, on the device, for recorded event `ev`.
+    virtual int wait_event(int stream, int ev) {
+        (void)stream; (void)ev;
+        return MIRIAM_ESTATE;
+    }
     virtual void stop() = 0;
 };
 
@@ -197,6 +204,10 @@ struct HipBackend : Backend {
             return hip_fail(e, "hipEventRecord");
         }
         return id;
+    }
+    int wait_event(int stream, int ev) override {
+        hipError_t e = hipStreamWaitEvent(streams[stream], events[ev], 0);
+        return e == hipSuccess ? MIRIAM_OK : hip_fail(e, "hipStreamWaitEvent");
     }
     int query(int ev) override {
         hipError_t e = hipEventQuery(events[ev]);
@@ -319,6 +330,10 @@ struct FakeBackend : Backend {
         return id;
     }
     int query(int ev) override { return mono_ns() >= ev_time[ev] ? 1 : 0; }
+    int wait_event(int stream, int ev) override {
+        busy_until[stream] = std::max(busy_until[stream], ev_time[ev]);
+        return MIRIAM_OK;
+    }
     void release(int ev) override { free_ev.push_back(ev); }
     double time_us(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int reps) override {
         (void)b; (void)block; (void)reps;
@@ -461,6 +476,8 @@ struct Coord {
     std::vector<int> inflight;                     // shards in flight per stream
     std::vector<double> inflight_us;               // their estimated duration per stream
     int rr_stream = 1;
+    // IB: barrier events (stream, event) of the kernel groups queued on the GPU, oldest first
+    std::deque<std::vector<std::pair<int, int>>> ib_groups;
 
     std::mutex log_mu;
     std::vector<miriam_launch_record> log;
@@ -917,6 +934,88 @@ bool pump_normal(Coord &c, int s) {
     return any;
 }
 
+// IB baseline: one group = the next unsharded kernel of every task with work (the critical
+// request in progress or next in line on the critical stream, each normal task's request on
+// its stream).  Before its kernel, each stream waits on the device for the previous group's
+// kernels on the other streams; after it, the stream records the group's barrier event.  At
+// most two groups are queued, so a newly released critical request starts its first kernel
+// behind at most two groups.  Kernels are launched op by op (a barrier follows every kernel),
+// with one completion event per request, on its last kernel.
+bool pump_ib(Coord &c) {
+    bool any = false;
+    while (!c.ib_groups.empty()) {
+        bool done = true;
+        for (const auto &se : c.ib_groups.front()) {
+            const int q = c.be->query(se.second);
+            if (q == 0) {
+                done = false;
+                break;
+            }
+        }
+        if (!done) break;
+        for (const auto &se : c.ib_groups.front()) c.be->release(se.second);
+        c.ib_groups.pop_front();
+        any = true;
+    }
+    if (c.ib_groups.size() >= 2) return any;
+    std::vector<std::pair<Req *, int>> members;
+    Req *cr = nullptr;
+    if (!c.crit_active.empty() && !c.crit_active.back()->launched_all) {
+        cr = c.crit_active.back();
+    } else if (!c.crit_ready.empty()) {
+        cr = c.crit_ready.front();
+        c.crit_ready.erase(c.crit_ready.begin());
+        c.crit_active.push_back(cr);
+    }
+    if (cr) members.push_back({cr, 0});
+    for (int s = 1; s < c.n_streams; ++s) {
+        Req *r = nullptr;
+        if (!c.be_active[s].empty() && !c.be_active[s].back()->launched_all) {
+            r = c.be_active[s].back();
+        } else if (!c.norm_ready[s].empty()) {
+            r = c.norm_ready[s].front();
+            c.norm_ready[s].pop_front();
+            c.be_active[s].push_back(r);
+        }
+        if (r) members.push_back({r, s});
+    }
+    if (members.empty()) return any;
+    const std::vector<std::pair<int, int>> prev =
+        c.ib_groups.empty() ? std::vector<std::pair<int, int>>() : c.ib_groups.back();
+    std::vector<std::pair<int, int>> cur;
+    for (const auto &m : members) {
+        Req *r = m.first;
+        const int s = m.second;
+        int rc = MIRIAM_OK;
+        for (const auto &se : prev)
+            if (se.first != s && rc == MIRIAM_OK) rc = c.be->wait_event(s, se.second);
+        const miriam_task *t = r->task;
+        const int oi = (int)r->op;
+        const bool last = r->op + 1 == t->ops.size();
+        if (rc == MIRIAM_OK) {
+            const miriam_op *op = t->ops[oi];
+            rc = issue(c, r, oi, 0, op->T, op_full_grid(op), 256, s, false, 0, t->prof[oi].t_unsh_us, last);
+        }
+        if (rc != MIRIAM_OK) {
+            r->status = rc;
+            r->op = t->ops.size();
+            r->launched_all = true;
+            continue;
+        }
+        r->op++;
+        if (last) r->launched_all = true;
+        const int ev = c.be->record(s);
+        if (ev >= 0) cur.push_back({s, ev});
+        else r->status = ev;
+    }
+    if (!cur.empty()) {
+        c.ib_groups.push_back(cur);
+        std::lock_guard<std::mutex> lk(c.stat_mu);
+        c.stats.barrier_groups++;
+    }
+    return true;
+}
+
 bool all_idle(Coord &c) {
     if (!c.crit_active.empty()) return false;
     for (auto &q : c.be_active)
@@ -1023,6 +1122,8 @@ void dispatcher(Coord *cp) {
                     }
                 }
             }
+        } else if (c.cfg.policy == MIRIAM_POLICY_IB) {
+            progress |= pump_ib(c);
         } else {
             // critical requests: unsharded, in order, on the critical stream
             while (!c.crit_ready.empty()) {
@@ -1221,7 +1322,7 @@ int miriam_init(const miriam_config *cfg) {
         set_error("null config");
         return MIRIAM_EINVAL;
     }
-    if (cfg->policy < 0 || cfg->policy > 2 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
+    if (cfg->policy < 0 || cfg->policy > 3 || cfg->backend < 0 || cfg->backend > 1 || cfg->n_be_streams < 1 ||
         cfg->n_be_streams > 7 || cfg->inflight_depth < 1 || !(cfg->top_frac > 0.0 && cfg->top_frac <= 1.0) ||
         !(cfg->quantum_us > 0.0) || cfg->max_blk_frac < 0.0 || cfg->max_pt_frac < 0.0 || cfg->profile_reps < 0 ||
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||

@@ -12,7 +12,7 @@ import ctypes
 from . import _lib as L
 
 POLICY = {"elastic": L.POLICY_ELASTIC, "sequential": L.POLICY_SEQUENTIAL,
-          "multistream": L.POLICY_MULTISTREAM}
+          "multistream": L.POLICY_MULTISTREAM, "ib": L.POLICY_IB}
 
 
 def default_config(**kw) -> L.Config:

@@ -67,7 +67,7 @@ def _collect(co, n, timeout=20.0):
 
 @pytest.mark.parametrize("policy,segments,event_us", [("elastic", 0, 0.0), ("elastic", 1, 0.0), ("elastic", 1, 25.0),
                                                       ("elastic", 0, 1e9), ("sequential", 0, 0.0),
-                                                      ("multistream", 0, 0.0)])
+                                                      ("multistream", 0, 0.0), ("ib", 0, 0.0)])
 def test_every_request_completes_once(L, policy, segments, event_us):
     # event_us: normal launches carry a completion event only every event_us of estimated work
     # (1e9: only each request's last launch)
@@ -164,6 +164,40 @@ def test_elastic_shards_follow_the_tree_and_eq2(L):
                 assert r.grid <= r.eq2_grid_limit
     finally:
         co.shutdown()
+
+
+def test_ib_kernels_advance_in_barrier_groups(L):
+    # Two normal tasks of three kernels each, one long (64 tiles: 4 waves on the simulated
+    # 8 x 2 slots) and one short (1 tile).  Under IB the short task's kernel k+1 waits for the
+    # long task's kernel k, so it ends after two long kernels; on separate streams without
+    # barriers it ends after its own three.
+    tile_ns = 200_000.0
+    long_ns = 4 * tile_ns
+    lat = {}
+    for policy in ("ib", "multistream"):
+        co = _coord(policy=policy, n_be_streams=2, fake_tile_ns=tile_ns, fake_launch_ns=1000.0, profile_reps=0)
+        try:
+            ta = co.task(_net(L, [64, 64, 64]))
+            tb = co.task(_net(L, [1, 1, 1]))
+            ka = co.submit(ta, False)
+            kb = co.submit(tb, False)
+            recs = {r.ticket: r for r in _collect(co, 2)}
+            assert set(recs) == {ka, kb} and all(r.status == 0 for r in recs.values())
+            lat[policy] = recs[kb].t_end_ns - recs[kb].t_release_ns
+            st = co.stats()
+            assert st.barrier_groups == (3 if policy == "ib" else 0)
+            log = co.launch_log()
+            assert len(log) == 6
+            for r in log:
+                assert (r.shard_begin, r.shard_len, r.grid, r.block) == (0, r.num_tiles, r.num_tiles, 256)
+            if policy == "ib":
+                # one kernel per task per group, issued in op order: A0 B0 | A1 B1 | A2 B2
+                by_issue = sorted(log, key=lambda r: r.t_issue_ns)
+                assert [r.op_index for r in by_issue] == [0, 0, 1, 1, 2, 2]
+        finally:
+            co.shutdown()
+    assert lat["ib"] >= 2 * long_ns
+    assert lat["multistream"] < 2 * long_ns
 
 
 def test_sequential_never_overlaps(L):

@@ -18,7 +18,7 @@ def _nan_outputs(net):
 
 
 @pytest.mark.parametrize("policy,graphs,segments,event_us",
-                         [(p, g, 0, 0.0) for p in ("elastic", "sequential", "multistream") for g in (0, 1)]
+                         [(p, g, 0, 0.0) for p in ("elastic", "sequential", "multistream", "ib") for g in (0, 1)]
                          + [("elastic", 1, 1, 0.0), ("elastic", 1, 1, 30.0)])
 def test_coordinator_outputs_match_eager(policy, graphs, segments, event_us):
     from paper_2307_04339_amd import models
@@ -61,8 +61,10 @@ def test_coordinator_outputs_match_eager(policy, graphs, segments, event_us):
         assert all(r.shard_begin == 0 and r.shard_len == r.num_tiles and r.block == 256 for r in crit_recs)
         assert st.launches == len(log)
         assert st.eq2_violations == 0
-        whole = reps * (3 if policy != "elastic" else 1)  # requests launched unsharded
+        # requests launched whole (IB launches kernel by kernel, a barrier after each)
+        whole = {"elastic": reps, "ib": 0}.get(policy, 3 * reps)
         assert st.graph_launches == (whole if graphs else 0)
+        assert (st.barrier_groups > 0) == (policy == "ib")
         assert (st.segment_launches > 0) == (segments == 1)
     finally:
         co.shutdown()
