@@ -382,7 +382,9 @@ def main():
                          "buffers), each its own closed-loop task and stream; Sequential still runs one "
                          "request at a time.  0: the workload's default (3 for the two-task co-runs, 1 for "
                          "the four-task mix, whose three networks already give three streams)")
-    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,ib,elastic,elastic_pause")
+    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,multistream_cu,ib,elastic,elastic_pause")
+    ap.add_argument("--cu-reserve", type=int, default=64,
+                    help="multistream_cu phase: compute units left out of the normal streams' CU mask")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
                     help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
@@ -462,12 +464,14 @@ def main():
                 busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
                 warm_critical=warm, arm_lead_us=arm, segments=args.segments)
     runs = {}
-    for ph in ("solo", "sequential", "multistream", "ib", "elastic", "elastic_pause"):
+    for ph in ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause"):
         if ph not in phases:
             continue
         log(f"phase {ph} ...")
-        policy = {"solo": "elastic", "elastic_pause": "elastic"}.get(ph, ph)
+        policy = {"solo": "elastic", "elastic_pause": "elastic", "multistream_cu": "multistream"}.get(ph, ph)
         pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else ccfg
+        if ph == "multistream_cu":
+            pcfg = dict(ccfg, be_cu_reserve=args.cu_reserve)
         runs[ph] = run_phase(policy, crit_net, be_tasks, args.warmup, args.steps, cfg["period_ms"],
                              cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
         r = runs[ph]
@@ -500,7 +504,7 @@ def main():
                    "inflight_us": inflight_us, "event_us": round(event_us, 2),
                    "busy_policy": 1 if main_name == "elastic_pause" else args.busy_policy,
                    "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
-                   "arm_lead_us": arm, "segments": args.segments},
+                   "arm_lead_us": arm, "segments": args.segments, "cu_reserve_multistream_cu": args.cu_reserve},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]
@@ -509,7 +513,7 @@ def main():
             "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
             "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
             "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
-        for other in ("elastic", "multistream", "ib", "sequential"):
+        for other in ("elastic", "multistream", "multistream_cu", "ib", "sequential"):
             if other in runs and other != main_name:
                 out["critical"][f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
     for ph, r in runs.items():

@@ -303,6 +303,12 @@ typedef struct miriam_config {
                                 much estimated work has gathered on its stream since the last event,
                                 and on each request's last launch (an event costs GPU time between
                                 kernels); 0 = an event per launch */
+    int32_t be_cu_reserve;   /* HIP backend, spatial isolation (any policy): the normal-task streams
+                                are created with a compute-unit mask that leaves out this many CUs
+                                (mask bits n_cu - be_cu_reserve .. n_cu - 1), so only the critical
+                                stream, which keeps every CU, runs there; shard sizing still counts
+                                every CU.  0 = no mask; must be below the device's CU count.
+                                FAKE backend: ignored. */
 } miriam_config;
 
 typedef struct miriam_completion {

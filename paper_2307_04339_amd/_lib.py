@@ -81,6 +81,7 @@ class Config(ctypes.Structure):
         ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32), ("warm_critical", ctypes.c_int32),
         ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
         ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
+        ("be_cu_reserve", ctypes.c_int32),
     ]
 
 

@@ -52,7 +52,9 @@ struct Captured {
 
 struct Backend {
     virtual ~Backend() {}
-    virtual int start(int n_streams) = 0;
+    // Create the streams: 0 critical, 1 .. n-1 normal; with cu_reserve > 0 the normal streams
+    // leave out the top cu_reserve of n_cu compute units.
+    virtual int start(int n_streams, int n_cu, int cu_reserve) = 0;
     virtual int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) = 0;
     virtual int record(int stream) = 0;       // event id >= 0, or < 0 error
     virtual int query(int ev) = 0;            // 1 done, 0 pending, < 0 error
@@ -109,13 +111,30 @@ struct HipBackend : Backend {
     uint64_t *gate_dev = nullptr;
     int wall_khz = 0;               // device wall-clock rate
 
-    int start(int n) override {
+    int start(int n, int n_cu, int cu_reserve) override {
         hipError_t e = hipGetDevice(&dev);
         if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+        std::vector<uint32_t> mask((size_t)(n_cu + 31) / 32, 0u);
+        for (int i = 0; i < n_cu - cu_reserve; ++i) mask[(size_t)i / 32] |= 1u << (i % 32);
         for (int i = 0; i < n; ++i) {
             hipStream_t s;
-            e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
-            if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+            if (i > 0 && cu_reserve > 0) {
+                e = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
+                if (e != hipSuccess) return hip_fail(e, "hipExtStreamCreateWithCUMask");
+                streams.push_back(s);
+                // the mask the stream reports must be the one asked for
+                std::vector<uint32_t> got(mask.size(), 0u);
+                e = hipExtStreamGetCUMask(s, (uint32_t)got.size(), got.data());
+                if (e != hipSuccess) return hip_fail(e, "hipExtStreamGetCUMask");
+                if (got != mask) {
+                    set_error("normal stream reports a different compute-unit mask than requested");
+                    return MIRIAM_ESTATE;
+                }
+                continue;
+            } else {
+                e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+                if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
+            }
             streams.push_back(s);
         }
         e = hipStreamCreateWithFlags(&prof, hipStreamNonBlocking);
@@ -296,7 +315,7 @@ struct FakeBackend : Backend {
     std::vector<int64_t> ev_time;
     std::vector<int> free_ev;
 
-    int start(int n) override {
+    int start(int n, int, int) override {
         busy_until.assign(n, 0);
         return MIRIAM_OK;
     }
@@ -1328,7 +1347,7 @@ int miriam_init(const miriam_config *cfg) {
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
         cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
         cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
-        cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0)) {
+        cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -1346,6 +1365,11 @@ int miriam_init(const miriam_config *cfg) {
             delete c;
             return rc;
         }
+        if (cfg->be_cu_reserve >= dd.n_cu) {
+            delete c;
+            set_error("be_cu_reserve must be below the device's compute-unit count");
+            return MIRIAM_EINVAL;
+        }
         c->n_cu = dd.n_cu;
         c->l_threads = dd.max_threads_per_cu;
         c->be = new HipBackend();
@@ -1359,7 +1383,7 @@ int miriam_init(const miriam_config *cfg) {
         c->l_threads = 2048;
         c->be = f;
     }
-    int rc = c->be->start(c->n_streams);
+    int rc = c->be->start(c->n_streams, c->n_cu, cfg->backend == MIRIAM_BACKEND_HIP ? cfg->be_cu_reserve : 0);
     if (rc != MIRIAM_OK) {
         c->be->stop();
         delete c->be;

@@ -40,6 +40,7 @@ def default_config(**kw) -> L.Config:
     c.arm_lead_us = 0.0
     c.segments = 0
     c.event_us = 0.0
+    c.be_cu_reserve = 0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

@@ -134,3 +134,41 @@ def test_release_gate_ends_on_flag_or_limit(limit_us, open_after_us):
         x = torch.ones(1024, device="cuda") * 2.0
     s.synchronize()
     assert float(x.sum()) == 2048.0
+
+
+@pytest.mark.parametrize("policy", ["multistream", "elastic"])
+def test_cu_masked_normal_streams_match_eager(policy):
+    """Normal streams created with a compute-unit mask (64 CUs left to the critical stream):
+    every request completes with outputs bitwise equal to the eager forward pass, and a
+    reserve of every CU is rejected."""
+    from paper_2307_04339_amd import models
+    from paper_2307_04339_amd import _lib as L
+    from paper_2307_04339_amd.runtime import Coordinator
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    with pytest.raises(L.MiriamError):
+        Coordinator(policy=policy, be_cu_reserve=n_cu, profile_reps=1)
+    crit = models.resnet18(batch=1, dtype="f16")
+    be = models.mobilenetv2(batch=4, dtype="bf16")
+    for n in (crit, be):
+        n.forward()
+    torch.cuda.synchronize()
+    ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
+    co = Coordinator(policy=policy, be_cu_reserve=64, profile_reps=1, n_be_streams=1, inflight_depth=2,
+                     quantum_us=20.0)
+    try:
+        ct = co.task(crit.ops())
+        bt = co.task(be.ops())
+        for rep in range(2):
+            _nan_outputs(crit)
+            _nan_outputs(be)
+            torch.cuda.synchronize()
+            tk = {co.submit(bt, False), co.submit(ct, True), co.submit(bt, False)}
+            co.drain(60000)
+            recs = {r.ticket: r for r in co.poll()}
+            assert set(recs) == tk and all(r.status == 0 for r in recs.values())
+            torch.cuda.synchronize()
+            for n in (crit, be):
+                for l, r in zip(n.layers, ref[n.name]):
+                    assert bits(l.t["y"]) == r, (policy, rep, n.name, l.name)
+    finally:
+        co.shutdown()
