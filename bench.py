@@ -146,6 +146,44 @@ def roofline_of(k, dtype):
                 frac=round(ach / PEAK_HBM_GBS, 4), traffic=None)
 
 
+def index_function_cost(net, reps, flush, lib_mod):
+    """Unsharded time of every layer on the pipelined contraction kernel with the
+    computation-based index function (the default) and with the memory-based one (row
+    indices from a host-computed table staged in LDS), median over `reps` cold launches."""
+    import torch
+
+    def med(op):
+        op.run()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            flush()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            op.run()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return 1000.0 * float(np.median(ts))
+
+    rows = []
+    for layer in net.layers:
+        op = layer.op
+        if op.info.path not in (lib_mod.PATH_DMA, lib_mod.PATH_DMA_UNIFORM) or op.info.ksplit > 1:
+            continue
+        twin = op.variant(flags=op.desc.flags | lib_mod.INDEX_MEMORY)
+        try:
+            if (twin.info.tile_m, twin.info.tile_n) != (op.info.tile_m, op.info.tile_n):
+                continue
+            c_us, m_us = med(op), med(twin)
+        finally:
+            twin.destroy()
+        rows.append(dict(name=layer.name, compute_us=round(c_us, 2), memory_us=round(m_us, 2),
+                         memory_over_compute=round(m_us / c_us, 4)))
+    return rows
+
+
 def shard_overhead(layer, reps, flush, n_cu, lib):
     import ctypes
     import torch
@@ -445,6 +483,9 @@ def main():
         kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
         result["elastic_overhead"] = dict(kernel=kern["kernel"],
                                           **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load()))
+        log("index functions ...")
+        result["index_function"] = {"net": dom_net.name,
+                                    "layers": index_function_cost(dom_net, args.reps, flush, L)}
         result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
                                   **{kk: vv for kk, vv in roofline_of(k, dtype).items()
                                      if kk in ("bound", "achieved", "unit", "frac")})

@@ -70,7 +70,15 @@ typedef enum { MIRIAM_ACT_NONE = 0, MIRIAM_ACT_RELU = 1, MIRIAM_ACT_RELU6 = 2, M
 enum {
     MIRIAM_EPI_BIAS = 1,      /* bias: float32[Cout] */
     MIRIAM_EPI_BN = 2,        /* bn: float32[4*Cout] = gamma, beta, running mean, running var */
-    MIRIAM_EPI_RESIDUAL = 4   /* residual: same dtype/layout/strides as y */
+    MIRIAM_EPI_RESIDUAL = 4,  /* residual: same dtype/layout/strides as y */
+    /* Not an epilogue step: index-function option (§6.4) for CONV2D / GEMM / BGEMM.  With it the
+     * host computes, at creation, every output row's (image, first input row, first input
+     * column) into a device table owned by the op, and each tile stages its rows of the table in
+     * LDS instead of dividing the row index in the kernel (memory-based index function; the
+     * default is computation-based).  Results are bitwise the same.  Served by the pipelined
+     * contraction kernel only: the op is created on it (16-byte aligned K-major operands; an
+     * explicit tile must be 1..4), else creation fails with MIRIAM_EINVAL. */
+    MIRIAM_INDEX_MEMORY = 8
 };
 
 /*

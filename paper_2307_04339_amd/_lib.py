@@ -23,6 +23,7 @@ DTYPE_CODE = {"f32": F32, "f16": F16, "bf16": BF16}
 ACT_NONE, ACT_RELU, ACT_RELU6, ACT_GELU = 0, 1, 2, 3
 ACT_CODE = {"none": 0, "relu": 1, "relu6": 2, "gelu": 3}
 EPI_BIAS, EPI_BN, EPI_RESIDUAL = 1, 2, 4
+INDEX_MEMORY = 8  # memory-based index function (host-computed row table)
 POLICY_ELASTIC, POLICY_SEQUENTIAL, POLICY_MULTISTREAM, POLICY_IB = 0, 1, 2, 3
 BACKEND_HIP, BACKEND_FAKE = 0, 1
 

@@ -84,7 +84,9 @@ struct DmaKernel {
     static_assert(KT % KSTEP == 0, "chunk must hold whole MFMA steps");
 };
 
-template <class T, int TM, int TN, int MS, int P, bool UNI>
+// MI: memory-based index function (output-row indices from the host-computed table a.rowtab,
+// staged in LDS per tile) instead of the computation-based default.
+template <class T, int TM, int TN, int MS, int P, bool UNI, bool MI = false>
 __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_SIMD)) void igemm_dma_kernel(
     IgemmArgs a, Shard sh) {
     typedef DmaKernel<T, TM, TN, MS, P> K_;
@@ -135,6 +137,15 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         const int64_t yoff = b0 * a.sy0 + b1 * a.sy1;
         const int64_t m0 = (int64_t)mt * TM, n0 = (int64_t)nt * TN;
 
+        // memory-based index function: the tile's rows of the host-computed table are staged
+        // in the ring's last stage, which the first DMA into it (after the main loop's first
+        // barrier) only overwrites once every wave has read its entries
+        const int4 *const tab = reinterpret_cast<const int4 *>(smem + (S - 1) * K_::STAGE);
+        if constexpr (MI) {
+            const int4 *src = reinterpret_cast<const int4 *>(a.rowtab) + m0;
+            for (int r = tid; r < TM; r += NT) const_cast<int4 *>(tab)[r] = src[r];
+            __syncthreads();
+        }
         // A instruction j of this wave covers tile rows 8q..8q+7, q = j*P + pw
         const T *a_base[NIA];
         int32_t a_h0[NIA], a_w0[NIA];
@@ -145,14 +156,22 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         for (int j = 0; j < NIA; ++j) {
             const int row = 8 * (j * P + pw) + lrow;
             const int64_t m = m0 + row;
-            a_ok[j] = m < a.M;
-            const uint32_t mm = a_ok[j] ? (uint32_t)m : 0u;
-            const uint32_t img = fdiv(mm, a.fd_howo);
-            const uint32_t pq = mm - img * HoWo32;
-            const uint32_t p = fdiv(pq, a.fd_wo), q = pq - p * Wo32;
-            a_base[j] = Xb + (int64_t)img * a.img_x;
-            a_h0[j] = (int32_t)p * a.stride - a.pad;
-            a_w0[j] = (int32_t)q * a.stride - a.pad;
+            if constexpr (MI) {
+                const int4 e = tab[row];
+                a_ok[j] = e.w != 0;
+                a_base[j] = Xb + (int64_t)e.x * a.img_x;
+                a_h0[j] = e.y;
+                a_w0[j] = e.z;
+            } else {
+                a_ok[j] = m < a.M;
+                const uint32_t mm = a_ok[j] ? (uint32_t)m : 0u;
+                const uint32_t img = fdiv(mm, a.fd_howo);
+                const uint32_t pq = mm - img * HoWo32;
+                const uint32_t p = fdiv(pq, a.fd_wo), q = pq - p * Wo32;
+                a_base[j] = Xb + (int64_t)img * a.img_x;
+                a_h0[j] = (int32_t)p * a.stride - a.pad;
+                a_w0[j] = (int32_t)q * a.stride - a.pad;
+            }
             // logical 16-byte piece of this slot, in the slice's first chunk
             const int32_t k = (int32_t)(slice * (uint32_t)a.cps) * KT + ((slot ^ ((row >> 1) & 7)) * VEC);
             if constexpr (UNI) {
@@ -501,11 +520,11 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
     }
 }
 
-template <class T, int TM, int TN, int MS, bool UNI>
+template <class T, int TM, int TN, int MS, bool UNI, bool MI = false>
 inline void igemm_dma_table(const void *out[3], int *lds) {
-    out[0] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 1, UNI>);
-    out[1] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 2, UNI>);
-    out[2] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 4, UNI>);
+    out[0] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 1, UNI, MI>);
+    out[1] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 2, UNI, MI>);
+    out[2] = reinterpret_cast<const void *>(&igemm_dma_kernel<T, TM, TN, MS, 4, UNI, MI>);
     *lds = DmaKernel<T, TM, TN, MS, 4>::LDS_BYTES;
 }
 
@@ -517,6 +536,18 @@ inline int igemm_dma_table_cfg(int cfg, const void *out[3], int *lds) {
     case CFG_128: igemm_dma_table<T, 128, 128, 32, UNI>(out, lds); return 0;
     case CFG_128x64: igemm_dma_table<T, 128, 64, 32, UNI>(out, lds); return 0;
     case CFG_256x128: igemm_dma_table<T, 256, 128, 32, UNI>(out, lds); return 0;
+    default: return -1;
+    }
+}
+
+// Memory-based index variants (tiles 32x32, 64x64, 128x128, 128x64).
+template <class T>
+inline int igemm_dma_mi_table_cfg(int cfg, bool uni, const void *out[3], int *lds) {
+    switch (cfg) {
+    case CFG_32: uni ? igemm_dma_table<T, 32, 32, 16, true, true>(out, lds) : igemm_dma_table<T, 32, 32, 16, false, true>(out, lds); return 0;
+    case CFG_64: uni ? igemm_dma_table<T, 64, 64, 32, true, true>(out, lds) : igemm_dma_table<T, 64, 64, 32, false, true>(out, lds); return 0;
+    case CFG_128: uni ? igemm_dma_table<T, 128, 128, 32, true, true>(out, lds) : igemm_dma_table<T, 128, 128, 32, false, true>(out, lds); return 0;
+    case CFG_128x64: uni ? igemm_dma_table<T, 128, 64, 32, true, true>(out, lds) : igemm_dma_table<T, 128, 64, 32, false, true>(out, lds); return 0;
     default: return -1;
     }
 }

@@ -21,6 +21,10 @@ enum Family { FAM_IGEMM = 0, FAM_PIX = 1, FAM_ROW = 2, FAM_SKINNY = 3 };
 int igemm_kernels_f32(int cfg, int lay, const void *out[3], int *lds);
 int igemm_kernels_f16(int cfg, int lay, const void *out[3], int *lds);
 int igemm_kernels_bf16(int cfg, int lay, const void *out[3], int *lds);
+// pipelined kernel with the memory-based index function (tiles 1..4); uni: chunk-uniform decode
+int igemm_mi_kernels_f32(int cfg, bool uni, const void *out[3], int *lds);
+int igemm_mi_kernels_f16(int cfg, bool uni, const void *out[3], int *lds);
+int igemm_mi_kernels_bf16(int cfg, bool uni, const void *out[3], int *lds);
 int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int skinny_kernels(int dtype, const void *out[3]);
@@ -47,6 +51,7 @@ struct miriam_op {
     std::atomic<int> pending{0};  // submitted requests that still reference the op
     void *work = nullptr;         // split-K partial tiles (device memory owned by the op)
     void *counters = nullptr;     // split-K arrival counters (device memory owned by the op)
+    void *rowtab = nullptr;       // memory-based index table (device memory owned by the op)
 };
 
 namespace miriam {

@@ -75,6 +75,9 @@ struct IgemmArgs {
     int32_t cps;           // K chunks per slice
     float *work;           // ksplit fp32 partial tiles per output tile (ksplit > 1)
     int32_t *counters;     // arrivals per output tile; back to 0 once a pass over the op completes
+    // memory-based index function: per output row m < mT * TM, (image, p * stride - pad,
+    // q * stride - pad, m < M) as 4 int32; null = computed in the kernel
+    const int32_t *rowtab;
     Epilogue epi;
 };
 

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "internal.h"
 
@@ -37,6 +38,15 @@ static int get_igemm_table(int dtype, int cfg, int lay, const void *out[3], int 
     case MIRIAM_F32: return igemm_kernels_f32(cfg, lay, out, lds);
     case MIRIAM_F16: return igemm_kernels_f16(cfg, lay, out, lds);
     case MIRIAM_BF16: return igemm_kernels_bf16(cfg, lay, out, lds);
+    default: return -1;
+    }
+}
+
+static int get_igemm_mi_table(int dtype, int cfg, bool uni, const void *out[3], int *lds) {
+    switch (dtype) {
+    case MIRIAM_F32: return igemm_mi_kernels_f32(cfg, uni, out, lds);
+    case MIRIAM_F16: return igemm_mi_kernels_f16(cfg, uni, out, lds);
+    case MIRIAM_BF16: return igemm_mi_kernels_bf16(cfg, uni, out, lds);
     default: return -1;
     }
 }
@@ -76,14 +86,14 @@ static Epilogue make_epi(const miriam_op_desc &d, int64_t C) {
     e.bn = static_cast<const float *>(d.bn);
     e.eps = d.eps;
     e.act = d.act;
-    e.flags = d.flags;
+    e.flags = d.flags & (MIRIAM_EPI_BIAS | MIRIAM_EPI_BN | MIRIAM_EPI_RESIDUAL);
     e.C = C;
     return e;
 }
 
-static int check_epi(const miriam_op_desc &d) {
+static int check_epi(const miriam_op_desc &d, int extra_flags = 0) {
     if (d.act < MIRIAM_ACT_NONE || d.act > MIRIAM_ACT_GELU) return einval("unknown activation");
-    if (d.flags & ~(MIRIAM_EPI_BIAS | MIRIAM_EPI_BN | MIRIAM_EPI_RESIDUAL)) return einval("unknown epilogue flag");
+    if (d.flags & ~(MIRIAM_EPI_BIAS | MIRIAM_EPI_BN | MIRIAM_EPI_RESIDUAL | extra_flags)) return einval("unknown epilogue flag");
     if ((d.flags & MIRIAM_EPI_BIAS) && !d.bias) return einval("bias flag without bias pointer");
     if ((d.flags & MIRIAM_EPI_BN) && !d.bn) return einval("bn flag without bn pointer");
     if ((d.flags & MIRIAM_EPI_RESIDUAL) && !d.residual) return einval("residual flag without residual pointer");
@@ -177,8 +187,9 @@ static int create_igemm(miriam_op *op) {
         b_vec = (a.K % V == 0) && (a.ldw % V == 0) && (a.sw0 % V == 0) && (a.sw1 % V == 0) && aligned16(d.wt);
     if (nmaj && d.dtype == MIRIAM_F32) return einval("bgemm: [k][n] right operand needs fp16/bf16");
     if (d.kind == MIRIAM_OP_CONV2D && d.b_nmajor) return einval("conv2d: weights must be [Cout][KH][KW][Cin]");
-    int rc = check_epi(d);
+    int rc = check_epi(d, MIRIAM_INDEX_MEMORY);
     if (rc) return rc;
+    const bool memidx = (d.flags & MIRIAM_INDEX_MEMORY) != 0;
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.Nc);
     if (a.Ho * a.Wo >= (int64_t)INT32_MAX) return einval("contraction: output image too large for 32-bit pixel indexing");
@@ -214,10 +225,15 @@ static int create_igemm(miriam_op *op) {
                        d.ksplit <= 1 && a.img_x < (int64_t)INT32_MAX;
     const int64_t rw_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
     int cfg = d.tile;
-    if (cfg == 0 && rw_ok && rw_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5) cfg = CFG_RW;
-    if (cfg == 0 && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5)
+    // the memory-based index function is served by the pipelined kernel only
+    if (cfg == 0 && !memidx && rw_ok && rw_T >= (int64_t)device_cus() * 3 / 2 && halo_tx * 32 * 4 <= a.Wo * 5)
+        cfg = CFG_RW;
+    if (cfg == 0 && !memidx && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 &&
+        halo_tx * 32 * 4 <= a.Wo * 5)
         cfg = CFG_HALO;
-    if (cfg == 0) cfg = skinny_ok ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
+    if (cfg == 0) cfg = (skinny_ok && !memidx) ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
+    if (memidx && (cfg == CFG_RW || cfg == CFG_HALO || cfg == TILE_SKINNY))
+        return einval("memory-based index function: tiles 1..4 only (pipelined contraction kernel)");
     if (cfg == CFG_RW) {
         if (!rw_ok) return einval("tile 8 (resident-weight direct conv) needs an fp16/bf16 conv that is 3x3 stride 1 with C in {8,16,32,64} and at most 64 output channels, 3x3 stride 2 with C = 8 and at most 64 output channels, or 1x1 stride 1 pad 0 with C in {16,24,32,64}; 16-byte rows; no split K");
         a.tX = halo_tx;
@@ -340,8 +356,40 @@ static int create_igemm(miriam_op *op) {
         else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
         // every 128-byte K chunk inside one filter tap: per-lane pointers advance per chunk
         if (op->lay == LAY_VEC && a.C % (128 / es) == 0) op->lay = LAY_VEC_UNI;
-        if (get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
+        if (!memidx && get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
             return einval("no kernel for this dtype / layout");
+        if (memidx) {
+            if (op->lay != LAY_VEC && op->lay != LAY_VEC_UNI)
+                return einval("memory-based index function needs 16-byte aligned K-major operands");
+            if (get_igemm_mi_table(d.dtype, cfg, op->lay == LAY_VEC_UNI, op->kern, &op->lds_bytes) != 0)
+                return einval("memory-based index function: tiles 1..4 only");
+            // host-computed index table: one (image, h0, w0, valid) row per tile row
+            const int64_t rows = a.mT * tile_m_of(cfg);
+            std::vector<int32_t> tab((size_t)rows * 4, 0);
+            const int64_t howo = a.Ho * a.Wo;
+            for (int64_t m = 0; m < rows; ++m) {
+                const int64_t mm = m < a.M ? m : 0;
+                const int64_t img = mm / howo, pq = mm % howo, p = pq / a.Wo, q = pq % a.Wo;
+                int32_t *e = &tab[(size_t)m * 4];
+                e[0] = (int32_t)img;
+                e[1] = (int32_t)(p * a.stride - a.pad);
+                e[2] = (int32_t)(q * a.stride - a.pad);
+                e[3] = m < a.M ? 1 : 0;
+            }
+            const size_t tb = tab.size() * sizeof(int32_t);
+            if (hipMalloc(&op->rowtab, tb) != hipSuccess) {
+                (void)hipGetLastError();
+                op->rowtab = nullptr;
+                set_error("memory-based index table allocation failed");
+                return MIRIAM_ENOMEM;
+            }
+            if (hipMemcpy(op->rowtab, tab.data(), tb, hipMemcpyHostToDevice) != hipSuccess) {
+                (void)hipGetLastError();
+                set_error("memory-based index table upload failed");
+                return MIRIAM_ENOMEM;
+            }
+            a.rowtab = static_cast<const int32_t *>(op->rowtab);
+        }
     }
     // kernels index tiles, rows and batch entries with 32-bit arithmetic
     if (op->T >= (int64_t)INT32_MAX || a.M >= (int64_t)INT32_MAX || batch >= (int64_t)INT32_MAX)
@@ -575,6 +623,7 @@ int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
     if (rc != MIRIAM_OK) {
         if (op->work) (void)hipFree(op->work);
         if (op->counters) (void)hipFree(op->counters);
+        if (op->rowtab) (void)hipFree(op->rowtab);
         delete op;
         return rc;
     }
@@ -630,6 +679,7 @@ int miriam_op_destroy(miriam_op *op) {
     }
     if (op->work) (void)hipFree(op->work);
     if (op->counters) (void)hipFree(op->counters);
+    if (op->rowtab) (void)hipFree(op->rowtab);
     delete op;
     return MIRIAM_OK;
 }

@@ -58,6 +58,25 @@ class ElasticOp:
             ctypes.c_void_p(owner_wg.data_ptr()), ctypes.c_void_p(owner_iter.data_ptr()),
             ctypes.c_void_p(count.data_ptr())), "miriam_elastic_launch_traced")
 
+    def variant(self, **changes) -> "ElasticOp":
+        """A second op over the same tensors, from this op's descriptor with `changes` applied
+        (for example flags=op.desc.flags | INDEX_MEMORY)."""
+        lib = L.load()
+        new = ElasticOp.__new__(ElasticOp)
+        d = L.OpDesc.from_buffer_copy(self.desc)
+        for k, v in changes.items():
+            setattr(d, k, v)
+        new.desc = d
+        new._keep = self._keep
+        h = ctypes.c_void_p()
+        L.check(lib.miriam_op_create(ctypes.byref(d), ctypes.byref(h)), "miriam_op_create")
+        new.handle = h
+        info = L.OpInfo()
+        L.check(lib.miriam_op_query(h, ctypes.byref(info)), "miriam_op_query")
+        new.info = info
+        new.T = int(info.num_tiles)
+        return new
+
     def run(self, stream=None) -> None:
         """Unsharded launch: the whole tile space at the op's full grid (one workgroup per
         tile, or the resident capacity for kernels that keep operands across tiles), block 256."""
@@ -93,27 +112,29 @@ def _epi(bias, bn, residual):
 
 
 def conv2d(x, w, y, stride=1, pad=0, bias=None, bn=None, residual=None, act="none", eps=1e-5, tile=0,
-           ksplit=0):
-    """x [N,H,W,C], w [K,KH,KW,C], y [N,Ho,Wo,K]; bias [K] f32; bn [4,K] f32."""
+           ksplit=0, memory_index=False):
+    """x [N,H,W,C], w [K,KH,KW,C], y [N,Ho,Wo,K]; bias [K] f32; bn [4,K] f32.
+    memory_index: output-row indices from a host-computed table instead of in-kernel division."""
     N, H, W, C = x.shape
     K, KH, KW, C2 = w.shape
     assert C2 == C
     return ElasticOp(L.OP_CONV2D, x.dtype, keep=(x, w, y, bias, bn, residual),
                      n=N, h=H, w=W, c=C, k=K, kh=KH, kw=KW, stride=stride, pad=pad, groups=1,
                      x=x, wt=w, y=y, bias=bias, bn=bn, residual=residual,
-                     flags=_epi(bias, bn, residual), act=L.ACT_CODE[act], eps=eps, tile=tile, ksplit=ksplit)
+                     flags=_epi(bias, bn, residual) | (L.INDEX_MEMORY if memory_index else 0),
+                     act=L.ACT_CODE[act], eps=eps, tile=tile, ksplit=ksplit)
 
 
 def gemm(x, w, y, bias=None, residual=None, act="none", tile=0, ldx=0, ldw=0, ldy=0, m=None, n=None, k=None,
-         ksplit=0):
+         ksplit=0, memory_index=False):
     """y[m][n] = act(x[m][:] . w[n][:] + bias + residual)."""
     M = m if m is not None else x.shape[0]
     Kk = k if k is not None else x.shape[-1]
     Nn = n if n is not None else w.shape[0]
     return ElasticOp(L.OP_GEMM, x.dtype, keep=(x, w, y, bias, residual),
                      m=M, nn=Nn, kk=Kk, ldx=ldx, ldw=ldw, ldy=ldy, x=x, wt=w, y=y, bias=bias,
-                     residual=residual, flags=_epi(bias, None, residual), act=L.ACT_CODE[act], tile=tile,
-                     ksplit=ksplit)
+                     residual=residual, flags=_epi(bias, None, residual) | (L.INDEX_MEMORY if memory_index else 0),
+                     act=L.ACT_CODE[act], tile=tile, ksplit=ksplit)
 
 
 def bgemm(x, w, y, m, n, k, batch, batch_div, ldx, ldw, ldy, sx=(0, 0), sw=(0, 0), sy=(0, 0),

@@ -179,8 +179,10 @@ def test_ib_kernels_advance_in_barrier_groups(L):
         try:
             ta = co.task(_net(L, [64, 64, 64]))
             tb = co.task(_net(L, [1, 1, 1]))
-            ka = co.submit(ta, False)
-            kb = co.submit(tb, False)
+            # one common timed release, so both requests are released in the same dispatcher pass
+            rel = co.now_ns() + 3_000_000
+            ka = co.submit(ta, False, release_ns=rel)
+            kb = co.submit(tb, False, release_ns=rel)
             recs = {r.ticket: r for r in _collect(co, 2)}
             assert set(recs) == {ka, kb} and all(r.status == 0 for r in recs.values())
             lat[policy] = recs[kb].t_end_ns - recs[kb].t_release_ns

@@ -154,7 +154,11 @@ def test_op_create_rejects_bad_descriptors(lib):
     assert lib.miriam_op_destroy(h) == 0
     bad = [dict(ok, kind=99), dict(ok, dtype=7), dict(ok, x=None), dict(ok, stride=0),
            dict(ok, kh=20, pad=0), dict(ok, groups=4), dict(ok, act=9), dict(ok, flags=1),
-           dict(ok, flags=64), dict(ok, c=0), dict(ok, tile=7)]
+           dict(ok, flags=64), dict(ok, c=0), dict(ok, tile=7),
+           # memory-based index function: pipelined contraction kernel only
+           dict(ok, c=64, k=64, h=32, w=32, flags=L.INDEX_MEMORY, tile=8),
+           dict(ok, c=3, flags=L.INDEX_MEMORY),  # rows not a 16-byte multiple: staged kernel
+           dict(ok, kind=L.OP_DWCONV, k=16, groups=16, kh=3, kw=3, wt=FAKE, flags=L.INDEX_MEMORY)]
     for d in bad:
         rc, _ = _create(lib, _desc(**d))
         assert rc == L.EINVAL, d
