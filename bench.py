@@ -184,6 +184,67 @@ def index_function_cost(net, reps, flush, lib_mod):
     return rows
 
 
+def transformed_overhead(reps, flush):
+    """Kernels elasticised by the source-to-source transformer: median time of the plain launch
+    and of the elastic form unsharded (grid = the plain grid) and as 4 shards, cold caches.
+    Workloads: bias + ReLU over 8 x 112 x 112 x 64 fp32, 2x2 max pooling of the same tensor,
+    and a 1024^3 fp32 product with 16 x 16 shared-memory tiles."""
+    import torch
+    from paper_2307_04339_amd.transform import lib as TL
+    T = TL.load()
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x = torch.rand((8, 112, 112, 64), device="cuda", generator=g) * 2 - 1
+    bvec = torch.rand(64, device="cuda", generator=g) * 2 - 1
+    y = torch.empty_like(x)
+    yp = torch.empty((8, 56, 56, 64), device="cuda")
+    A = torch.rand((1024, 1024), device="cuda", generator=g)
+    B = torch.rand((1024, 1024), device="cuda", generator=g)
+    C = torch.empty((1024, 1024), device="cuda")
+    n = x.numel()
+    cases = {
+        "bias_relu": ((n + 255) // 256, 256,
+                      lambda G, bl: T.plain_bias_relu_plain_launch(x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64,
+                                                                   G, bl, None),
+                      lambda G, b0, l, gr, bl: T.plain_bias_relu_elastic_launch(
+                          x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64, G, b0, l, gr, bl, None)),
+        "maxpool2": ((yp.numel() + 127) // 128, 128,
+                     lambda G, bl: T.plain_maxpool2_plain_launch(x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, bl,
+                                                                 None),
+                     lambda G, b0, l, gr, bl: T.plain_maxpool2_elastic_launch(
+                         x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, b0, l, gr, bl, None)),
+        "tiled_gemm": (64 * 64, 256,
+                       lambda G, bl: T.plain_tiled_gemm_plain_launch(A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                                                     1024, 1024, 1024, G, bl, None),
+                       lambda G, b0, l, gr, bl: T.plain_tiled_gemm_elastic_launch(
+                           A.data_ptr(), B.data_ptr(), C.data_ptr(), 1024, 1024, 1024, G, b0, l, gr, bl, None)),
+    }
+
+    def med(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            flush()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return 1000.0 * float(np.median(ts))
+
+    out = {}
+    for name, (G, blk, plain, elastic) in cases.items():
+        q = [(i * G // 4, (i + 1) * G // 4 - i * G // 4) for i in range(4)]
+        t_plain = med(lambda: plain(G, blk))
+        t_el = med(lambda: elastic(G, 0, G, G, blk))
+        t_4 = med(lambda: [elastic(G, b0, l, l, blk) for b0, l in q])
+        out[name] = dict(logical_blocks=G, block=blk, plain_us=round(t_plain, 2), elastic_us=round(t_el, 2),
+                         shards4_us=round(t_4, 2), elastic_over_plain=round(t_el / t_plain, 4))
+    return out
+
+
 def shard_overhead(layer, reps, flush, n_cu, lib):
     import ctypes
     import torch
@@ -486,6 +547,8 @@ def main():
         log("index functions ...")
         result["index_function"] = {"net": dom_net.name,
                                     "layers": index_function_cost(dom_net, args.reps, flush, L)}
+        log("transformed kernels ...")
+        result["transformed_kernels"] = transformed_overhead(args.reps, flush)
         result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
                                   **{kk: vv for kk, vv in roofline_of(k, dtype).items()
                                      if kk in ("bound", "achieved", "unit", "frac")})

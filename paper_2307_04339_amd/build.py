@@ -14,6 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libmiriam.so")
+ELASTIFIED = os.path.join(PKG, "libmiriam_elastified.so")
 BUILD = os.path.join(ROOT, "_build")
 
 ARCH = "gfx950"
@@ -62,6 +63,9 @@ def build(incremental: bool = False, jobs: int | None = None) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
     os.replace(tmp, OUT)
+    # plain kernels and their elastic forms from the source-to-source transformer
+    from paper_2307_04339_amd.transform import elastify
+    elastify.build(ELASTIFIED, os.path.join(BUILD, "elastify"), FLAGS)
     return OUT
 
 

@@ -1,0 +1,76 @@
+"""The source-to-source elastic transformer on the host: parsing of plain kernels, the id
+rewrites, rejected inputs, and the generated library's launchers (argument checks only; no
+kernel runs without a GPU)."""
+import ctypes
+import os
+
+import pytest
+
+from paper_2307_04339_amd.transform import elastify
+
+
+def _plain():
+    with open(os.path.join(elastify.PLAIN_DIR, "kernels.hip")) as f:
+        return f.read()
+
+
+def test_parse_plain_kernels():
+    ks = {k.name: k for k in elastify.parse(_plain())}
+    assert set(ks) == {"plain_bias_relu", "plain_maxpool2", "plain_tiled_gemm"}
+    assert (ks["plain_bias_relu"].block, ks["plain_bias_relu"].block_elastic) == (256, True)
+    assert (ks["plain_maxpool2"].block, ks["plain_maxpool2"].block_elastic) == (128, True)
+    g = ks["plain_tiled_gemm"]
+    assert (g.block, g.block_elastic) == (256, False)
+    assert len(g.shared_decls) == 2 and "__shared__" not in g.body
+    assert ks["plain_bias_relu"].param_names == ["x", "b", "y", "n", "c"]
+
+
+def test_ids_become_logical():
+    out = elastify.transform(_plain())
+    for k in elastify.parse(_plain()):
+        start = out.index(f"__global__ void {k.name}_elastic(")
+        end = out.index('extern "C"', start)
+        kern = out[start:end]
+        # physical ids appear only in the shard loop and the logical-thread rounds
+        body = kern[kern.index("[&]() {"):]
+        for ident in ("blockIdx.x", "gridDim.x", "threadIdx.x", "blockDim.x"):
+            assert ident not in body, (k.name, ident)
+        assert "__mi_sh.begin + blockIdx.x" in kern and "__mi_b += gridDim.x" in kern
+        if k.block_elastic:
+            assert f"{k.block}u / blockDim.x" in kern
+        else:
+            assert "const unsigned __mi_tid = threadIdx.x;" in kern
+    assert "__mi_bid * __mi_bdim + __mi_tid" in out
+    assert "i += __mi_grid * __mi_bdim" in out  # a grid-stride loop keeps the logical grid
+
+
+@pytest.mark.parametrize("src,msg", [
+    ("// elastic: block 256\n__global__ void k(float *y) { y[blockIdx.y] = 0.0f; }", "multi-dimensional"),
+    ("__global__ void k(float *y) { y[blockIdx.x] = 0.0f; }", "no '// elastic: block N'"),
+    ("// elastic: block 96\n__global__ void k(float *y) { y[blockIdx.x] = 0.0f; }", "64, 128 or 256"),
+    ("// elastic: block 64\n__global__ void k(float *y) { y[0] = 0.0f; ", "unbalanced"),
+])
+def test_rejects_unsupported_kernels(src, msg):
+    with pytest.raises(elastify.TransformError, match=msg):
+        elastify.parse(src)
+
+
+def test_return_ends_one_logical_thread():
+    # an early return stays inside the per-thread lambda, so the shard loop goes on
+    src = "// elastic: block 64\n__global__ void k(float *y, int n) {\n  if (threadIdx.x >= n) return;\n  y[threadIdx.x] = 1.0f;\n}\n"
+    out = elastify.transform(src)
+    kern = out[out.index("__global__ void k_elastic("):out.index('extern "C"')]
+    assert kern.index("for (long long __mi_b") < kern.index("[&]() {") < kern.index("return;")
+
+
+def test_launchers_check_arguments():
+    from paper_2307_04339_amd.transform import lib as T
+    lib = T.load()
+    nul = None
+    # shard out of range, zero grid, block not dividing the logical block, fixed block changed
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 2, 3, 1, 256, nul) == -3
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 0, 1, 0, 256, nul) == -3
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 0, 1, 1, 96, nul) == -3
+    assert lib.plain_maxpool2_elastic_launch(nul, nul, 1, 4, 4, 8, 2, 0, 2, 1, 256, nul) == -3
+    assert lib.plain_tiled_gemm_elastic_launch(nul, nul, nul, 16, 16, 16, 1, 0, 1, 1, 128, nul) == -3
+    assert lib.plain_tiled_gemm_plain_launch(nul, nul, nul, 16, 16, 16, 1, 64, nul) == -3
