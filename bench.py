@@ -482,6 +482,9 @@ def main():
                          "request at a time.  0: the workload's default (3 for the two-task co-runs, 1 for "
                          "the four-task mix, whose three networks already give three streams)")
     ap.add_argument("--phases", default="kernels,solo,sequential,multistream,multistream_cu,ib,elastic,elastic_pause")
+    ap.add_argument("--whole-when-clear", type=int, default=-1,
+                    help="launch normal requests whole when they end before the next known critical "
+                         "release (-1: with the release guard)")
     ap.add_argument("--cu-reserve", type=int, default=64,
                     help="multistream_cu phase: compute units left out of the normal streams' CU mask")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -562,11 +565,12 @@ def main():
     guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
     warm = args.warm_critical if args.warm_critical >= 0 else guard
     arm = args.arm_lead_us if args.arm_lead_us >= 0 else (500.0 if guard else 0.0)
+    whole = args.whole_when_clear if args.whole_when_clear >= 0 else guard
     inflight_us = args.inflight_us if args.inflight_us >= 0 else 100.0
     event_us = args.event_us if args.event_us >= 0 else inflight_us / 3.0
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=inflight_us, event_us=event_us,
                 busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
-                warm_critical=warm, arm_lead_us=arm, segments=args.segments)
+                warm_critical=warm, arm_lead_us=arm, segments=args.segments, whole_when_clear=whole)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause"):
         if ph not in phases:
@@ -608,7 +612,8 @@ def main():
                    "inflight_us": inflight_us, "event_us": round(event_us, 2),
                    "busy_policy": 1 if main_name == "elastic_pause" else args.busy_policy,
                    "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
-                   "arm_lead_us": arm, "segments": args.segments, "cu_reserve_multistream_cu": args.cu_reserve},
+                   "arm_lead_us": arm, "segments": args.segments, "whole_when_clear": whole,
+                   "cu_reserve_multistream_cu": args.cu_reserve},
     }
     if "solo" in runs and main_run:
         solo = runs["solo"]

@@ -317,6 +317,13 @@ typedef struct miriam_config {
                                 stream, which keeps every CU, runs there; shard sizing still counts
                                 every CU.  0 = no mask; must be below the device's CU count.
                                 FAKE backend: ignored. */
+    int32_t whole_when_clear; /* ELASTIC with release_guard and graphs: a normal request not yet
+                                started, whose whole unsharded sequence (task profile) ends,
+                                behind the normal work queued, before the next timed critical
+                                release while no critical work is pending or running, is launched
+                                as one replay of its captured graph (the greedy whole-GPU rule
+                                taken to the whole request) instead of as shards; 0 = shards
+                                only. */
 } miriam_config;
 
 typedef struct miriam_completion {
@@ -344,6 +351,8 @@ typedef struct miriam_stats {
     int64_t armed_releases;   /* critical requests queued behind a gate ahead of their release */
     int64_t segment_launches; /* runs of short normal ops issued as one captured unit */
     int64_t barrier_groups;   /* IB: kernel groups issued behind an inter-stream barrier */
+    int64_t whole_clear_launches; /* normal requests launched whole before a known release
+                                     (whole_when_clear) */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */

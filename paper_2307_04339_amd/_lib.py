@@ -82,7 +82,7 @@ class Config(ctypes.Structure):
         ("graphs", ctypes.c_int32), ("release_guard", ctypes.c_int32), ("warm_critical", ctypes.c_int32),
         ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
         ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
-        ("be_cu_reserve", ctypes.c_int32),
+        ("be_cu_reserve", ctypes.c_int32), ("whole_when_clear", ctypes.c_int32),
     ]
 
 
@@ -111,7 +111,7 @@ class Stats(ctypes.Structure):
         ("decision_ns_total", ctypes.c_double), ("completed", ctypes.c_int64),
         ("graph_launches", ctypes.c_int64), ("warm_launches", ctypes.c_int64),
         ("armed_releases", ctypes.c_int64), ("segment_launches", ctypes.c_int64),
-        ("barrier_groups", ctypes.c_int64),
+        ("barrier_groups", ctypes.c_int64), ("whole_clear_launches", ctypes.c_int64),
     ]
 
 

@@ -810,6 +810,25 @@ bool guard_holds(Coord &c, int64_t t0, double est_us) {
     return true;
 }
 
+// whole_when_clear: normal request r, not started, may run as one replay of its task's captured
+// sequence: no critical request is pending or on the GPU, the next critical release is known
+// (release guard), and the request's whole estimated time behind the normal work queued ends
+// before that release.
+constexpr double kWholeMargin = 2.0;
+
+bool whole_fits(Coord &c, const Req *r, int64_t t0) {
+    if (!c.cfg.release_guard || !c.cfg.graphs || r->op != 0 || r->cursor != 0 || r->n_shards != 0) return false;
+    const miriam_task *t = r->task;
+    if (t->graphs.empty() || t->end_us.empty() || c.crit_timed.empty()) return false;
+    if (!c.crit_ready.empty() || !c.crit_active.empty() || c.armed) return false;
+    const Req *nx = c.crit_timed.top();
+    const double warm_us = c.cfg.warm_critical ? nx->task->warm_us : 0.0;
+    // the task profile times each op alone with warm caches; requests of several streams
+    // running side by side from cold caches take longer, hence the margin
+    const double est = kWholeMargin * (queued_normal_us(c) + t->end_us.back());
+    return t0 + (int64_t)(1000.0 * (est + warm_us)) <= nx->release;
+}
+
 // Launch segment sg of normal request r on `stream` and record its event.
 int issue_segment(Coord &c, Req *r, const miriam_task::Segment &sg, int stream, bool with_event) {
     int rc = c.be->launch_captured(sg.unit, stream);
@@ -893,6 +912,16 @@ bool pump_normal(Coord &c, int s) {
             break;
         }
         miriam_task *t = r->task;
+        if (c.cfg.whole_when_clear && whole_fits(c, r, t0)) {
+            launch_whole(c, r, s);
+            {
+                std::lock_guard<std::mutex> lk(c.stat_mu);
+                c.stats.whole_clear_launches++;
+            }
+            any = true;
+            if (r->status != MIRIAM_OK) seal(c, r, s);
+            continue;
+        }
         const int sid = (!busy && r->cursor == 0 && r->op < t->seg_at.size()) ? t->seg_at[r->op] : -1;
         if (sid >= 0) {  // a run of short ops as one captured unit
             const miriam_task::Segment &sg = t->segs[sid];
@@ -1347,7 +1376,8 @@ int miriam_init(const miriam_config *cfg) {
         cfg->inflight_us < 0.0 || cfg->busy_policy < 0 || cfg->busy_policy > 2 || cfg->graphs < 0 ||
         cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
         cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
-        cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0) {
+        cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0 ||
+        cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }

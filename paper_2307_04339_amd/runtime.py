@@ -41,6 +41,7 @@ def default_config(**kw) -> L.Config:
     c.segments = 0
     c.event_us = 0.0
     c.be_cu_reserve = 0
+    c.whole_when_clear = 0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

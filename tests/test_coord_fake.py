@@ -341,3 +341,44 @@ def test_armed_critical_requests_start_at_release(L):
         assert got[a].t_start_ns >= rel
     finally:
         co.shutdown()
+
+
+def test_whole_requests_launch_only_clear_of_timed_releases(L):
+    # whole_when_clear: a normal request goes out as one whole-request launch only while no
+    # critical work is pending or running and it is estimated to end before the next timed
+    # release; near a release its ops are sharded (and held by the guard) as usual
+    co = _coord(release_guard=1, whole_when_clear=1, busy_policy=1, inflight_depth=4, quantum_us=100.0,
+                fake_tile_ns=2000.0, fake_launch_ns=3000.0)
+    try:
+        crit = co.task(_net(L, [4, 4]))
+        be = co.task(_net(L, [32, 32, 32]))
+        now = co.now_ns()
+        period = 2_000_000
+        rel = [now + 3_000_000 + i * period for i in range(5)]
+        tk = [co.submit(crit, True, release_ns=r) for r in rel]
+        tk += [co.submit(be, False) for _ in range(30)]
+        recs = _collect(co, len(tk), timeout=30.0)
+        assert sorted(r.ticket for r in recs) == sorted(tk) and all(r.status == 0 for r in recs)
+        st = co.stats()
+        assert st.whole_clear_launches > 0
+        log = co.launch_log()
+        crit_t = {r.ticket for r in recs if r.criticality == 1}
+        # every whole normal request was issued with its estimated end before the next release
+        whole = {}
+        for r in log:
+            if r.criticality == 0:
+                whole.setdefault(r.ticket, []).append(r)
+        # a whole launch logs each op at its full grid (32 tiles); shards sized by the
+        # coordinator use at most the simulated 8 x 2 workgroup slots
+        def is_whole(rs):
+            return len(rs) == 3 and all(x.shard_len == x.num_tiles == x.grid for x in rs)
+        assert sum(1 for rs in whole.values() if is_whole(rs)) == st.whole_clear_launches
+        for rs in whole.values():
+            if is_whole(rs):
+                t_issue = rs[0].t_issue_ns
+                est_end = t_issue + int(1000 * sum(x.est_us for x in rs))
+                nxt = [r for r in rel if r > t_issue]
+                assert not nxt or est_end <= nxt[0]
+        assert crit_t
+    finally:
+        co.shutdown()

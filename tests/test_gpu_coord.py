@@ -70,12 +70,13 @@ def test_coordinator_outputs_match_eager(policy, graphs, segments, event_us):
         co.shutdown()
 
 
-@pytest.mark.parametrize("arm_lead_us", [0.0, 500.0])
-def test_warmed_periodic_critical_requests_match_eager(arm_lead_us):
+@pytest.mark.parametrize("arm_lead_us,whole", [(0.0, 0), (500.0, 0), (500.0, 1)])
+def test_warmed_periodic_critical_requests_match_eager(arm_lead_us, whole):
     """Timed critical releases with normal work running: the release guard holds normal
     shards and a cache-warming pass runs ahead of each release, and (arm_lead_us > 0) each
-    critical request is queued behind a gate before its release; outputs stay bitwise equal
-    and armed requests complete after their release."""
+    critical request is queued behind a gate before its release; with whole_when_clear, normal
+    requests that fit before the next release run as whole-request launches.  Outputs stay
+    bitwise equal and armed requests complete after their release."""
     from paper_2307_04339_amd import models
     from paper_2307_04339_amd.runtime import Coordinator
     crit = models.resnet18(batch=1, dtype="f16")
@@ -86,7 +87,7 @@ def test_warmed_periodic_critical_requests_match_eager(arm_lead_us):
     ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
     co = Coordinator(policy="elastic", graphs=1, release_guard=1, warm_critical=1, busy_policy=1,
                      profile_reps=1, n_be_streams=1, inflight_depth=4, inflight_us=100.0, quantum_us=40.0,
-                     arm_lead_us=arm_lead_us)
+                     arm_lead_us=arm_lead_us, whole_when_clear=whole)
     try:
         ct = co.task(crit.ops())
         bt = co.task(be.ops())
@@ -109,7 +110,8 @@ def test_warmed_periodic_critical_requests_match_eager(arm_lead_us):
                     assert bits(l.t["y"]) == r, (rep, n.name, l.name)
         st = co.stats()
         assert st.warm_launches >= 1
-        assert st.graph_launches == 8
+        assert st.graph_launches == 8 + st.whole_clear_launches
+        assert (st.whole_clear_launches > 0) == (whole == 1)
         assert st.armed_releases == (8 if arm_lead_us > 0 else 0)
     finally:
         co.shutdown()
