@@ -89,8 +89,9 @@ struct PixArgs {
     const void *res;   // same layout as y
     int64_t N, H, W, C, Ho, Wo;
     int32_t KH, KW, stride, pad;
-    int64_t items;     // lane items: N*Ho*Wo*(C/V)
-    FastDiv fd_cv, fd_howo, fd_wo;  // division by C/V, Ho*Wo and Wo (item -> pixel -> image, row, column)
+    int64_t items;     // lane items: N*Ho*Wo*(C/V); PIX_DW3: N*Ho*Ws*(C/V)
+    int64_t Ws;        // PIX_DW3: strips of kDwStrip output pixels per output row
+    FastDiv fd_cv, fd_howo, fd_wo;  // division by C/V, Ho*Wo and Wo (PIX_DW3: Ho*Ws and Ws)
     Epilogue epi;
 };
 
@@ -107,7 +108,8 @@ struct RowArgs {
     int has_res;
 };
 
-enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3 };
+enum PixKind { PIX_DW = 0, PIX_MAX = 1, PIX_AVG = 2, PIX_EW = 3, PIX_DW3 = 4 };
+constexpr int kDwStrip = 4;  // PIX_DW3: output pixels along a row per lane item
 enum RowKind { ROW_SOFTMAX = 0, ROW_LAYERNORM = 1 };
 enum IgemmLayout { LAY_VEC = 0, LAY_SCALAR = 1, LAY_VEC_NB = 2, LAY_SCALAR_NB = 3, LAY_VEC_UNI = 4, LAY_HALO = 5, LAY_RW = 6 };
 enum IgemmCfg { CFG_32 = 1, CFG_64 = 2, CFG_128 = 3, CFG_128x64 = 4, CFG_256x128 = 6, CFG_HALO = 7, CFG_RW = 8 };

@@ -24,6 +24,10 @@ static int pix_table_k(int kind, bool vec, const void *out[3]) {
     case PIX_MAX: pix_table_v<T, PIX_MAX>(vec, out); return 0;
     case PIX_AVG: pix_table_v<T, PIX_AVG>(vec, out); return 0;
     case PIX_EW: pix_table_v<T, PIX_EW>(vec, out); return 0;
+    case PIX_DW3:
+        if (!vec) return -1;
+        pix_table<T, 16 / sizeof(T), PIX_DW3>(out);
+        return 0;
     default: return -1;
     }
 }

@@ -175,6 +175,84 @@ __device__ __forceinline__ void pix_item(const PixArgs &a, int64_t u) {
     }
 }
 
+// One lane item of the 3x3 depthwise strip kernel: V consecutive channels of kDwStrip
+// horizontally adjacent output pixels.  The strip's window (3 rows of (kDwStrip - 1) * ST + 3
+// input pixels) is loaded once, and the weights and epilogue parameters once per item; each
+// output element then takes its taps in row-major order, skipping padding taps, exactly as in
+// pix_item, so the results are bitwise those of the per-pixel kernel.
+template <class T, int V, int ACT, int ST>
+__device__ __forceinline__ void pix_dw3_item(const PixArgs &a, int64_t u) {
+    constexpr int NW = (kDwStrip - 1) * ST + 3;  // input pixels per window row
+    const T *__restrict__ X = static_cast<const T *>(a.x);
+    T *__restrict__ Y = static_cast<T *>(a.y);
+    const T *const zsrc = reinterpret_cast<const T *>(g_pix_zero);
+    const uint32_t CV = (uint32_t)(a.C / V), u32 = (uint32_t)u;
+    const uint32_t stu = fdiv(u32, a.fd_cv);  // strip index
+    const int64_t c0 = (int64_t)(u32 - stu * CV) * V;
+    const uint32_t HoWs = (uint32_t)(a.Ho * a.Ws), Ws = (uint32_t)a.Ws;
+    const uint32_t n = fdiv(stu, a.fd_howo);
+    const uint32_t pq = stu - n * HoWs;
+    const uint32_t pu = fdiv(pq, a.fd_wo);
+    const int32_t p = (int32_t)pu, q0 = (int32_t)(pq - pu * Ws) * kDwStrip;
+    const int32_t h0 = p * ST - a.pad, w0 = q0 * ST - a.pad;
+    const int32_t H32 = (int32_t)a.H, W32 = (int32_t)a.W, Wo32 = (int32_t)a.Wo;
+    const T *xn = X + (int64_t)n * a.H * a.W * a.C + c0;
+    const T *Wt = static_cast<const T *>(a.w);
+    T xv[3][NW][V], wv[9][V];
+    bool rok[3], cok[NW];
+#pragma unroll
+    for (int j = 0; j < NW; ++j) cok[j] = w0 + j >= 0 && w0 + j < W32;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        const int32_t h = h0 + r;
+        rok[r] = h >= 0 && h < H32;
+#pragma unroll
+        for (int j = 0; j < NW; ++j)
+            ld_items<T, V>(rok[r] && cok[j] ? xn + ((int64_t)h * a.W + w0 + j) * a.C : zsrc, xv[r][j]);
+    }
+#pragma unroll
+    for (int k = 0; k < 9; ++k) ld_items<T, V>(Wt + (int64_t)k * a.C + c0, wv[k]);
+    ChanParams cp[V];
+    chan_params_vec<V>(a.epi, c0, cp);
+#pragma unroll
+    for (int i = 0; i < kDwStrip; ++i) {
+        const int32_t q = q0 + i;
+        if (q >= Wo32) break;
+        float acc[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+            for (int s = 0; s < 3; ++s) {
+                const int j = i * ST + s;
+                if (!(rok[r] && cok[j])) continue;
+#pragma unroll
+                for (int e = 0; e < V; ++e)
+                    acc[e] = __builtin_fmaf(TypeOps<T>::to_f(xv[r][j][e]), TypeOps<T>::to_f(wv[3 * r + s][e]), acc[e]);
+            }
+        const int64_t pix = ((int64_t)n * a.Ho + p) * a.Wo + q;
+        T rv[V];
+        if (a.epi.flags & EPI_RES) ld_items<T, V>(static_cast<const T *>(a.res) + pix * a.C + c0, rv);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            float v = epilogue_pre(a.epi, cp[e], acc[e]);
+            if (a.epi.flags & EPI_RES) v += TypeOps<T>::to_f(rv[e]);
+            acc[e] = act_c<ACT>(v);
+        }
+        T *dst = Y + pix * a.C + c0;
+        if constexpr (V * sizeof(T) == 16) {
+            Vec16<T> o;
+#pragma unroll
+            for (int e = 0; e < V; ++e) o.e[e] = TypeOps<T>::from_f(acc[e]);
+            st_vec(dst, o);
+        } else {
+#pragma unroll
+            for (int e = 0; e < V; ++e) st_f(dst + e, acc[e]);
+        }
+    }
+}
+
 template <class T, int V, int KIND, int P>
 __global__ __launch_bounds__(kWave * P) void pix_kernel(PixArgs a, Shard sh) {
     const int pw = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -191,7 +269,14 @@ __global__ __launch_bounds__(kWave * P) void pix_kernel(PixArgs a, Shard sh) {
             for (int s = 0; s < kLogicalWaves / P; ++s) {
                 const int lam = s * P + pw;
                 const int64_t u = t * kLogicalBlock + lam * kWave + lane;
-                if (u < a.items) pix_item<T, V, KIND, ACT>(a, u);
+                if constexpr (KIND == PIX_DW3) {
+                    if (u < a.items) {
+                        if (a.stride == 1) pix_dw3_item<T, V, ACT, 1>(a, u);
+                        else pix_dw3_item<T, V, ACT, 2>(a, u);
+                    }
+                } else if (u < a.items) {
+                    pix_item<T, V, KIND, ACT>(a, u);
+                }
             }
         }
     });

@@ -145,6 +145,9 @@ DW_CASES = [
     (2, 28, 28, 192, 2, "bn"),
     (1, 7, 7, 960, 1, "bn"),
     (1, 13, 11, 20, 2, "bias"),   # C not a vector multiple -> element path
+    (1, 9, 10, 16, 2, "bias"),    # stride 2, 5-pixel output rows, odd height
+    (3, 5, 6, 8, 1, "bn"),        # one channel vector, 6-pixel rows, batch 3
+    (16, 56, 54, 144, 1, "bn"),   # strip kernel (3 tiles per CU): 54-pixel rows end in a half strip
 ]
 
 
@@ -168,6 +171,9 @@ def test_dwconv_matches_oracle(ops, orc, dtype, case):
     Ho, Wo = (H + 2 - 3) // s + 1, (W + 2 - 3) // s + 1
     y = empty((N, Ho, Wo, C), dtype)
     op = ops.dwconv(x, w, y, stride=s, pad=1, bias=bias, bn=bn, act="relu6")
+    if (N, H, W, C) == (16, 56, 54, 144) and dtype != "f32":
+        # 3x3 stride-1 strips of 4 output pixels per 16-byte channel vector: 14 strips per row
+        assert op.T == (N * Ho * 14 * (C // 8) + 255) // 256
     op.run()
     torch.cuda.synchronize()
     # oracle weights [C][3][3][1] (groups = C)
