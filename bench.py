@@ -485,6 +485,8 @@ def main():
     ap.add_argument("--whole-when-clear", type=int, default=-1,
                     help="launch normal requests whole when they end before the next known critical "
                          "release (-1: with the release guard)")
+    ap.add_argument("--whole-margin", type=float, default=0.0,
+                    help="factor on the estimate of whole-request launches (0: the library's 2.0)")
     ap.add_argument("--cu-reserve", type=int, default=64,
                     help="multistream_cu phase: compute units left out of the normal streams' CU mask")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -570,7 +572,8 @@ def main():
     event_us = args.event_us if args.event_us >= 0 else inflight_us / 3.0
     ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=inflight_us, event_us=event_us,
                 busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
-                warm_critical=warm, arm_lead_us=arm, segments=args.segments, whole_when_clear=whole)
+                warm_critical=warm, arm_lead_us=arm, segments=args.segments, whole_when_clear=whole,
+                whole_margin=args.whole_margin)
     runs = {}
     for ph in ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause"):
         if ph not in phases:

@@ -324,6 +324,8 @@ typedef struct miriam_config {
                                 as one replay of its captured graph (the greedy whole-GPU rule
                                 taken to the whole request) instead of as shards; 0 = shards
                                 only. */
+    double whole_margin;     /* whole_when_clear: factor on the estimated time of the queued normal
+                                work plus the request (profiled alone, warm caches); 0 = 2.0 */
 } miriam_config;
 
 typedef struct miriam_completion {

@@ -83,6 +83,7 @@ class Config(ctypes.Structure):
         ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
         ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
         ("be_cu_reserve", ctypes.c_int32), ("whole_when_clear", ctypes.c_int32),
+        ("whole_margin", ctypes.c_double),
     ]
 
 

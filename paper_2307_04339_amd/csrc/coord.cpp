@@ -814,8 +814,6 @@ bool guard_holds(Coord &c, int64_t t0, double est_us) {
 // sequence: no critical request is pending or on the GPU, the next critical release is known
 // (release guard), and the request's whole estimated time behind the normal work queued ends
 // before that release.
-constexpr double kWholeMargin = 2.0;
-
 bool whole_fits(Coord &c, const Req *r, int64_t t0) {
     if (!c.cfg.release_guard || !c.cfg.graphs || r->op != 0 || r->cursor != 0 || r->n_shards != 0) return false;
     const miriam_task *t = r->task;
@@ -825,7 +823,8 @@ bool whole_fits(Coord &c, const Req *r, int64_t t0) {
     const double warm_us = c.cfg.warm_critical ? nx->task->warm_us : 0.0;
     // the task profile times each op alone with warm caches; requests of several streams
     // running side by side from cold caches take longer, hence the margin
-    const double est = kWholeMargin * (queued_normal_us(c) + t->end_us.back());
+    const double margin = c.cfg.whole_margin > 0.0 ? c.cfg.whole_margin : 2.0;
+    const double est = margin * (queued_normal_us(c) + t->end_us.back());
     return t0 + (int64_t)(1000.0 * (est + warm_us)) <= nx->release;
 }
 
@@ -1377,7 +1376,7 @@ int miriam_init(const miriam_config *cfg) {
         cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
         cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
         cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0 ||
-        cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1) {
+        cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1 || !(cfg->whole_margin >= 0.0)) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }

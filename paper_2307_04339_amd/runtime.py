@@ -42,6 +42,7 @@ def default_config(**kw) -> L.Config:
     c.event_us = 0.0
     c.be_cu_reserve = 0
     c.whole_when_clear = 0
+    c.whole_margin = 0.0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]
