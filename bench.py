@@ -496,7 +496,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(each task set is placed on one device; see the multi-GPU note in DESIGN.md)",
+              "(with several GPUs each critical / best-effort task set runs on a device of its own, "
+              "so the co-run is measured on one)",
               file=sys.stderr)
         sys.exit(2)
 
