@@ -272,11 +272,14 @@ static int create_igemm(miriam_op *op) {
         // K slices: each slice keeps at least one 128-element group per logical wave.  The
         // library choice splits until the op has about four tiles per CU, so a shard of a
         // quarter of the op still gives every CU a tile (more slices measured slower
-        // unsharded: VGG-16 fc6 at eight tiles per CU 73 us against 59 us).
+        // unsharded: VGG-16 fc6 at eight tiles per CU 73 us against 59 us), and keeps slices of
+        // about 1024 K values or more beyond two slices (VGG-16 fc8, 4096 -> 1000: 12.0 us at
+        // 8 slices, 9.9 us at 4)
         const int64_t max_ks = std::max<int64_t>(1, cdiv(a.K, 128) / 4);
         int64_t ks = d.ksplit > 1 ? std::min<int64_t>(d.ksplit, max_ks)
                      : d.ksplit == 1 ? 1
-                                     : std::min<int64_t>(max_ks, cdiv(4 * (int64_t)device_cus(), a.nT));
+                                     : std::min<int64_t>(std::min<int64_t>(max_ks, cdiv(4 * (int64_t)device_cus(), a.nT)),
+                                                         std::max<int64_t>(2, a.K / 1024));
         ks = std::max<int64_t>(1, ks);
         a.ksplit = 1;
         if (ks > 1) {
