@@ -204,19 +204,19 @@ def transformed_overhead(reps, flush):
     cases = {
         "bias_relu": ((n + 255) // 256, 256,
                       lambda G, bl: T.plain_bias_relu_plain_launch(x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64,
-                                                                   G, bl, None),
+                                                                   G, 1, None),
                       lambda G, b0, l, gr, bl: T.plain_bias_relu_elastic_launch(
-                          x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64, G, b0, l, gr, bl, None)),
+                          x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64, G, 1, b0, l, gr, bl, None)),
         "maxpool2": ((yp.numel() + 127) // 128, 128,
-                     lambda G, bl: T.plain_maxpool2_plain_launch(x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, bl,
+                     lambda G, bl: T.plain_maxpool2_plain_launch(x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, 1,
                                                                  None),
                      lambda G, b0, l, gr, bl: T.plain_maxpool2_elastic_launch(
-                         x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, b0, l, gr, bl, None)),
+                         x.data_ptr(), yp.data_ptr(), 8, 112, 112, 64, G, 1, b0, l, gr, bl, None)),
         "tiled_gemm": (64 * 64, 256,
                        lambda G, bl: T.plain_tiled_gemm_plain_launch(A.data_ptr(), B.data_ptr(), C.data_ptr(),
-                                                                     1024, 1024, 1024, G, bl, None),
+                                                                     1024, 1024, 1024, G, 1, None),
                        lambda G, b0, l, gr, bl: T.plain_tiled_gemm_elastic_launch(
-                           A.data_ptr(), B.data_ptr(), C.data_ptr(), 1024, 1024, 1024, G, b0, l, gr, bl, None)),
+                           A.data_ptr(), B.data_ptr(), C.data_ptr(), 1024, 1024, 1024, G, 1, b0, l, gr, bl, None)),
     }
 
     def med(fn):

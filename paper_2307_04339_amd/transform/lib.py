@@ -53,11 +53,12 @@ def load():
     for name, k in kernels().items():
         args = [_argtype(p) for p in k.params.split(",")]
         fp = getattr(lib, f"{name}_plain_launch")
-        fp.argtypes = args + [ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+        fp.argtypes = args + [ctypes.c_int, ctypes.c_int, ctypes.c_void_p]  # grid_x, grid_y, stream
         fp.restype = ctypes.c_int
         fe = getattr(lib, f"{name}_elastic_launch")
-        fe.argtypes = args + [ctypes.c_longlong, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int, ctypes.c_int,
-                              ctypes.c_void_p]
+        # grid_x, grid_y, begin, len, grid, block, stream
+        fe.argtypes = args + [ctypes.c_int, ctypes.c_int, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int,
+                              ctypes.c_int, ctypes.c_void_p]
         fe.restype = ctypes.c_int
     _lib = lib
     return lib

@@ -48,3 +48,26 @@ __global__ void plain_tiled_gemm(const float *A, const float *B, float *C, int M
     }
     if (row < M && col < N) C[(long long)row * N + col] = acc;
 }
+
+// y = a * x + (x one column to the right, zero past the edge) over an R x C row-major image,
+// one element per thread on a 2-D grid of 32 x 8 blocks.
+// elastic: block 32x8
+__global__ void plain_shift_add2d(const float *x, float *y, int rows, int cols, float a) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    const int r = blockIdx.y * blockDim.y + threadIdx.y;
+    if (r >= rows || c >= cols) return;
+    const float right = c + 1 < cols ? x[(long long)r * cols + c + 1] : 0.0f;
+    y[(long long)r * cols + c] = a * x[(long long)r * cols + c] + right;
+}
+
+// out = in transposed (R x C -> C x R) through a 16 x 17 shared tile on a 2-D grid of 16 x 16
+// blocks; it synchronises its block, so its elastic form keeps the 256-thread block.
+// elastic: block 16x16
+__global__ void plain_transpose16(const float *in, float *out, int rows, int cols) {
+    __shared__ float tile[16][17];
+    const int c = blockIdx.x * 16 + threadIdx.x, r = blockIdx.y * 16 + threadIdx.y;
+    if (r < rows && c < cols) tile[threadIdx.y][threadIdx.x] = in[(long long)r * cols + c];
+    __syncthreads();
+    const int oc = blockIdx.y * 16 + threadIdx.x, orow = blockIdx.x * 16 + threadIdx.y;
+    if (orow < cols && oc < rows) out[(long long)orow * rows + oc] = tile[threadIdx.x][threadIdx.y];
+}

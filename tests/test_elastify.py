@@ -16,7 +16,10 @@ def _plain():
 
 def test_parse_plain_kernels():
     ks = {k.name: k for k in elastify.parse(_plain())}
-    assert set(ks) == {"plain_bias_relu", "plain_maxpool2", "plain_tiled_gemm"}
+    assert set(ks) == {"plain_bias_relu", "plain_maxpool2", "plain_tiled_gemm", "plain_shift_add2d",
+                       "plain_transpose16"}
+    assert (ks["plain_shift_add2d"].bx, ks["plain_shift_add2d"].by, ks["plain_shift_add2d"].block_elastic) == (32, 8, True)
+    assert (ks["plain_transpose16"].bx, ks["plain_transpose16"].by, ks["plain_transpose16"].block_elastic) == (16, 16, False)
     assert (ks["plain_bias_relu"].block, ks["plain_bias_relu"].block_elastic) == (256, True)
     assert (ks["plain_maxpool2"].block, ks["plain_maxpool2"].block_elastic) == (128, True)
     g = ks["plain_tiled_gemm"]
@@ -33,19 +36,25 @@ def test_ids_become_logical():
         kern = out[start:end]
         # physical ids appear only in the shard loop and the logical-thread rounds
         body = kern[kern.index("[&]() {"):]
-        for ident in ("blockIdx.x", "gridDim.x", "threadIdx.x", "blockDim.x"):
+        for ident in ("blockIdx.x", "gridDim.x", "threadIdx.x", "blockDim.x", "blockIdx.y", "gridDim.y",
+                      "threadIdx.y", "blockDim.y"):
             assert ident not in body, (k.name, ident)
         assert "__mi_sh.begin + blockIdx.x" in kern and "__mi_b += gridDim.x" in kern
         if k.block_elastic:
             assert f"{k.block}u / blockDim.x" in kern
         else:
-            assert "const unsigned __mi_tid = threadIdx.x;" in kern
-    assert "__mi_bid * __mi_bdim + __mi_tid" in out
-    assert "i += __mi_grid * __mi_bdim" in out  # a grid-stride loop keeps the logical grid
+            assert "const unsigned __mi_t = threadIdx.x;" in kern
+    assert "__mi_bx * __mi_bdx + __mi_tx" in out
+    assert "i += __mi_gx * __mi_bdx" in out  # a grid-stride loop keeps the logical grid
+    assert "__mi_by * __mi_bdy + __mi_ty" in out  # 2-D ids from the flattened block and thread
+    assert "__mi_by = __mi_gy == 1u ? 0u : __mi_bu / __mi_gx;" in out
+    assert "__mi_bx = __mi_bu - __mi_by * __mi_gx;" in out
+    assert "__mi_tx = __mi_t % 32u, __mi_ty = __mi_t / 32u" in out
 
 
 @pytest.mark.parametrize("src,msg", [
-    ("// elastic: block 256\n__global__ void k(float *y) { y[blockIdx.y] = 0.0f; }", "multi-dimensional"),
+    ("// elastic: block 256\n__global__ void k(float *y) { y[blockIdx.z] = 0.0f; }", "not supported"),
+    ("// elastic: block 16x12\n__global__ void k(float *y) { y[threadIdx.y] = 0.0f; }", "64, 128 or 256"),
     ("__global__ void k(float *y) { y[blockIdx.x] = 0.0f; }", "no '// elastic: block N'"),
     ("// elastic: block 96\n__global__ void k(float *y) { y[blockIdx.x] = 0.0f; }", "64, 128 or 256"),
     ("// elastic: block 64\n__global__ void k(float *y) { y[0] = 0.0f; ", "unbalanced"),
@@ -67,10 +76,14 @@ def test_launchers_check_arguments():
     from paper_2307_04339_amd.transform import lib as T
     lib = T.load()
     nul = None
-    # shard out of range, zero grid, block not dividing the logical block, fixed block changed
-    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 2, 3, 1, 256, nul) == -3
-    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 0, 1, 0, 256, nul) == -3
-    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 0, 1, 1, 96, nul) == -3
-    assert lib.plain_maxpool2_elastic_launch(nul, nul, 1, 4, 4, 8, 2, 0, 2, 1, 256, nul) == -3
-    assert lib.plain_tiled_gemm_elastic_launch(nul, nul, nul, 16, 16, 16, 1, 0, 1, 1, 128, nul) == -3
-    assert lib.plain_tiled_gemm_plain_launch(nul, nul, nul, 16, 16, 16, 1, 64, nul) == -3
+    # shard out of range, zero grid, block not dividing the logical block, fixed block changed,
+    # empty logical grid
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 1, 2, 3, 1, 256, nul) == -3
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 1, 0, 1, 0, 256, nul) == -3
+    assert lib.plain_bias_relu_elastic_launch(nul, nul, nul, 10, 2, 4, 1, 0, 1, 1, 96, nul) == -3
+    assert lib.plain_maxpool2_elastic_launch(nul, nul, 1, 4, 4, 8, 2, 1, 0, 2, 1, 256, nul) == -3
+    assert lib.plain_tiled_gemm_elastic_launch(nul, nul, nul, 16, 16, 16, 1, 1, 0, 1, 1, 128, nul) == -3
+    assert lib.plain_transpose16_elastic_launch(nul, nul, 16, 16, 1, 1, 0, 1, 1, 64, nul) == -3
+    assert lib.plain_shift_add2d_elastic_launch(nul, nul, 8, 32, 1.0, 2, 3, 0, 7, 1, 256, nul) == -3
+    assert lib.plain_shift_add2d_plain_launch(nul, nul, 8, 32, 1.0, 0, 1, nul) == -3
+    assert lib.plain_tiled_gemm_plain_launch(nul, nul, nul, 16, 16, 16, 1, 0, nul) == -3

@@ -4,7 +4,8 @@ shard-length blocks and every allowed physical block, writes bitwise the output 
 launch, which matches a numpy reference.
 
 Inputs: seeded U[-1, 1] float32 tensors (bias + ReLU over 1000 x 37, max pooling of a
-2 x 18 x 22 x 24 image, a 100 x 70 by 70 x 90 product)."""
+2 x 18 x 22 x 24 image, a 100 x 70 by 70 x 90 product; on 2-D grids and blocks a shifted
+sum over a 45 x 70 image and the transpose of a 50 x 37 matrix)."""
 import numpy as np
 import pytest
 import torch
@@ -60,8 +61,8 @@ def test_bias_relu(T):
     y = torch.empty((n_rows, c), dtype=torch.float32, device="cuda")
     n = n_rows * c
     G = (n + 255) // 256
-    _check_elastic(lambda G: T.plain_bias_relu_plain_launch(_p(x), _p(b), _p(y), n, c, G, 256, None),
-                   lambda G, b0, l, g, bl: T.plain_bias_relu_elastic_launch(_p(x), _p(b), _p(y), n, c, G, b0, l, g, bl,
+    _check_elastic(lambda G: T.plain_bias_relu_plain_launch(_p(x), _p(b), _p(y), n, c, G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_bias_relu_elastic_launch(_p(x), _p(b), _p(y), n, c, G, 1, b0, l, g, bl,
                                                                              None),
                    y, G, [64, 128, 256], seed=1)
     assert np.array_equal(y.cpu().numpy(), np.maximum(x64 + b64[None, :], np.float32(0)))
@@ -74,8 +75,8 @@ def test_maxpool2(T):
     x = _dev(x64)
     y = torch.empty((N, H // 2, W // 2, C), dtype=torch.float32, device="cuda")
     G = 7  # a grid-stride kernel: 7 logical blocks of 128 threads cover all 4752 outputs
-    _check_elastic(lambda G: T.plain_maxpool2_plain_launch(_p(x), _p(y), N, H, W, C, G, 128, None),
-                   lambda G, b0, l, g, bl: T.plain_maxpool2_elastic_launch(_p(x), _p(y), N, H, W, C, G, b0, l, g, bl,
+    _check_elastic(lambda G: T.plain_maxpool2_plain_launch(_p(x), _p(y), N, H, W, C, G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_maxpool2_elastic_launch(_p(x), _p(y), N, H, W, C, G, 1, b0, l, g, bl,
                                                                            None),
                    y, G, [64, 128], seed=3)
     ref = x64.reshape(N, H // 2, 2, W // 2, 2, C).max(axis=(2, 4))
@@ -90,10 +91,41 @@ def test_tiled_gemm_keeps_its_block(T):
     A, B = _dev(a64), _dev(b64)
     C = torch.empty((M, N), dtype=torch.float32, device="cuda")
     G = ((M + 15) // 16) * ((N + 15) // 16)
-    _check_elastic(lambda G: T.plain_tiled_gemm_plain_launch(_p(A), _p(B), _p(C), M, N, K, G, 256, None),
-                   lambda G, b0, l, g, bl: T.plain_tiled_gemm_elastic_launch(_p(A), _p(B), _p(C), M, N, K, G, b0, l,
+    _check_elastic(lambda G: T.plain_tiled_gemm_plain_launch(_p(A), _p(B), _p(C), M, N, K, G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_tiled_gemm_elastic_launch(_p(A), _p(B), _p(C), M, N, K, G, 1, b0, l,
                                                                              g, bl, None),
                    C, G, [256], seed=5)
     ref = a64.astype(np.float64) @ b64.astype(np.float64)
     err = np.max(np.abs(C.cpu().numpy() - ref)) / np.max(np.abs(ref))
     assert err < 1e-5
+
+
+def test_shift_add2d_on_a_2d_grid(T):
+    rng = np.random.default_rng(6)
+    R, Cc, a = 45, 70, 0.75
+    x64 = rng.uniform(-1, 1, (R, Cc)).astype(np.float32)
+    x = _dev(x64)
+    y = torch.empty((R, Cc), dtype=torch.float32, device="cuda")
+    gx, gy = (Cc + 31) // 32, (R + 7) // 8  # 32 x 8 blocks
+    _check_elastic(lambda G: T.plain_shift_add2d_plain_launch(_p(x), _p(y), R, Cc, a, gx, gy, None),
+                   lambda G, b0, l, g, bl: T.plain_shift_add2d_elastic_launch(_p(x), _p(y), R, Cc, a, gx, gy, b0, l,
+                                                                              g, bl, None),
+                   y, gx * gy, [64, 128, 256], seed=7)
+    right = np.zeros_like(x64)
+    right[:, :-1] = x64[:, 1:]
+    ref = (np.float32(a) * x64 + right).astype(np.float32)
+    assert np.allclose(y.cpu().numpy(), ref, rtol=0, atol=2e-7)
+
+
+def test_transpose16_keeps_its_2d_block(T):
+    rng = np.random.default_rng(8)
+    R, Cc = 50, 37
+    x64 = rng.uniform(-1, 1, (R, Cc)).astype(np.float32)
+    x = _dev(x64)
+    y = torch.empty((Cc, R), dtype=torch.float32, device="cuda")
+    gx, gy = (Cc + 15) // 16, (R + 15) // 16
+    _check_elastic(lambda G: T.plain_transpose16_plain_launch(_p(x), _p(y), R, Cc, gx, gy, None),
+                   lambda G, b0, l, g, bl: T.plain_transpose16_elastic_launch(_p(x), _p(y), R, Cc, gx, gy, b0, l, g,
+                                                                              bl, None),
+                   y, gx * gy, [256], seed=9)
+    assert np.array_equal(y.cpu().numpy(), x64.T)
