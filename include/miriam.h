@@ -201,11 +201,28 @@ int miriam_elastic_launch(const miriam_op *op, int64_t shard_begin, int64_t shar
 /*
  * Same launch, additionally recording for every tile t of the shard, in caller-owned
  * device arrays of T int32 entries: owner_wg[t] = physical workgroup, owner_iter[t] =
- * persistent-loop iteration, and count[t] += 1 (atomic).  Used to check the tile map.
+ * persistent-loop iteration, and count[t] += 1 (atomic).  Used to check the tile map
+ * (§6.2 elastic grid).  When wave_phys and wave_slot (caller-owned device arrays of 4 T
+ * int32 entries) are non-null, entry 4 t + lambda receives, from the physical wave that ran
+ * logical wave lambda (0..3) of tile t, that wave's index in the workgroup and the place of
+ * lambda among the logical waves it runs (§6.1 N:1 logical-to-physical map: expected
+ * lambda mod (block / 64) and lambda div (block / 64)).  Entries of tiles outside the shard
+ * are left untouched.  MIRIAM_EINVAL if owner_wg, owner_iter or count is null, or if only
+ * one of wave_phys and wave_slot is.
  */
 int miriam_elastic_launch_traced(const miriam_op *op, int64_t shard_begin, int64_t shard_len,
                                  int grid, int block, void *stream,
-                                 int32_t *owner_wg, int32_t *owner_iter, int32_t *count);
+                                 int32_t *owner_wg, int32_t *owner_iter, int32_t *count,
+                                 int32_t *wave_phys, int32_t *wave_slot);
+
+/* Split-K ops (miriam_op_info.ksplit > 1) count the slices that have arrived at each output
+ * tile, and the last one to arrive reduces them and resets the count; a pass that covers the
+ * whole tile space leaves every count at zero.  After a pass that did not (abandoned, or ended
+ * by a failed launch), queue this on the stream of that pass before the next pass over the op:
+ * it clears the counts in stream order (asynchronous).  MIRIAM_OK and nothing queued for ops
+ * without split K; MIRIAM_EHIP if the clear cannot be queued.  The coordinator does this itself
+ * for the ops of a request that a failed launch ends. */
+int miriam_op_reset_counters(const miriam_op *op, void *stream);
 
 /* Release the operator.  MIRIAM_EBUSY if a submitted task that uses it is pending. */
 int miriam_op_destroy(miriam_op *op);
@@ -326,6 +343,9 @@ typedef struct miriam_config {
                                 only. */
     double whole_margin;     /* whole_when_clear: factor on the estimated time of the queued normal
                                 work plus the request (profiled alone, warm caches); 0 = 2.0 */
+    int32_t fake_fail_launch; /* FAKE backend only: the n-th launch (1-based, counting kernel launches
+                                and captured replays since miriam_init) fails with MIRIAM_EHIP, ending
+                                its request with that status; 0 = none (tests of the failure path) */
 } miriam_config;
 
 typedef struct miriam_completion {
@@ -355,6 +375,9 @@ typedef struct miriam_stats {
     int64_t barrier_groups;   /* IB: kernel groups issued behind an inter-stream barrier */
     int64_t whole_clear_launches; /* normal requests launched whole before a known release
                                      (whole_when_clear) */
+    int64_t failed_requests;  /* requests ended by a failed launch (completion status < 0) */
+    int64_t failed_pass_resets; /* ops of those requests whose split-K arrival counters were cleared
+                                   in stream order after the failure (every op of the request's task) */
 } miriam_stats;
 
 /* Start the coordinator (creates its streams and its dispatcher thread). */

@@ -15,6 +15,9 @@
  *     GEMM is Y[m][n] = sum_k X[m][k] * W[n][k].
  *   - Every value is a double; callers widen fp32/fp16/bf16 inputs exactly.
  *   - Functions return 0 on success and a negative number on bad arguments.
+ *   - The convolution and the matrix products may spread their output elements over
+ *     host threads (OpenMP, or_set_threads); each element is still computed by one
+ *     thread with the loop order written below, so results do not depend on the count.
  *
  * Pins: every function here is checked by tests against closed forms, brute
  * force on tiny inputs, worked values, invariants, or an independent library
@@ -22,6 +25,7 @@
  * fixed by the paper; the predicate itself is pinned by hand cases).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -306,6 +310,7 @@ int or_conv2d(const double *x, int64_t N, int64_t H, int64_t W, int64_t C,
     int64_t Wo = (W + 2 * pad - KW) / stride + 1;
     if (Ho < 1 || Wo < 1) return -1;
     int64_t cg = C / groups, kg = K / groups;
+#pragma omp parallel for collapse(3) schedule(static)
     for (int64_t n = 0; n < N; n++)
         for (int64_t p = 0; p < Ho; p++)
             for (int64_t q = 0; q < Wo; q++)
@@ -333,6 +338,7 @@ int or_conv2d(const double *x, int64_t N, int64_t H, int64_t W, int64_t C,
 /* Fully connected layer / matrix product: Y[m][n] = sum_k X[m][k] * W[n][k]. */
 int or_gemm_nt(const double *X, const double *Wt, int64_t M, int64_t N, int64_t K, double *Y)
 {
+#pragma omp parallel for collapse(2) schedule(static)
     for (int64_t m = 0; m < M; m++)
         for (int64_t n = 0; n < N; n++) {
             double s = 0.0;
@@ -345,6 +351,7 @@ int or_gemm_nt(const double *X, const double *Wt, int64_t M, int64_t N, int64_t 
 /* Matrix product with the right operand stored K x N: Y[m][n] = sum_k X[m][k] * B[k][n]. */
 int or_gemm_nn(const double *X, const double *B, int64_t M, int64_t N, int64_t K, double *Y)
 {
+#pragma omp parallel for collapse(2) schedule(static)
     for (int64_t m = 0; m < M; m++)
         for (int64_t n = 0; n < N; n++) {
             double s = 0.0;
@@ -475,4 +482,12 @@ int or_layernorm_rows(const double *x, const double *res, int64_t rows, int64_t 
     }
     free(v);
     return 0;
+}
+
+/* Host threads for the convolution and the matrix products (n >= 1); returns the count now in
+ * force.  n = 0 only reports it. */
+int or_set_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
 }

@@ -32,7 +32,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(
-            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math",
+            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math", "-fopenmp",
              "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
@@ -55,7 +55,14 @@ _INT = ctypes.POINTER(ctypes.c_int)
 i64 = ctypes.c_int64
 
 
+def set_threads(n: int = 0) -> int:
+    """Host threads of the convolution and matrix products (0: report only)."""
+    return int(lib().or_set_threads(int(n)))
+
+
 def _declare(L):
+    L.or_set_threads.argtypes = [ctypes.c_int]
+    L.or_set_threads.restype = ctypes.c_int
     L.or_dichotomy.argtypes = [i64, _I64, ctypes.c_int]
     L.or_balanced_split.argtypes = [i64, i64, _I64, _I64]
     L.or_wg_rank.argtypes = [i64, i64, i64]

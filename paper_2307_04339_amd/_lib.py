@@ -83,7 +83,7 @@ class Config(ctypes.Structure):
         ("graph_chunk", ctypes.c_int32), ("arm_lead_us", ctypes.c_double),
         ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
         ("be_cu_reserve", ctypes.c_int32), ("whole_when_clear", ctypes.c_int32),
-        ("whole_margin", ctypes.c_double),
+        ("whole_margin", ctypes.c_double), ("fake_fail_launch", ctypes.c_int32),
     ]
 
 
@@ -113,6 +113,7 @@ class Stats(ctypes.Structure):
         ("graph_launches", ctypes.c_int64), ("warm_launches", ctypes.c_int64),
         ("armed_releases", ctypes.c_int64), ("segment_launches", ctypes.c_int64),
         ("barrier_groups", ctypes.c_int64), ("whole_clear_launches", ctypes.c_int64),
+        ("failed_requests", ctypes.c_int64), ("failed_pass_resets", ctypes.c_int64),
     ]
 
 
@@ -129,8 +130,9 @@ SIGNATURES = {
     "miriam_op_create": ([ctypes.POINTER(OpDesc), ctypes.POINTER(_P)], _INT),
     "miriam_op_query": ([_P, ctypes.POINTER(OpInfo)], _INT),
     "miriam_elastic_launch": ([_P, _I64, _I64, _INT, _INT, _P], _INT),
-    "miriam_elastic_launch_traced": ([_P, _I64, _I64, _INT, _INT, _P, _P, _P, _P], _INT),
+    "miriam_elastic_launch_traced": ([_P, _I64, _I64, _INT, _INT, _P, _P, _P, _P, _P, _P], _INT),
     "miriam_op_destroy": ([_P], _INT),
+    "miriam_op_reset_counters": ([_P, _P], _INT),
     "miriam_plan_dichotomy": ([_I64, _I64P, _INT], _INT),
     "miriam_plan_split": ([_I64, _I64, _I64P, _I64P], _INT),
     "miriam_plan_wg_rank": ([_I64, _I64, _I64], _I64),

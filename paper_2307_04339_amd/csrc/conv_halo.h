@@ -246,6 +246,7 @@ __global__ __launch_bounds__(kWave * P, (P == 4 ? 2 : 1)) void halo_kernel(Igemm
             for (int sl = 0; sl < SL; ++sl) {
                 const int lam = (rd * SL + sl) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
+                trace_wave(sh, t, lam, pw, rd * SL + sl);
 #pragma unroll
                 for (int jn = 0; jn < BN; ++jn) {
                     const int col = wn * (TN / 2) + jn * MS + lane % MS;

@@ -25,8 +25,9 @@
 // multiple of 16 the last step's upper half is zero on both operands.
 //
 // Elastic block: a physical block of P waves runs logical wave lambda on wave
-// lambda mod P.  P = 2 runs both row halves of one channel half (same weights) at once;
-// P = 1 runs the channel halves in two rounds, reloading the weights per round.  Each
+// lambda mod P, as its (lambda div P)-th logical wave.  P = 2 runs both row halves of one
+// channel half (same weights) at once; P = 1 runs the four logical waves in four rounds,
+// loading the weights of each round's channel half.  Each
 // output element sees the same MFMA sequence in every configuration, so results are
 // bit-identical for every shard plan, grid and physical block.
 #pragma once
@@ -57,7 +58,7 @@ struct RwKernel {
     static constexpr int KTOT = KS * KS * C;
     static constexpr int NS = (KTOT + 15) / 16;            // MFMA k-steps of 16
     static constexpr int LW = kLogicalWaves / P;
-    static constexpr int SL = P == 4 ? 1 : 2;              // logical waves held at once
+    static constexpr int SL = P == 2 ? 2 : 1;              // logical waves held at once
     static constexpr int ROUNDS = LW / SL;
     static constexpr int LDC = TN + 4;                     // staged fp32 row (residual epilogue)
     static constexpr int LDY = TN + 8;                     // staged output row in elements
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
     auto load_affine = [&](uint32_t nt) {
 #pragma unroll
         for (int rd = 0; rd < ROUNDS; ++rd) {
-            const int wn = P == 1 ? rd : wn_mine;
+            const int wn = P == 1 ? (rd & 1) : wn_mine;
             const int64_t col = 64 * (int64_t)nt + 32 * wn + xl;
             chan_affine(a.epi, col < a.Nc ? col : 0, esc[rd], esh[rd]);
         }
@@ -236,13 +237,15 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
 #pragma unroll
         for (int rd = 0; rd < ROUNDS; ++rd) {
             acc_t acc[SL][2];
-            const int wn = P == 1 ? rd : wn_mine;
+            // logical wave lambda = (rd SL + sl) P + pw owns tile rows 2 wm, 2 wm + 1 and channel
+            // half wn, with wm = lambda div 2 and wn = lambda mod 2
+            const int wn = P == 1 ? (rd & 1) : wn_mine;
             if constexpr (P == 1) load_weights(bw, ntile, wn);
             // operand base of block i of slot sl: patch pixel (tile row y, column xl) + this lane's half
             const char *abase[SL][2];
 #pragma unroll
             for (int sl = 0; sl < SL; ++sl) {
-                const int wm = P == 4 ? (pw >> 1) : sl;
+                const int wm = P == 4 ? (pw >> 1) : (P == 2 ? sl : (rd >> 1));
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int y = 2 * wm + i;
@@ -293,11 +296,14 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
             // type, otherwise it is staged as fp32 (tile row y, column x -> staged row y * TW + x)
             if constexpr (K_::OVERLAY) __syncthreads();  // every wave is done reading this patch
             const int col = 32 * wn + xl;
+#pragma unroll
+            for (int sl = 0; sl < SL; ++sl)
+                trace_wave(sh, t, 2 * (P == 4 ? (pw >> 1) : (P == 2 ? sl : (rd >> 1))) + wn, pw, rd * SL + sl);
             auto stage1 = [&](auto actc) {
                 constexpr int ACT = decltype(actc)::value;
 #pragma unroll
                 for (int sl = 0; sl < SL; ++sl) {
-                    const int wm = P == 4 ? (pw >> 1) : sl;
+                    const int wm = P == 4 ? (pw >> 1) : (P == 2 ? sl : (rd >> 1));
 #pragma unroll
                     for (int i = 0; i < 2; ++i) {
                         // element e of the block sits at tile column x = 8 (e / 4) + 4 hx + e % 4

@@ -29,6 +29,7 @@
 #include <mutex>
 #include <new>
 #include <queue>
+#include <shared_mutex>
 #include <sys/prctl.h>
 #include <thread>
 #include <vector>
@@ -81,6 +82,9 @@ struct Backend {
         return MIRIAM_ESTATE;
     }
     virtual void open_gates(uint64_t seq) { (void)seq; }
+    // Clear, in the order of `stream`, the split-K arrival counters of `op` after a pass over it
+    // that may have stopped part-way (a failed launch ended its request).
+    virtual int reset_op(const miriam_op *op, int stream) = 0;
     // Make later work on `stream` wait, on the device, for recorded event `ev`.
     virtual int wait_event(int stream, int ev) {
         (void)stream; (void)ev;
@@ -174,7 +178,7 @@ struct HipBackend : Backend {
         for (size_t i = i0; i < i1; ++i) {
             const miriam_op *op = ops[i];
             const int grid = op_full_grid(op);
-            if (op_launch(op, 0, op->T, grid, 256, cap, nullptr, nullptr, nullptr) != MIRIAM_OK) {
+            if (op_launch(op, 0, op->T, grid, 256, cap) != MIRIAM_OK) {
                 ok = false;
                 break;
             }
@@ -200,7 +204,7 @@ struct HipBackend : Backend {
         return MIRIAM_OK;
     }
     int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) override {
-        return op_launch(op, b, l, grid, block, streams[stream], nullptr, nullptr, nullptr);
+        return op_launch(op, b, l, grid, block, streams[stream]);
     }
     int record(int stream) override {
         int id;
@@ -243,11 +247,11 @@ struct HipBackend : Backend {
             return -1.0;
         }
         double best = -1.0;
-        if (op_launch(op, b, l, grid, block, prof, nullptr, nullptr, nullptr) == MIRIAM_OK &&
+        if (op_launch(op, b, l, grid, block, prof) == MIRIAM_OK &&
             hipStreamSynchronize(prof) == hipSuccess) {
             for (int r = 0; r < reps; ++r) {
                 (void)hipEventRecord(e0, prof);
-                if (op_launch(op, b, l, grid, block, prof, nullptr, nullptr, nullptr) != MIRIAM_OK) break;
+                if (op_launch(op, b, l, grid, block, prof) != MIRIAM_OK) break;
                 (void)hipEventRecord(e1, prof);
                 if (hipEventSynchronize(e1) != hipSuccess) break;
                 float ms = 0.0f;
@@ -273,7 +277,7 @@ struct HipBackend : Backend {
         for (int r = 0; r < reps + 1; ++r) {
             (void)hipEventRecord(e0, prof);
             bool ok = true;
-            for (int i = 0; i < n && ok; ++i) ok = op_launch(op, 0, 1, 1, 256, prof, nullptr, nullptr, nullptr) == MIRIAM_OK;
+            for (int i = 0; i < n && ok; ++i) ok = op_launch(op, 0, 1, 1, 256, prof) == MIRIAM_OK;
             (void)hipEventRecord(e1, prof);
             if (!ok || hipEventSynchronize(e1) != hipSuccess) break;
             float ms = 0.0f;
@@ -285,6 +289,7 @@ struct HipBackend : Backend {
         (void)hipEventDestroy(e1);
         return best;
     }
+    int reset_op(const miriam_op *op, int stream) override { return op_reset_counters(op, streams[stream]); }
     void stop() override {
         open_gates(UINT64_MAX);
         for (hipStream_t s : streams) (void)hipStreamSynchronize(s);
@@ -311,6 +316,13 @@ struct HipBackend : Backend {
 struct FakeBackend : Backend {
     int n_cu = 8, slots = 2;
     double tile_ns = 1000.0, launch_ns = 2000.0;
+    int64_t fail_at = 0;   // this launch (1-based, launches and captured replays) fails; 0 = none
+    int64_t n_launch = 0;
+    bool injected() {
+        if (++n_launch != fail_at) return false;
+        set_error("injected launch failure (simulated device)");
+        return true;
+    }
     std::vector<int64_t> busy_until;
     std::vector<int64_t> ev_time;
     std::vector<int> free_ev;
@@ -330,6 +342,7 @@ struct FakeBackend : Backend {
             set_error("fake launch: bad shard");
             return MIRIAM_ERANGE;
         }
+        if (injected()) return MIRIAM_EHIP;
         const int64_t now = mono_ns();
         const int64_t st = std::max(now, busy_until[stream]);
         busy_until[stream] = st + duration(op, l, grid);
@@ -368,6 +381,7 @@ struct FakeBackend : Backend {
         return u;
     }
     int launch_captured(Captured *unit, int stream) override {
+        if (injected()) return MIRIAM_EHIP;
         int64_t st = std::max(mono_ns(), busy_until[stream]);
         for (const miriam_op *op : static_cast<FakeUnit *>(unit)->ops) st += duration(op, op->T, op_full_grid(op));
         busy_until[stream] = st;
@@ -377,6 +391,7 @@ struct FakeBackend : Backend {
         busy_until[stream] = std::max(std::max(busy_until[stream], mono_ns()), release_ns);
         return MIRIAM_OK;
     }
+    int reset_op(const miriam_op *, int) override { return MIRIAM_OK; }
     void stop() override {}
 };
 
@@ -507,7 +522,9 @@ struct Coord {
 };
 
 Coord *g = nullptr;
-std::mutex g_life;  // serialises init / shutdown
+// Lifetime of g: init, shutdown and task creation hold it exclusively; submit, poll, drain,
+// stats and the launch log hold it shared, so they never see g deleted under them.
+std::shared_mutex g_life;
 
 int64_t eq2_limit(int n_cu, int64_t n_rt) { return miriam_plan_eq2_grid_limit(n_cu, n_rt); }
 
@@ -585,6 +602,23 @@ void finish(Coord &c, Req *r) {
     c.cv_done.notify_all();
 }
 
+// A launch of request r failed on `stream`: the request ends with that error.  The pass over
+// the op it was on may have stopped part-way, leaving split-K arrival counters non-zero, so
+// the counters of every op of its task are cleared in stream order, before any later launch
+// on the stream (a later request's pass then reduces the right slices).
+void fail_request(Coord &c, Req *r, int status, int stream) {
+    if (r->status == MIRIAM_OK) {
+        std::lock_guard<std::mutex> lk(c.stat_mu);
+        c.stats.failed_requests++;
+    }
+    r->status = status;
+    int64_t n = 0;
+    for (const miriam_op *op : r->task->ops)
+        if (c.be->reset_op(op, stream) == MIRIAM_OK) ++n;
+    std::lock_guard<std::mutex> lk(c.stat_mu);
+    c.stats.failed_pass_resets += n;
+}
+
 // Launch every op of a request unsharded (grid = T, block 256) on `stream`: one replay of
 // the task's captured sequence where there is one (one host call and one completion event
 // instead of one launch and one event per op), else op by op.
@@ -599,7 +633,7 @@ void launch_whole(Coord &c, Req *r, int stream) {
         for (size_t k = 0; k < t->graphs.size() && rc == MIRIAM_OK; ++k) rc = c.be->launch_captured(t->graphs[k], stream);
         int ev = rc == MIRIAM_OK ? c.be->record(stream) : rc;
         if (ev < 0) {
-            r->status = ev;
+            fail_request(c, r, ev, stream);
         } else {
             const double total = t->end_us.empty() ? 0.0 : t->end_us.back();
             r->t_start = now;
@@ -626,7 +660,7 @@ void launch_whole(Coord &c, Req *r, int stream) {
         const int grid = op_full_grid(op);
         int rc = issue(c, r, (int)i, 0, op->T, grid, 256, stream, false, 0);
         if (rc != MIRIAM_OK) {
-            r->status = rc;
+            fail_request(c, r, rc, stream);
             break;
         }
     }
@@ -936,7 +970,7 @@ bool pump_normal(Coord &c, int s) {
             }
             any = true;
             if (rc != MIRIAM_OK) {
-                r->status = rc;
+                fail_request(c, r, rc, s);
                 r->launched_all = true;
                 seal(c, r, s);
                 continue;
@@ -966,7 +1000,7 @@ bool pump_normal(Coord &c, int s) {
         }
         any = true;
         if (rc != MIRIAM_OK) {
-            r->status = rc;
+            fail_request(c, r, rc, s);
             r->launched_all = true;
             seal(c, r, s);
             continue;
@@ -1044,9 +1078,10 @@ bool pump_ib(Coord &c) {
             rc = issue(c, r, oi, 0, op->T, op_full_grid(op), 256, s, false, 0, t->prof[oi].t_unsh_us, last);
         }
         if (rc != MIRIAM_OK) {
-            r->status = rc;
+            fail_request(c, r, rc, s);
             r->op = t->ops.size();
             r->launched_all = true;
+            seal(c, r, s);  // its earlier kernels carry no event: retire them with one
             continue;
         }
         r->op++;
@@ -1363,7 +1398,7 @@ int miriam_gate_check(void *stream, int64_t limit_us, int64_t open_after_us, dou
 }
 
 int miriam_init(const miriam_config *cfg) {
-    std::lock_guard<std::mutex> life(g_life);
+    std::unique_lock<std::shared_mutex> life(g_life);
     if (g) return estate("already initialised");
     if (!cfg) {
         set_error("null config");
@@ -1376,7 +1411,8 @@ int miriam_init(const miriam_config *cfg) {
         cfg->graphs > 1 || cfg->release_guard < 0 || cfg->release_guard > 1 ||
         cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
         cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0 ||
-        cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1 || !(cfg->whole_margin >= 0.0)) {
+        cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1 || !(cfg->whole_margin >= 0.0) ||
+        cfg->fake_fail_launch < 0) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -1408,6 +1444,7 @@ int miriam_init(const miriam_config *cfg) {
         f->slots = cfg->fake_slots_per_cu > 0 ? cfg->fake_slots_per_cu : 2;
         f->tile_ns = cfg->fake_tile_ns > 0 ? cfg->fake_tile_ns : 1000.0;
         f->launch_ns = cfg->fake_launch_ns >= 0 ? cfg->fake_launch_ns : 2000.0;
+        f->fail_at = cfg->fake_fail_launch;
         c->n_cu = f->n_cu;
         c->l_threads = 2048;
         c->be = f;
@@ -1440,7 +1477,7 @@ int miriam_task_create(miriam_op *const *ops, int n_ops, miriam_task **out) {
             set_error("null op in task");
             return MIRIAM_EINVAL;
         }
-    std::lock_guard<std::mutex> life(g_life);
+    std::unique_lock<std::shared_mutex> life(g_life);
     if (!g) return estate("coordinator not initialised");
     miriam_task *t = new (std::nothrow) miriam_task();
     if (!t) {
@@ -1481,7 +1518,7 @@ int miriam_submit(miriam_task *task, int criticality, int64_t release_ns, int64_
         set_error("bad submit arguments");
         return MIRIAM_EINVAL;
     }
-    std::lock_guard<std::mutex> life(g_life);
+    std::shared_lock<std::shared_mutex> life(g_life);
     if (!g) return estate("coordinator not initialised");
     Req *r = new (std::nothrow) Req();
     if (!r) {
@@ -1519,6 +1556,7 @@ int miriam_poll(miriam_completion *out, int max_out) {
         set_error("bad poll arguments");
         return MIRIAM_EINVAL;
     }
+    std::shared_lock<std::shared_mutex> life(g_life);
     Coord *c = g;
     if (!c) return estate("coordinator not initialised");
     std::lock_guard<std::mutex> lk(c->mu);
@@ -1531,6 +1569,7 @@ int miriam_poll(miriam_completion *out, int max_out) {
 }
 
 int miriam_drain(int64_t timeout_ms) {
+    std::shared_lock<std::shared_mutex> life(g_life);
     Coord *c = g;
     if (!c) return estate("coordinator not initialised");
     std::unique_lock<std::mutex> lk(c->mu);
@@ -1548,6 +1587,7 @@ int miriam_stats_get(miriam_stats *out) {
         set_error("null output");
         return MIRIAM_EINVAL;
     }
+    std::shared_lock<std::shared_mutex> life(g_life);
     Coord *c = g;
     if (!c) return estate("coordinator not initialised");
     std::lock_guard<std::mutex> lk(c->stat_mu);
@@ -1560,6 +1600,7 @@ int miriam_launch_log(miriam_launch_record *out, int max_out) {
         set_error("bad arguments");
         return MIRIAM_EINVAL;
     }
+    std::shared_lock<std::shared_mutex> life(g_life);
     Coord *c = g;
     if (!c) return estate("coordinator not initialised");
     std::lock_guard<std::mutex> lk(c->log_mu);
@@ -1586,7 +1627,7 @@ int miriam_task_destroy(miriam_task *t) {
 }
 
 int miriam_shutdown(void) {
-    std::lock_guard<std::mutex> life(g_life);
+    std::unique_lock<std::shared_mutex> life(g_life);
     Coord *c = g;
     if (!c) return estate("coordinator not initialised");
     {

@@ -50,6 +50,15 @@ __device__ __forceinline__ void trace_tile(const Shard &sh, int64_t t, int iter)
     }
 }
 
+// Record, from the physical wave that runs it, where logical wave `lam` of tile t ran:
+// on physical wave `pw` of the workgroup, as the `slot`-th logical wave that wave runs.
+__device__ __forceinline__ void trace_wave(const Shard &sh, int64_t t, int lam, int pw, int slot) {
+    if (sh.wave_phys != nullptr && (threadIdx.x % kWave) == 0) {
+        sh.wave_phys[4 * t + lam] = pw;
+        sh.wave_slot[4 * t + lam] = slot;
+    }
+}
+
 // ---------------------------------------------------------------- types
 template <class T> struct TypeOps;
 template <> struct TypeOps<float> {

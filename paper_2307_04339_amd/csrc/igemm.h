@@ -325,6 +325,7 @@ __global__ __launch_bounds__(kWave * P) void igemm_kernel(IgemmArgs a, Shard sh)
             for (int s = 0; s < SL; ++s) {
                 const int lam = (rd * SL + s) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
+                trace_wave(sh, t, lam, pw, rd * SL + s);
 #pragma unroll
                 for (int jn = 0; jn < BN; ++jn) {
                     const int col = wn * (TN / 2) + jn * MS + lane % MS;

@@ -372,6 +372,7 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 for (int s = 0; s < SL; ++s) {
                     const int lam = (rd * SL + s) * P + pw;
                     const int wm = lam >> 1, wn = lam & 1;
+                    trace_wave(sh, t, lam, pw, rd * SL + s);
 #pragma unroll
                     for (int i = 0; i < BM; ++i)
 #pragma unroll
@@ -394,6 +395,7 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             for (int s = 0; s < SL; ++s) {
                 const int lam = (rd * SL + s) * P + pw;
                 const int wm = lam >> 1, wn = lam & 1;
+                trace_wave(sh, t, lam, pw, rd * SL + s);
 #pragma unroll
                 for (int jn = 0; jn < BN; ++jn) {
                     const int col = wn * (TN / 2) + jn * MS + lane % MS;

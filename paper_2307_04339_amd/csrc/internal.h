@@ -51,6 +51,7 @@ struct miriam_op {
     std::atomic<int> pending{0};  // submitted requests that still reference the op
     void *work = nullptr;         // split-K partial tiles (device memory owned by the op)
     void *counters = nullptr;     // split-K arrival counters (device memory owned by the op)
+    size_t counters_bytes = 0;
     void *rowtab = nullptr;       // memory-based index table (device memory owned by the op)
 };
 
@@ -62,7 +63,11 @@ inline int op_full_grid(const miriam_op *op) {
 
 // Launch helper used by the public entry points and by the coordinator.
 int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
-              int32_t *owner_wg, int32_t *owner_iter, int32_t *count);
+              int32_t *owner_wg = nullptr, int32_t *owner_iter = nullptr, int32_t *count = nullptr,
+              int32_t *wave_phys = nullptr, int32_t *wave_slot = nullptr);
+
+// Clear the op's split-K arrival counters on `st` (stream-ordered); MIRIAM_OK without split K.
+int op_reset_counters(const miriam_op *op, hipStream_t st);
 
 // Read-only parameter ranges of an op (weights, bias, batch-norm and layer-norm vectors)
 // that every request reads again: up to 3 (pointer, bytes) pairs; returns the count.

@@ -35,13 +35,18 @@ inline uint32_t fastdiv_host(uint32_t n, FastDiv f) {
 }
 
 // Shard description passed to every kernel.  The trace arrays are null except
-// in traced launches, where they record the tile -> (workgroup, iteration) map.
+// in traced launches, where they record the tile -> (workgroup, iteration) map and,
+// when wave_phys is set, the logical wave -> (physical wave, slot) map of every tile:
+// entry 4 t + lambda of wave_phys / wave_slot is written by the physical wave that ran
+// logical wave lambda of tile t (slot = its place among the logical waves that wave runs).
 struct Shard {
     int64_t begin;
     int64_t len;
     int32_t *owner_wg;
     int32_t *owner_iter;
     int32_t *count;
+    int32_t *wave_phys;
+    int32_t *wave_slot;
 };
 
 // Fused epilogue: v = act(BN(acc + bias[c]) + residual).

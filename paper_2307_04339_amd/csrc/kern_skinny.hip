@@ -73,6 +73,7 @@ __global__ __launch_bounds__(kWave * P) void skinny_kernel(IgemmArgs a, Shard sh
         const T *wr = Wt + n * a.ldw;
         for (int s = 0; s < kLogicalWaves / P; ++s) {
             const int lam = s * P + pw;
+            trace_wave(sh, t, lam, pw, s);
             const int64_t kb = sb + lam * kq;
             const int64_t ke = kb + kq < se ? kb + kq : se;
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};

@@ -268,6 +268,7 @@ __global__ __launch_bounds__(kWave * P) void pix_kernel(PixArgs a, Shard sh) {
 #pragma unroll
             for (int s = 0; s < kLogicalWaves / P; ++s) {
                 const int lam = s * P + pw;
+                trace_wave(sh, t, lam, pw, s);
                 const int64_t u = t * kLogicalBlock + lam * kWave + lane;
                 if constexpr (KIND == PIX_DW3) {
                     if (u < a.items) {
@@ -398,7 +399,9 @@ __global__ __launch_bounds__(kWave * P) void row_kernel(RowArgs a, Shard sh) {
     for (int64_t t = sh.begin + rank; t < sh.begin + sh.len; t += G, ++iter) {
         trace_tile(sh, t, iter);
         for (int s = 0; s < kLogicalWaves / P; ++s) {
-            const int64_t row = t * kLogicalWaves + s * P + pw;
+            const int lam = s * P + pw;
+            trace_wave(sh, t, lam, pw, s);
+            const int64_t row = t * kLogicalWaves + lam;
             if (row >= a.rows) continue;
             if constexpr (KIND == ROW_SOFTMAX) softmax_row<T, V>(a, row, lane);
             else layernorm_row<T, V>(a, row, lane);

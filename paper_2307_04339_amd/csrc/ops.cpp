@@ -290,6 +290,7 @@ static int create_igemm(miriam_op *op) {
                 a.ksplit = (int32_t)ks;
                 a.work = static_cast<float *>(op->work);
                 a.counters = static_cast<int32_t *>(op->counters);
+                op->counters_bytes = cbytes;
             } else {
                 (void)hipGetLastError();
                 if (op->work) (void)hipFree(op->work);
@@ -338,6 +339,7 @@ static int create_igemm(miriam_op *op) {
                     a.cps = (int32_t)cps;
                     a.work = static_cast<float *>(op->work);
                     a.counters = static_cast<int32_t *>(op->counters);
+                    op->counters_bytes = cbytes;
                     op->T *= ks;
                 } else {
                     (void)hipGetLastError();
@@ -506,7 +508,7 @@ static int create_row(miriam_op *op) {
 }
 
 int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hipStream_t st,
-              int32_t *owner_wg, int32_t *owner_iter, int32_t *count) {
+              int32_t *owner_wg, int32_t *owner_iter, int32_t *count, int32_t *wave_phys, int32_t *wave_slot) {
     if (!op) return einval("null op");
     if (b < 0 || l < 1 || b + l > op->T || b + l < b) {
         set_error("shard outside the tile space");
@@ -523,7 +525,7 @@ int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hi
     case 256: pi = 2; break;
     default: set_error("block must be 64, 128 or 256"); return MIRIAM_ERANGE;
     }
-    Shard sh{b, l, owner_wg, owner_iter, count};
+    Shard sh{b, l, owner_wg, owner_iter, count, wave_phys, wave_slot};
     void *args[2];
     switch (op->family) {
     case FAM_IGEMM:
@@ -535,6 +537,12 @@ int op_launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, hi
     hipError_t e = hipLaunchKernel(op->kern[pi], dim3(grid), dim3(block), args, 0, st);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return MIRIAM_OK;
+}
+
+int op_reset_counters(const miriam_op *op, hipStream_t st) {
+    if (!op->counters || op->counters_bytes == 0) return MIRIAM_OK;
+    hipError_t e = hipMemsetAsync(op->counters, 0, op->counters_bytes, st);
+    return e == hipSuccess ? MIRIAM_OK : hip_fail(e, "hipMemsetAsync (split-K counters)");
 }
 
 int op_param_ranges(const miriam_op *op, const void *ptr[3], int64_t bytes[3]) {
@@ -674,15 +682,21 @@ int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
 int miriam_elastic_launch(const miriam_op *op, int64_t shard_begin, int64_t shard_len, int grid, int block,
                           void *stream) {
     return op_launch(op, shard_begin, shard_len, grid, block, static_cast<hipStream_t>(stream), nullptr,
-                     nullptr, nullptr);
+                     nullptr, nullptr, nullptr, nullptr);
 }
 
 int miriam_elastic_launch_traced(const miriam_op *op, int64_t shard_begin, int64_t shard_len, int grid,
                                  int block, void *stream, int32_t *owner_wg, int32_t *owner_iter,
-                                 int32_t *count) {
+                                 int32_t *count, int32_t *wave_phys, int32_t *wave_slot) {
     if (!owner_wg || !owner_iter || !count) return einval("trace arrays required");
+    if ((wave_phys == nullptr) != (wave_slot == nullptr)) return einval("wave_phys and wave_slot go together");
     return op_launch(op, shard_begin, shard_len, grid, block, static_cast<hipStream_t>(stream), owner_wg,
-                     owner_iter, count);
+                     owner_iter, count, wave_phys, wave_slot);
+}
+
+int miriam_op_reset_counters(const miriam_op *op, void *stream) {
+    if (!op) return einval("null op");
+    return op_reset_counters(op, static_cast<hipStream_t>(stream));
 }
 
 int miriam_op_destroy(miriam_op *op) {

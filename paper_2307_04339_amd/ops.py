@@ -52,11 +52,20 @@ class ElasticOp:
         L.check(L.load().miriam_elastic_launch(self.handle, begin, length, grid, block,
                                                _stream_handle(stream)), "miriam_elastic_launch")
 
-    def launch_traced(self, begin, length, grid, block, owner_wg, owner_iter, count, stream=None):
+    def launch_traced(self, begin, length, grid, block, owner_wg, owner_iter, count, stream=None,
+                      wave_phys=None, wave_slot=None):
+        def ptr(t):
+            return None if t is None else ctypes.c_void_p(t.data_ptr())
         L.check(L.load().miriam_elastic_launch_traced(
             self.handle, begin, length, grid, block, _stream_handle(stream),
-            ctypes.c_void_p(owner_wg.data_ptr()), ctypes.c_void_p(owner_iter.data_ptr()),
-            ctypes.c_void_p(count.data_ptr())), "miriam_elastic_launch_traced")
+            ptr(owner_wg), ptr(owner_iter), ptr(count), ptr(wave_phys), ptr(wave_slot)),
+            "miriam_elastic_launch_traced")
+
+    def reset_counters(self, stream=None) -> None:
+        """Clear the split-K arrival counters (stream-ordered) after a pass that did not cover
+        the whole tile space."""
+        L.check(L.load().miriam_op_reset_counters(self.handle, _stream_handle(stream)),
+                "miriam_op_reset_counters")
 
     def variant(self, **changes) -> "ElasticOp":
         """A second op over the same tensors, from this op's descriptor with `changes` applied

@@ -178,10 +178,16 @@ def emit(k: Kernel) -> str:
                  f"            [&]() {{{body}}}();\n"
                  f"        }}\n")
     else:
+        # a kernel that synchronises or shares memory: the shared arrays are hoisted to kernel
+        # scope, so every logical block ends at a barrier before the workgroup starts the next
+        # one (its threads would otherwise overwrite shared data that others still read); the
+        # trip count of the shard loop depends on blockIdx.x only, so the barrier is uniform
+        barrier = "            __syncthreads();\n" if k.syncs else ""
         inner = (f"        {{\n"
                  f"            const unsigned __mi_t = threadIdx.x;\n"
                  f"{tid}"
                  f"            [&]() {{{body}}}();\n"
+                 f"{barrier}"
                  f"        }}\n")
     kern = (f"__global__ void {k.name}_elastic({k.params}, miriam_elastic_shard __mi_sh) {{\n"
             f"{shared}"

@@ -382,3 +382,33 @@ def test_whole_requests_launch_only_clear_of_timed_releases(L):
         assert crit_t
     finally:
         co.shutdown()
+
+
+@pytest.mark.parametrize("policy,fail_at", [("elastic", 5), ("elastic", 1), ("sequential", 3),
+                                            ("multistream", 2), ("ib", 4)])
+def test_injected_launch_failure_ends_one_request(L, policy, fail_at):
+    # the simulated device fails its fail_at-th launch: exactly the request that launch belonged
+    # to completes with MIRIAM_EHIP, the counters of its task's ops are cleared once per op, and
+    # every other request, including ones submitted after the failure, completes normally
+    co = _coord(policy=policy, n_be_streams=2, inflight_depth=2, fake_fail_launch=fail_at, profile_reps=0)
+    try:
+        crit = co.task(_net(L, [3, 5, 2]))
+        be = co.task(_net(L, [9, 17, 4, 6]))
+        tickets = [co.submit(crit, True)]
+        tickets += [co.submit(be, False) for _ in range(3)]
+        recs = _collect(co, len(tickets))
+        assert sorted(r.ticket for r in recs) == sorted(tickets)
+        bad = [r for r in recs if r.status != 0]
+        assert len(bad) == 1
+        assert bad[0].status == -3
+        st = co.stats()
+        assert st.failed_requests == 1
+        n_ops = 3 if bad[0].criticality == 1 else 4
+        assert st.failed_pass_resets == n_ops
+        later = [co.submit(be, False), co.submit(crit, True)]
+        recs2 = _collect(co, 2)
+        assert sorted(r.ticket for r in recs2) == sorted(later)
+        assert all(r.status == 0 for r in recs2)
+        assert co.stats().failed_requests == 1
+    finally:
+        co.shutdown()

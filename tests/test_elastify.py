@@ -87,3 +87,24 @@ def test_launchers_check_arguments():
     assert lib.plain_shift_add2d_elastic_launch(nul, nul, 8, 32, 1.0, 2, 3, 0, 7, 1, 256, nul) == -3
     assert lib.plain_shift_add2d_plain_launch(nul, nul, 8, 32, 1.0, 0, 1, nul) == -3
     assert lib.plain_tiled_gemm_plain_launch(nul, nul, nul, 16, 16, 16, 1, 0, nul) == -3
+
+
+def test_synchronising_kernels_end_each_logical_block_at_a_barrier():
+    # the shared arrays of a fixed-block kernel live at kernel scope across the logical blocks
+    # of a shard: each logical block's lambda is followed by a barrier before the next block
+    # reuses them; kernels without barriers or shared memory get none
+    out = elastify.transform(_plain())
+    for k in elastify.parse(_plain()):
+        start = out.index(f"__global__ void {k.name}_elastic(")
+        kern = out[start:out.index('extern "C"', start)]
+        call = kern.index("}();", kern.index("[&]() {"))
+        tail = kern[call + len("}();"):]
+        if k.syncs:
+            assert tail.lstrip().startswith("__syncthreads();"), k.name
+            # the barrier sits inside the shard loop, after the logical block
+            assert tail.index("__syncthreads();") < tail.index("}")
+        else:
+            assert "__syncthreads();" not in tail, k.name
+    ks = {k.name: k for k in elastify.parse(_plain())}
+    assert ks["plain_transpose16"].syncs and ks["plain_tiled_gemm"].syncs
+    assert not ks["plain_bias_relu"].syncs

@@ -284,3 +284,40 @@ def test_launch_errors_do_not_launch(ops):
         op.launch(0, 1, 1, 192)
     torch.cuda.synchronize()
     assert torch.isnan(y.float()).all()  # nothing ran
+
+
+@pytest.mark.parametrize("tile,shape", [(5, (8, 300, 4096)), (2, None)])
+def test_split_k_counters_reset_after_abandoned_pass(ops, orc, tile, shape):
+    # a pass that covers only part of a split-K op's tile space leaves arrival counts behind;
+    # miriam_op_reset_counters clears them in stream order, and the next whole pass reduces the
+    # right slices again (checked against the oracle and bitwise against an untouched pass)
+    dtype = "f16"
+    if tile == 5:
+        M, N, K = shape
+        x, x64 = rand((M, K), dtype, 31)
+        w, w64 = rand((N, K), dtype, 32, -0.05, 0.05)
+        y = empty((M, N), dtype)
+        op = ops.gemm(x, w, y, act="relu", tile=5, ksplit=4)
+        ref = orc.linear(x64, w64, act="relu")
+    else:
+        x, x64 = rand((1, 7, 7, 256), dtype, 33)
+        w, w64 = rand((64, 3, 3, 256), dtype, 34, -0.05, 0.05)
+        y = empty((1, 7, 7, 64), dtype)
+        op = ops.conv2d(x, w, y, stride=1, pad=1, act="relu", tile=2, ksplit=3)
+        ref = orc.conv2d(x64, w64, stride=1, pad=1, act="relu")
+    ks = op.info.ksplit
+    assert ks > 1
+    op.run()
+    torch.cuda.synchronize()
+    good = bits(y)
+    assert rel_err(to_f64(y), ref) <= RTOL[dtype]
+    # abandon a pass after its first slices: every output tile's count is left part-way
+    op.launch(0, op.T // 2 + 1, 7, 256)
+    op.reset_counters()
+    y.fill_(float("nan"))
+    op.run()
+    torch.cuda.synchronize()
+    assert bits(y) == good
+    op.run()
+    torch.cuda.synchronize()
+    assert bits(y) == good

@@ -244,3 +244,23 @@ def test_layernorm_moments_and_torch(orc):
     ref = F.layer_norm(torch.from_numpy(x + r), (n,), torch.from_numpy(gamma),
                        torch.from_numpy(beta), eps=1e-5).numpy()
     np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_thread_count_does_not_change_results(orc):
+    # the convolution and the products spread whole output elements over host threads; each
+    # element keeps its loop order, so the results are bitwise the same for any count
+    rng = np.random.default_rng(5)
+    x = rng.uniform(-1, 1, (2, 9, 11, 24))
+    w = rng.uniform(-1, 1, (10, 3, 3, 24))
+    A = rng.uniform(-1, 1, (37, 53))
+    B = rng.uniform(-1, 1, (41, 53))
+    prev = orc.set_threads()
+    try:
+        outs = []
+        for n in (1, 3):
+            assert orc.set_threads(n) == n
+            outs.append((orc.conv2d_raw(x, w, 2, 1), orc.gemm_nt(A, B), orc.gemm_nn(A, B.T.copy())))
+        for a, b in zip(outs[0], outs[1]):
+            assert np.array_equal(a, b)
+    finally:
+        orc.set_threads(prev)

@@ -145,6 +145,35 @@ def test_wave_map_is_bijection(orc, P):
         assert pairs == [(lam, 0) for lam in range(L)]
 
 
+def test_wave_map_hand_table(orc):
+    # N:1 map of a 4-wave logical block onto P physical waves, written out by hand:
+    # logical wave lam runs on physical wave lam mod P as that wave's (lam div P)-th logical wave
+    table = {
+        1: [(0, 0), (0, 1), (0, 2), (0, 3)],
+        2: [(0, 0), (1, 0), (0, 1), (1, 1)],
+        4: [(0, 0), (1, 0), (2, 0), (3, 0)],
+    }
+    for P, want in table.items():
+        assert [orc.wave_map(4, P, lam) for lam in range(4)] == want, P
+
+
+@pytest.mark.parametrize("P", [1, 2, 4])
+def test_wave_map_from_logical_thread_loop(orc, P):
+    # brute force over threads: a physical block of 64 P threads runs the 256 logical threads
+    # of the logical block in rounds, physical thread tid taking logical thread i * 64 P + tid in
+    # round i; every thread of a logical wave must land on one physical wave in one round, the
+    # pair the oracle gives
+    B = 64 * P
+    where = {}
+    for i in range(256 // B):
+        for tid in range(B):
+            tau = i * B + tid
+            where.setdefault(tau // 64, set()).add((tid // 64, i))
+    for lam in range(4):
+        assert len(where[lam]) == 1
+        assert orc.wave_map(4, P, lam) == next(iter(where[lam]))
+
+
 def test_wave_map_rejects(orc):
     with pytest.raises(ValueError):
         orc.wave_map(4, 3, 0)
