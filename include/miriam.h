@@ -182,6 +182,26 @@ int miriam_device_query(miriam_device_desc *out);
  * function is computation-based (logical ids computed in-kernel). */
 int miriam_op_create(const miriam_op_desc *d, miriam_op **out);
 
+/* Device scratch of ops created by miriam_op_create_noalloc, per GPU: 1 MiB of split-K arrival
+ * counters followed by the fp32 partials. */
+#define MIRIAM_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under stream capture, serving loops,
+ * harnesses that forbid hipMalloc): miriam_op_create without any device allocation.  An op
+ * whose kernels need a workspace (split K, miriam_op_info.ksplit > 1) takes it from a static
+ * device array of MIRIAM_NOALLOC_SCRATCH_BYTES that the library holds on each GPU until the
+ * process ends, shared by every op created this way on that GPU; the arrival counters it uses
+ * are cleared here (a synchronous clear on the null stream).  Launches, queries and
+ * miriam_op_destroy work as for any op.  Passes over two ops created this way on one GPU must
+ * not overlap in time: they race on the shared array.  Errors: as miriam_op_create;
+ * MIRIAM_EINVAL for MIRIAM_INDEX_MEMORY (its table is device memory); MIRIAM_ERANGE when the
+ * caller asks for split K (ksplit > 1) and the workspace exceeds the array (more than 1 MiB of
+ * counters or the rest of the array in partials); a split the library would choose is then
+ * left out instead.  Host memory for the op object is still allocated.
+ */
+int miriam_op_create_noalloc(const miriam_op_desc *d, miriam_op **out);
+
 /* Fill *out with the operator's tile space and resource figures. */
 int miriam_op_query(const miriam_op *op, miriam_op_info *out);
 

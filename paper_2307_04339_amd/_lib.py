@@ -128,6 +128,7 @@ SIGNATURES = {
     "miriam_last_error": ([], ctypes.c_char_p),
     "miriam_device_query": ([ctypes.POINTER(DeviceDesc)], _INT),
     "miriam_op_create": ([ctypes.POINTER(OpDesc), ctypes.POINTER(_P)], _INT),
+    "miriam_op_create_noalloc": ([ctypes.POINTER(OpDesc), ctypes.POINTER(_P)], _INT),
     "miriam_op_query": ([_P, ctypes.POINTER(OpInfo)], _INT),
     "miriam_elastic_launch": ([_P, _I64, _I64, _INT, _INT, _P], _INT),
     "miriam_elastic_launch_traced": ([_P, _I64, _I64, _INT, _INT, _P, _P, _P, _P, _P, _P], _INT),

@@ -52,6 +52,7 @@ struct miriam_op {
     void *work = nullptr;         // split-K partial tiles (device memory owned by the op)
     void *counters = nullptr;     // split-K arrival counters (device memory owned by the op)
     size_t counters_bytes = 0;
+    bool noalloc = false;         // created by miriam_op_create_noalloc: workspace in the device scratch
     void *rowtab = nullptr;       // memory-based index table (device memory owned by the op)
 };
 

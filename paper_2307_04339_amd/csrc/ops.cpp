@@ -5,9 +5,12 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
+
+#include <hip/hip_runtime.h>
 
 #include "internal.h"
 
@@ -130,6 +133,88 @@ static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
     return CFG_32;
 }
 
+// ---------------------------------------------------------- device scratch
+// Split-K workspace of ops created by miriam_op_create_noalloc: a static device array per GPU
+// (held until the process ends), shared by every such op on that GPU.  Host code never uses
+// the array's name as an address: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and kept in g_scratch_ptr.  Layout: the
+// arrival counters of every such op start at offset 0 (a whole pass leaves each count it
+// used at zero, so the region is all zeros between passes whichever op ran last), the fp32
+// partials at kScratchCounters; passes over two such ops must not overlap in time.
+constexpr size_t kScratchBytes = (size_t)MIRIAM_NOALLOC_SCRATCH_BYTES;
+constexpr size_t kScratchCounters = (size_t)1 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch_ptr[kMaxDevices];
+
+static int scratch_ptr(void **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device index beyond the scratch table");
+        return MIRIAM_ERANGE;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e, "hipGetSymbolAddress (scratch)");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MIRIAM_OK;
+}
+
+// Split-K workspace: wbytes of fp32 partials and cbytes of arrival counters, the counters zeroed.
+// Regular ops allocate it; no-alloc ops (op->noalloc) take it from the device scratch.  Returns
+// 1 when placed, 0 when the op runs without split K instead (allocation failed and the split was
+// the library's choice), < 0 on error (the caller asked for the split, `required`).
+static int alloc_workspace(miriam_op *op, size_t wbytes, size_t cbytes, bool required) {
+    if (op->noalloc) {
+        if (cbytes > kScratchCounters || wbytes > kScratchBytes - kScratchCounters) {
+            if (!required) return 0;
+            set_error("split-K workspace exceeds the no-alloc device scratch (" +
+                      std::to_string((kScratchBytes - kScratchCounters) >> 20) + " MiB of partials, " +
+                      std::to_string(kScratchCounters / 4) + " counters)");
+            return MIRIAM_ERANGE;
+        }
+        void *base = nullptr;
+        int rc = scratch_ptr(&base);
+        if (rc != MIRIAM_OK) return rc;
+        char *b = static_cast<char *>(base);
+        hipError_t e = hipMemsetAsync(b, 0, cbytes, nullptr);
+        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+        if (e != hipSuccess) return hip_fail(e, "clearing the split-K counters in the device scratch");
+        op->counters = b;
+        op->work = b + kScratchCounters;
+        op->counters_bytes = cbytes;
+        return 1;
+    }
+    if (hipMalloc(&op->work, wbytes) == hipSuccess && hipMalloc(&op->counters, cbytes) == hipSuccess &&
+        hipMemset(op->counters, 0, cbytes) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
+        op->counters_bytes = cbytes;
+        return 1;
+    }
+    (void)hipGetLastError();
+    if (op->work) (void)hipFree(op->work);
+    if (op->counters) (void)hipFree(op->counters);
+    (void)hipGetLastError();
+    op->work = op->counters = nullptr;
+    if (!required) return 0;
+    set_error("split-K workspace allocation failed");
+    return MIRIAM_ENOMEM;
+}
+
+// Release an op's device memory (none for no-alloc ops: their workspace is the scratch).
+static void free_device(miriam_op *op) {
+    if (op->noalloc) return;
+    if (op->work) (void)hipFree(op->work);
+    if (op->counters) (void)hipFree(op->counters);
+    if (op->rowtab) (void)hipFree(op->rowtab);
+}
+
 static int create_igemm(miriam_op *op) {
     const miriam_op_desc &d = op->d;
     IgemmArgs &a = op->ig;
@@ -190,6 +275,7 @@ static int create_igemm(miriam_op *op) {
     int rc = check_epi(d, MIRIAM_INDEX_MEMORY);
     if (rc) return rc;
     const bool memidx = (d.flags & MIRIAM_INDEX_MEMORY) != 0;
+    if (memidx && op->noalloc) return einval("memory-based index function: needs a device table (not with no-alloc ops)");
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.Nc);
     if (a.Ho * a.Wo >= (int64_t)INT32_MAX) return einval("contraction: output image too large for 32-bit pixel indexing");
@@ -285,22 +371,12 @@ static int create_igemm(miriam_op *op) {
         if (ks > 1) {
             const size_t wbytes = (size_t)a.nT * (size_t)ks * 16 * 16 * sizeof(float);
             const size_t cbytes = (size_t)a.nT * sizeof(int32_t);
-            if (hipMalloc(&op->work, wbytes) == hipSuccess && hipMalloc(&op->counters, cbytes) == hipSuccess &&
-                hipMemset(op->counters, 0, cbytes) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
+            const int wr = alloc_workspace(op, wbytes, cbytes, d.ksplit > 1);
+            if (wr < 0) return wr;
+            if (wr > 0) {
                 a.ksplit = (int32_t)ks;
                 a.work = static_cast<float *>(op->work);
                 a.counters = static_cast<int32_t *>(op->counters);
-                op->counters_bytes = cbytes;
-            } else {
-                (void)hipGetLastError();
-                if (op->work) (void)hipFree(op->work);
-                if (op->counters) (void)hipFree(op->counters);
-                (void)hipGetLastError();
-                op->work = op->counters = nullptr;
-                if (d.ksplit > 1) {
-                    set_error("split-K workspace allocation failed");
-                    return MIRIAM_ENOMEM;
-                }
             }
         }
         op->T = a.nT * a.ksplit;
@@ -333,24 +409,14 @@ static int create_igemm(miriam_op *op) {
                 ks = cdiv(nch, cps);  // no empty slices
                 const size_t wbytes = (size_t)op->T * (size_t)ks * tile_m_of(cfg) * tile_n_of(cfg) * sizeof(float);
                 const size_t cbytes = (size_t)op->T * sizeof(int32_t);
-                if (hipMalloc(&op->work, wbytes) == hipSuccess && hipMalloc(&op->counters, cbytes) == hipSuccess &&
-                    hipMemset(op->counters, 0, cbytes) == hipSuccess && hipDeviceSynchronize() == hipSuccess) {
+                const int wr = alloc_workspace(op, wbytes, cbytes, d.ksplit > 1);
+                if (wr < 0) return wr;
+                if (wr > 0) {
                     a.ksplit = (int32_t)ks;
                     a.cps = (int32_t)cps;
                     a.work = static_cast<float *>(op->work);
                     a.counters = static_cast<int32_t *>(op->counters);
-                    op->counters_bytes = cbytes;
                     op->T *= ks;
-                } else {
-                    (void)hipGetLastError();
-                    if (op->work) (void)hipFree(op->work);
-                    if (op->counters) (void)hipFree(op->counters);
-                    (void)hipGetLastError();
-                    op->work = op->counters = nullptr;
-                    if (d.ksplit > 1) {
-                        set_error("split-K workspace allocation failed");
-                        return MIRIAM_ENOMEM;
-                    }
                 }
             }
         }
@@ -603,7 +669,7 @@ int miriam_device_query(miriam_device_desc *out) {
     return MIRIAM_OK;
 }
 
-int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
+static int op_create(const miriam_op_desc *d, miriam_op **out, bool noalloc) {
     if (!d || !out) return einval("null argument");
     *out = nullptr;
     if (d->dtype < MIRIAM_F32 || d->dtype > MIRIAM_BF16) return einval("unknown dtype");
@@ -614,6 +680,7 @@ int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
         return MIRIAM_ENOMEM;
     }
     op->d = *d;
+    op->noalloc = noalloc;
     int rc;
     switch (d->kind) {
     case MIRIAM_OP_CONV2D:
@@ -643,9 +710,7 @@ int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
         rc = einval("unknown op kind");
     }
     if (rc != MIRIAM_OK) {
-        if (op->work) (void)hipFree(op->work);
-        if (op->counters) (void)hipFree(op->counters);
-        if (op->rowtab) (void)hipFree(op->rowtab);
+        free_device(op);
         delete op;
         return rc;
     }
@@ -653,6 +718,10 @@ int miriam_op_create(const miriam_op_desc *d, miriam_op **out) {
     *out = op;
     return MIRIAM_OK;
 }
+
+int miriam_op_create(const miriam_op_desc *d, miriam_op **out) { return op_create(d, out, false); }
+
+int miriam_op_create_noalloc(const miriam_op_desc *d, miriam_op **out) { return op_create(d, out, true); }
 
 int miriam_op_query(const miriam_op *op, miriam_op_info *out) {
     if (!op || !out) return einval("null argument");
@@ -705,9 +774,7 @@ int miriam_op_destroy(miriam_op *op) {
         set_error("op referenced by a pending request");
         return MIRIAM_EBUSY;
     }
-    if (op->work) (void)hipFree(op->work);
-    if (op->counters) (void)hipFree(op->counters);
-    if (op->rowtab) (void)hipFree(op->rowtab);
+    free_device(op);
     delete op;
     return MIRIAM_OK;
 }
