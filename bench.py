@@ -1,16 +1,18 @@
 #!/usr/bin/env python3
 """Miriam co-run benchmark on one MI355X.
 
-Default workload (two-task co-run, fp16): the critical task is a ResNet-18-shaped
-CNN at batch 1 released every 20 ms; the best-effort task is a VGG-16-shaped CNN
-at batch 8 run closed-loop on 224x224 inputs.  Inputs and weights are seeded
-synthetic tensors resident in HBM before timing starts.
+Main line (the workload of `value`): the two-task co-run in fp16 whose critical task is a
+ResNet-18-shaped CNN at batch 1 released every 20 ms, next to a VGG-16-shaped CNN at batch 8
+run closed-loop on 224x224 inputs as best-effort work.  Inputs and weights are seeded synthetic
+tensors resident in HBM before timing starts.
 
-Phases: (1) per-kernel timing of the best-effort network with HIP events (the
-roofline object for its dominant kernel and the elastic-shard overhead of that
-kernel); (2) critical task alone (solo); (3) the Sequential baseline; (4) Miriam
-(elastic policy).  A "step" is one critical release period of the co-run; W
-warm-up periods are run first, then exactly K timed periods.
+One step is a batch of critical release periods (--periods-per-step, 25): W warm-up steps, then
+exactly K timed steps, per co-run phase.  Phases: per-kernel timing of the main workload's
+networks (roofline of its dominant kernel, elastic-shard overhead and its launch / persistent
+decomposition), the single fp32 elastic convolution, the ResNet-18 b1 per-kernel roofline with
+seeded shard plans, then the co-run phases (critical task alone, Sequential, Multi-stream, the
+inter-stream-barrier baseline, Miriam under the paper's fill rule and under the hold-back rule),
+the other two co-run workloads as sub-lines, and the CPU oracle baseline.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -245,42 +247,198 @@ def transformed_overhead(reps, flush):
     return out
 
 
-def shard_overhead(layer, reps, flush, n_cu, lib):
-    import ctypes
+def launch_gap_us(reps=5, n=32):
+    """Extra time of one more back-to-back launch on one stream: n launches of a one-tile
+    elementwise op over 8 values against one, per launch (the t_launch of the Eq. (5) launch
+    term); minimum over reps."""
     import torch
-    op = layer.op
-    T = op.T
-    cap = max(1, op.info.max_wg_per_cu[2])
-
-    def timed(plan):
-        # median over the repetitions: a single host-side stall between two shard launches
-        # would otherwise dominate a 20-sample mean
+    from paper_2307_04339_amd import ops
+    x = torch.zeros((1, 8), dtype=torch.float16, device="cuda")
+    y = torch.empty_like(x)
+    op = ops.bn_act(x, y, 1, 8, act="relu")
+    best = None
+    for _ in range(reps):
         ts = []
-        for _ in range(reps):
-            flush()
+        for k in (1, n):
+            torch.cuda.synchronize()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
-            for (b, l, g, bl) in plan:
-                op.launch(b, l, g, bl)
+            for _ in range(k):
+                op.launch(0, 1, 1, 256)
             e1.record()
             e1.synchronize()
             ts.append(e0.elapsed_time(e1))
-        return 1000.0 * float(np.median(ts))
+        g = 1000.0 * (ts[1] - ts[0]) / (n - 1)
+        best = g if best is None else min(best, g)
+    return best
 
-    base = timed([(0, T, int(op.info.full_grid), 256)])
-    res = {"unsharded_us": round(base, 2)}
+
+def _median_us(run, reps, flush=None):
+    """Median over reps of the time between events around run() on torch's current stream (the
+    stream every launch here goes to); flush() before each when given."""
+    import torch
+    ts = []
+    for _ in range(reps):
+        if flush is not None:
+            flush()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return 1000.0 * float(np.median(ts)), 1000.0 * float(np.mean(ts))
+
+
+def _plan(lib, T, n):
+    import ctypes
+    b = (ctypes.c_int64 * n)()
+    ln = (ctypes.c_int64 * n)()
+    lib.miriam_plan_split(T, n, b, ln)
+    return [(int(b[j]), int(ln[j])) for j in range(n)]
+
+
+def shard_overhead(layer, reps, flush, n_cu, lib, gap_us):
+    """Unsharded time of the op and of its balanced 1/2/4/8-shard plans run back to back on one
+    stream (each shard a persistent grid of its length, up to the resident capacity, block 256),
+    medians over cold-cache repetitions.  The overhead t_plan / t_unsharded - 1 is split as in
+    Eq. (5): the launch term LO_blk = (n - 1) t_launch (t_launch: the back-to-back launch gap of
+    a one-tile kernel) and the rest, LO_pt, the persistent shards' own cost (rounds a shard leaves
+    under-filled, its prologue and its tail)."""
+    op = layer.op
+    T = op.T
+    cap = max(1, op.info.max_wg_per_cu[2])
+    base, _ = _median_us(lambda: op.launch(0, T, int(op.info.full_grid), 256), reps, flush)
+    res = {"unsharded_us": round(base, 2), "launch_gap_us": round(gap_us, 2), "tiles": T}
     for n in (1, 2, 4, 8):
         if n > T:
             continue
-        b = (ctypes.c_int64 * n)()
-        ln = (ctypes.c_int64 * n)()
-        lib.miriam_plan_split(T, n, b, ln)
-        plan = [(b[j], ln[j], int(min(ln[j], n_cu * cap)), 256) for j in range(n)]
-        t = timed(plan)
+        plan = [(b, l, int(min(l, n_cu * cap)), 256) for (b, l) in _plan(lib, T, n)]
+        t, _ = _median_us(lambda: [op.launch(b, l, g, bl) for (b, l, g, bl) in plan], reps, flush)
+        lo_blk = (n - 1) * gap_us
         res[f"shards{n}_us"] = round(t, 2)
         res[f"shards{n}_overhead"] = round(t / base - 1.0, 4)
+        res[f"shards{n}_lo_blk_us"] = round(lo_blk, 2)
+        res[f"shards{n}_lo_pt_us"] = round(t - base - lo_blk, 2)
     return res
+
+
+def config1_phase(reps, n_cu, lib, gap_us):
+    """The single elastic fp32 convolution: x 1x56x56x64 and w 64x64x3x3 ~ U[-1, 1] (seeds 0 and
+    1), bias ~ U[-1, 1] (seed 2), stride 1, pad 1, ReLU.  Its 1.75 MB working set stays in the
+    caches, so launches are timed warm, back to back: the mean of 200 launches between two
+    events, and the median of single launches between events.  Then every plan n in {1, 2, 4, 8}
+    x block {64, 128, 256} x forward / reverse shard order (persistent grids), each checked
+    bitwise against the unsharded output."""
+    import torch
+    from paper_2307_04339_amd import ops, synth
+    xs, _ = synth.storage_tensor((1, 56, 56, 64), "f32", seed=0)
+    ws, _ = synth.storage_tensor((64, 3, 3, 64), "f32", seed=1)
+    bs = np.random.default_rng(2).uniform(-1, 1, 64).astype(np.float32)
+    x, w, bias = (torch.from_numpy(a).cuda() for a in (xs, ws, bs))
+    y = torch.empty((1, 56, 56, 64), dtype=torch.float32, device="cuda")
+    op = ops.conv2d(x, w, y, stride=1, pad=1, bias=bias, act="relu")
+    T = op.T
+    full = int(op.info.full_grid)
+    for _ in range(50):
+        op.launch(0, T, full, 256)
+    torch.cuda.synchronize()
+    ref = y.clone()
+    nb = 200
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(nb):
+        op.launch(0, T, full, 256)
+    e1.record()
+    e1.synchronize()
+    mean_b2b = 1000.0 * e0.elapsed_time(e1) / nb
+    med_single, _ = _median_us(lambda: op.launch(0, T, full, 256), reps)
+    flops = op.info.flops
+    out = {"workload": "conv 1x56x56x64 * 64x64x3x3 fp32, bias + ReLU", "tiles": T,
+           "tile": [op.info.tile_m, op.info.tile_n], "flops": flops,
+           "unsharded_us_back_to_back": round(mean_b2b, 3), "unsharded_us_single_median": round(med_single, 3),
+           "tflops": round(flops / (mean_b2b * 1e-6) / 1e12, 2)}
+    out["frac_fp32_peak"] = round(out["tflops"] / PEAK_TFLOPS["f32"], 4)
+    plans = {}
+    bitwise = True
+    for n in (1, 2, 4, 8):
+        shards = _plan(lib, T, n)
+        for block in (64, 128, 256):
+            cap = max(1, op.info.max_wg_per_cu[{64: 0, 128: 1, 256: 2}[block]])
+            for order in ("fwd", "rev"):
+                seq = shards if order == "fwd" else shards[::-1]
+                plan = [(b, l, int(min(l, n_cu * cap)), block) for (b, l) in seq]
+                run = lambda: [op.launch(b, l, g, bl) for (b, l, g, bl) in plan]
+                y.fill_(float("nan"))
+                run()
+                torch.cuda.synchronize()
+                bitwise = bitwise and torch.equal(y.view(torch.int32), ref.view(torch.int32))
+                e0.record()
+                for _ in range(nb):
+                    run()
+                e1.record()
+                e1.synchronize()
+                t = 1000.0 * e0.elapsed_time(e1) / nb
+                lo_blk = (n - 1) * gap_us
+                plans[f"n{n}_b{block}_{order}"] = {"us": round(t, 3), "overhead": round(t / mean_b2b - 1.0, 4),
+                                                   "lo_blk_us": round(lo_blk, 3),
+                                                   "lo_pt_us": round(t - mean_b2b - lo_blk, 3)}
+    out["launch_gap_us"] = round(gap_us, 3)
+    out["plans"] = plans
+    out["bitwise_identical_all_plans"] = bool(bitwise)
+    ovs = [v["overhead"] for v in plans.values()]
+    out["overhead_max"] = round(max(ovs), 4)
+    out["overhead_by_shards_b256_fwd"] = {n: plans[f"n{n}_b256_fwd"]["overhead"] for n in (1, 2, 4, 8)}
+    return out
+
+
+def config2_phase(reps, flush, dtype="f16", seed=5):
+    """ResNet-18 b1 (fp16): every kernel unsharded with cold caches (roofline per kernel), then
+    with a seeded shard plan per layer (n in {1, 2, 3, 4, 8}, block in {64, 128, 256}, forward or
+    reverse order, persistent grids) and the network's outputs compared bitwise with the
+    unsharded forward pass."""
+    import torch
+    from paper_2307_04339_amd import models
+    from paper_2307_04339_amd import _lib as L
+    lib = L.load()
+    net = models.resnet18(batch=1, dtype=dtype)
+    net.forward()
+    torch.cuda.synchronize()
+    ref = [l.t["y"].clone() for l in net.layers]
+    rng = np.random.default_rng(seed)
+    rows = []
+    plans = {}
+    for i, layer in enumerate(net.layers):
+        op = layer.op
+        T = op.T
+        n = int(min(T, rng.choice([1, 2, 3, 4, 8])))
+        block = int(rng.choice([64, 128, 256]))
+        shards = _plan(lib, T, n)
+        if rng.random() < 0.5:
+            shards = shards[::-1]
+        cap = max(1, op.info.max_wg_per_cu[{64: 0, 128: 1, 256: 2}[block]])
+        plans[i] = [(b, l, int(min(l, 256 * cap)), block) for (b, l) in shards]
+        t_un, _ = _median_us(lambda: op.run(), reps, flush)
+        t_pl, _ = _median_us(lambda: [op.launch(b, l, g, bl) for (b, l, g, bl) in plans[i]], reps, flush)
+        flops = op.info.flops
+        if layer.kind == "conv" and layer.params.get("logical_c"):
+            flops *= layer.params["logical_c"] / layer.t["x"].shape[-1]
+        k = dict(name=layer.name, us=t_un, flops=flops, bytes=op.info.bytes, tiles=T)
+        rf = roofline_of(k, dtype)
+        rows.append(dict(name=layer.name, tiles=T, path=int(op.info.path), unsharded_us=round(t_un, 2),
+                         bound=rf["bound"], achieved=rf["achieved"], unit=rf["unit"], frac=rf["frac"],
+                         plan=f"{n}x{block}", sharded_us=round(t_pl, 2), shard_overhead=round(t_pl / t_un - 1.0, 4)))
+    for l in net.layers:
+        l.t["y"].fill_(float("nan"))
+    net.forward(plans=plans)
+    torch.cuda.synchronize()
+    same = all(torch.equal(l.t["y"].view(torch.int16), r.view(torch.int16)) for l, r in zip(net.layers, ref))
+    tot = sum(r["unsharded_us"] for r in rows)
+    return {"workload": "resnet18 b1 fp16", "kernels": rows, "kernel_sum_us": round(tot, 2),
+            "sharded_sum_us": round(sum(r["sharded_us"] for r in rows), 2),
+            "flops": net.flops(), "bitwise_identical_sharded_vs_unsharded": bool(same)}
 
 
 # ----------------------------------------------------------------- co-run
@@ -346,8 +504,8 @@ def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, se
     for j, n in enumerate(be_nets if with_be else []):
         cnt = sum(1 for (jj, te) in be_done if jj == j and t_win0 <= te <= t_win1)
         per_task.append(dict(net=n.name, batch=n.batch, req_s=cnt / win_s, img_s=cnt * n.batch / win_s))
-    return dict(policy=policy, p50_ms=pct(lat_ms, 50), p99_ms=pct(lat_ms, 99), mean_ms=float(np.mean(lat_ms)),
-                max_ms=float(np.max(lat_ms)), window_s=win_s, be=per_task,
+    return dict(policy=policy, releases=len(lat_ms), p50_ms=pct(lat_ms, 50), p99_ms=pct(lat_ms, 99),
+                mean_ms=float(np.mean(lat_ms)), max_ms=float(np.max(lat_ms)), window_s=win_s, be=per_task,
                 be_img_s=sum(p["img_s"] for p in per_task), be_req_s=sum(p["req_s"] for p in per_task),
                 crit_req_s=n_steps / win_s, launches=st.launches,
                 decision_us=st.decision_ns_total / max(1, st.decisions) / 1000.0,
@@ -355,59 +513,139 @@ def run_phase(policy, crit_net, be_nets, n_warm, n_steps, period_ms, arrival, se
 
 
 # ------------------------------------------------------------ cpu baseline
-def cpu_baseline(net_name, kw, budget_macs=1.5e9, seed=0):
-    """Oracle time of one best-effort inference image, from a bounded sample: each
-    convolution computes sampled output pixels (all channels), scaled by the pixel
-    count; pooling and FC layers run in full for one image."""
-    from oracle import oracle as orc
+def _host_info():
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model,
+            "affinity_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+
+
+def _oracle_layers(net_name, kw):
+    """Layer shapes of one inference (batch 1) of a workload network, as oracle calls."""
     from paper_2307_04339_amd import models  # shapes only
-    rng = np.random.default_rng(seed)
-    shapes = []
-    # replay the network's layer shapes on the host (batch 1)
-    import torch  # noqa: F401
     net = models.BUILDERS[net_name](**dict(kw, batch=1))
+    out = []
     for l in net.layers:
-        x = l.t.get("x")
-        xs = None if x is None else tuple(x.shape)
-        ws = None if l.t.get("w") is None else tuple(l.t["w"].shape)
-        if l.kind == "conv" and l.params.get("logical_c"):
-            lc = l.params["logical_c"]  # the oracle convolves the logical channels only
-            xs = xs[:-1] + (lc,)
-            ws = ws[:-1] + (lc,)
-        shapes.append((l.kind, xs, l.t["y"].shape, ws, dict(l.params)))
+        p = dict(l.params)
+        shp = {k: (tuple(v.shape) if hasattr(v, "shape") else None) for k, v in l.t.items()}
+        if l.kind == "conv" and p.get("logical_c"):
+            lc = p["logical_c"]  # the oracle convolves the logical channels only
+            shp["x"] = shp["x"][:-1] + (lc,)
+            shp["w"] = shp["w"][:-1] + (lc,)
+        out.append((l.kind, shp, p))
     del net
-    total = 0.0
-    t_start = time.time()
-    for kind, xs, ys, ws, p in shapes:
+    return out
+
+
+def _oracle_inference(layers, rng):
+    """Run every layer of one inference through the oracle on random inputs of its shape;
+    returns the oracle time in seconds (input generation excluded)."""
+    from oracle import oracle as orc
+    tot = 0.0
+    for kind, shp, p in layers:
         if kind == "conv":
-            N, H, W, C = xs
-            K, KH, KW, _ = ws
-            _, Ho, Wo, _ = ys
-            npx = Ho * Wo
-            per = K * KH * KW * C
-            s = int(max(1, min(npx, budget_macs // per)))
-            crops = rng.uniform(-1, 1, (s, KH, KW, C))
-            w = rng.uniform(-1, 1, ws)
+            x = rng.uniform(-1, 1, shp["x"])
+            w = rng.uniform(-1, 1, shp["w"])
+            K = shp["w"][0]
             t0 = time.perf_counter()
-            orc.conv2d(crops, w, stride=1, pad=0, act=p["act"])
-            total += (time.perf_counter() - t0) * npx / s
+            y = orc.conv2d_raw(x, w, stride=p["stride"], pad=p["pad"])
+            orc.epilogue(y, bias=np.zeros(K), bn=(np.ones(K), np.zeros(K), np.zeros(K), np.ones(K)),
+                         residual=y if shp.get("residual") else None, act=p["act"])
+        elif kind == "dwconv":
+            x = rng.uniform(-1, 1, shp["x"])
+            C = shp["x"][-1]
+            w = rng.uniform(-1, 1, (C, 3, 3, 1))
+            t0 = time.perf_counter()
+            y = orc.conv2d_raw(x, w, stride=p["stride"], pad=p["pad"], groups=C)
+            orc.epilogue(y, bn=(np.ones(C), np.zeros(C), np.zeros(C), np.ones(C)), act=p["act"])
         elif kind in ("maxpool", "avgpool"):
-            x = rng.uniform(-1, 1, xs)
+            x = rng.uniform(-1, 1, shp["x"])
             fn = orc.maxpool if kind == "maxpool" else orc.avgpool
             t0 = time.perf_counter()
             fn(x, p["k"], p["stride"], p["pad"])
-            total += time.perf_counter() - t0
         elif kind == "gemm":
-            x = rng.uniform(-1, 1, (1, xs[1]))
-            w = rng.uniform(-1, 1, ws)
+            x = rng.uniform(-1, 1, shp["x"])
+            w = rng.uniform(-1, 1, shp["w"])
             t0 = time.perf_counter()
-            orc.linear(x, w, act=p["act"])
-            total += time.perf_counter() - t0
+            orc.linear(x, w, bias=np.zeros(shp["w"][0]), residual=np.zeros((shp["x"][0], shp["w"][0]))
+                       if shp.get("residual") else None, act=p["act"])
+        elif kind == "bgemm":
+            B, H, S, D = p["B"], p["H"], p["S"], p["D"]
+            q = rng.uniform(-1, 1, (S, D))
+            pm = rng.uniform(0, 1, (S, S))
+            t0 = time.perf_counter()
+            for _ in range(B * H):
+                if p["which"] == "qk":
+                    orc.gemm_nt(q, q)
+                else:
+                    orc.gemm_nn(pm, q)
+        elif kind == "softmax":
+            n = shp["x"][-1]
+            x = rng.uniform(-1, 1, (int(np.prod(shp["x"])) // n, n))
+            t0 = time.perf_counter()
+            orc.softmax_rows(x, scale=p["scale"])
+        elif kind == "layernorm":
+            x = rng.uniform(-1, 1, shp["x"])
+            n = shp["x"][-1]
+            t0 = time.perf_counter()
+            orc.layernorm_rows(x, np.ones(n), np.zeros(n), eps=p["eps"])
+        else:
+            raise ValueError(kind)
+        tot += time.perf_counter() - t0
+    return tot
+
+
+def cpu_baseline(dtype, seed=0):
+    """The CPU oracle (plain C loops in double precision) timed on this host: one inference of
+    each workload network (batch 1, every layer in full, random inputs of the layer shapes) and
+    the single fp32 convolution (median of 5), single-threaded and on every host core the
+    process may use (OpenMP over output elements in the convolution and the products; pooling,
+    epilogues, softmax and LayerNorm stay on one thread).  `value` is VGG-16 images per second
+    on all cores."""
+    from oracle import oracle as orc
+    rng = np.random.default_rng(seed)
+    host = _host_info()
+    all_cores = host["affinity_cpus"] or host["nproc"] or 1
+    omp = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    if omp > 0:
+        all_cores = min(all_cores, omp)
+    nets = [("vgg16", {}), ("resnet18", {}), ("mobilenetv2", {}), ("encoder", {"seq": 128})]
+    shapes = {n: _oracle_layers(n, dict(kw, dtype=dtype)) for n, kw in nets}
+    prev = orc.set_threads()
+    res = {}
+    t_start = time.time()
+    try:
+        x = rng.uniform(-1, 1, (1, 56, 56, 64))
+        w = rng.uniform(-1, 1, (64, 3, 3, 64))
+        for label, th in (("1_thread", 1), (f"{all_cores}_threads", all_cores)):
+            used = orc.set_threads(th)
+            ts = []
+            for _ in range(5):
+                t0 = time.perf_counter()
+                orc.conv2d(x, w, stride=1, pad=1, bias=np.zeros(64), act="relu")
+                ts.append(time.perf_counter() - t0)
+            c1 = float(np.median(ts))
+            per = {n: _oracle_inference(shapes[n], rng) for n, _ in nets}
+            res[label] = {"threads": used, "config1_conv_ms": round(1000 * c1, 2),
+                          "config1_conv_gflops": round(231211008 / c1 / 1e9, 2),
+                          "ms_per_inference": {n: round(1000 * t, 1) for n, t in per.items()}}
+    finally:
+        orc.set_threads(prev)
     wall = time.time() - t_start
-    return dict(value=round(1.0 / total, 5), unit="img/s", cores=1, kind="oracle",
-                sample=f"one {net_name} image: <= {budget_macs:.0e} MACs of sampled output pixels per "
-                       f"convolution (scaled by pixel count), pooling and FC in full; "
-                       f"{wall:.1f} s of CPU work, single thread")
+    top = res[f"{all_cores}_threads"]
+    vgg_ms = top["ms_per_inference"]["vgg16"]
+    return dict(value=round(1000.0 / vgg_ms, 4), unit="img/s", cores=top["threads"], kind="oracle",
+                sample=(f"one VGG-16 image (batch 1, every layer in full, fp64) on {top['threads']} host threads; "
+                        f"also ResNet-18, MobileNetV2 and the encoder (seq 128) per image and the single fp32 "
+                        f"convolution, on 1 and {top['threads']} threads; {wall:.1f} s of CPU work"),
+                host=host, runs=res)
 
 
 def profile_op(args, cfg):
@@ -446,23 +684,157 @@ def profile_op(args, cfg):
 
 
 # ------------------------------------------------------------------- main
+PHASE_POLICY = {"solo": "elastic", "elastic_pause": "elastic", "multistream_cu": "multistream"}
+# co-run phases of the main workload and of the sub-line workloads
+MAIN_PHASES = ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause")
+SUB_PHASES = ("solo", "sequential", "elastic", "elastic_pause")
+
+
+def coordinator_cfg(args, cfg):
+    guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
+    warm = args.warm_critical if args.warm_critical >= 0 else guard
+    arm = args.arm_lead_us if args.arm_lead_us >= 0 else (500.0 if guard else 0.0)
+    whole = args.whole_when_clear if args.whole_when_clear >= 0 else guard
+    inflight_us = args.inflight_us if args.inflight_us >= 0 else 100.0
+    event_us = args.event_us if args.event_us >= 0 else inflight_us / 3.0
+    return dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=inflight_us, event_us=event_us,
+                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
+                warm_critical=warm, arm_lead_us=arm, segments=args.segments, whole_when_clear=whole,
+                whole_margin=args.whole_margin)
+
+
+def build_workload(cfg, n_inst):
+    from paper_2307_04339_amd import models
+    dtype = cfg["dtype"]
+    cname, ckw = cfg["crit"]
+    crit_net = models.BUILDERS[cname](dtype=dtype, **ckw)
+    be_nets = [models.BUILDERS[n](dtype=dtype, **kw) for (n, kw) in cfg["be"]]
+    be_tasks = []  # every instance of every best-effort network
+    for first, (n, kw) in zip(be_nets, cfg["be"]):
+        be_tasks.append(first)
+        for _ in range(n_inst - 1):
+            be_tasks.append(models.BUILDERS[n](dtype=dtype, share=first, **kw))
+    crit_net.forward()
+    for n in be_tasks:
+        n.forward()
+    return crit_net, be_nets, be_tasks
+
+
+def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
+    """Run the co-run phases of one workload; returns (runs, summary)."""
+    runs = {}
+    for ph in MAIN_PHASES:
+        if ph not in phases:
+            continue
+        log(f"  phase {ph} ...")
+        policy = PHASE_POLICY.get(ph, ph)
+        pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else dict(ccfg)
+        if ph == "multistream_cu":
+            pcfg = dict(ccfg, be_cu_reserve=args.cu_reserve)
+        runs[ph] = run_phase(policy, crit_net, be_tasks, args.warmup * pps, args.steps * pps, cfg["period_ms"],
+                             cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
+        r = runs[ph]
+        log(f"    p50 {r['p50_ms']:.3f} ms  p99 {r['p99_ms']:.3f} ms  be {r['be_img_s']:.1f} img/s "
+            f"launches {r['launches']} releases {r['releases']}")
+    main_name = next((n for n in ("elastic_pause", "elastic") if n in runs), None)
+    main_run = runs[main_name] if main_name else next(iter(runs.values()), None)
+    summary = {}
+    foreknowledge = bool(ccfg["release_guard"] or ccfg["arm_lead_us"] > 0 or ccfg["whole_when_clear"])
+    if "solo" in runs and main_run:
+        solo = runs["solo"]
+        crit = {"policy": main_name, "busy_policy": 1 if main_name == "elastic_pause" else 0,
+                "release_foreknowledge": foreknowledge,
+                "releases": main_run["releases"],
+                "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
+                "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
+                "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
+        for other in ("elastic", "multistream", "multistream_cu", "ib", "sequential"):
+            if other in runs and other != main_name:
+                crit[f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
+        summary["critical"] = crit
+    if "sequential" in runs and main_run:
+        seq = runs["sequential"]
+        be = {"policy": main_name,
+              "elastic_img_s": round(main_run["be_img_s"], 2), "sequential_img_s": round(seq["be_img_s"], 2),
+              "speedup_vs_sequential": round(main_run["be_img_s"] / max(1e-9, seq["be_img_s"]), 3),
+              "sequential_p99_ms": round(seq["p99_ms"], 4)}
+        summary["best_effort"] = be
+    if "elastic" in runs and "solo" in runs:
+        el = runs["elastic"]
+        pr = {"busy_policy": 0, "release_foreknowledge": foreknowledge,
+              "p50_ms": round(el["p50_ms"], 4), "p99_ms": round(el["p99_ms"], 4),
+              "p99_overhead": round(el["p99_ms"] / runs["solo"]["p99_ms"] - 1.0, 4),
+              "be_img_s": round(el["be_img_s"], 2)}
+        if "sequential" in runs:
+            pr["speedup_vs_sequential"] = round(el["be_img_s"] / max(1e-9, runs["sequential"]["be_img_s"]), 3)
+        summary["paper_rule"] = pr
+    phases_out = {ph: {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()} for ph, r in runs.items()}
+    return runs, main_name, main_run, summary, phases_out
+
+
+def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
+    """Per-kernel timing of the workload's networks; the dominant kernel's roofline, shard
+    overhead (with its Eq. (5) decomposition), index functions and transformed kernels."""
+    dtype = cfg["dtype"]
+    flush = CacheFlush()
+    table = []
+    for n in be_nets + [crit_net]:
+        for k in time_layers(n, args.reps, flush):
+            k["net"] = n.name
+            table.append(k)
+    dom_net = be_nets[0]
+    dom = max((k for k in table if k["net"] == dom_net.name), key=lambda k: k["us"])
+    kern = roofline_of(dom, dtype)
+    kern["kernel"] = f"{dom_net.name}.{dom['name']}"
+    kern["launch_us"] = round(dom["us"], 2)
+    kern["flops_per_launch"] = dom["flops"]
+    kern["bytes_per_launch"] = dom["bytes"]
+    layer = next(l for l in dom_net.layers if l.name == dom["name"])
+    kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
+    kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
+    gap = launch_gap_us()
+    result["launch_gap_us"] = round(gap, 3)
+    log("  shard overhead ...")
+    ovh = {"kernel": kern["kernel"], **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load(), gap)}
+    # the memory-bound kernel with the most time, next to the contraction
+    result["elastic_overhead"] = ovh
+    log("  index functions ...")
+    result["index_function"] = {"net": dom_net.name, "layers": index_function_cost(dom_net, args.reps, flush, L)}
+    log("  transformed kernels ...")
+    result["transformed_kernels"] = transformed_overhead(args.reps, flush)
+    result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
+                              **{kk: vv for kk, vv in roofline_of(k, dtype).items()
+                                 if kk in ("bound", "achieved", "unit", "frac")})
+                         for k in sorted(table, key=lambda k: -k["us"])[:16]]
+    result["be_solo_ms_per_request"] = {n.name: round(sum(k["us"] for k in table if k["net"] == n.name) / 1000, 3)
+                                        for n in be_nets}
+    result["crit_kernel_sum_ms"] = round(sum(k["us"] for k in table if k["net"] == crit_net.name) / 1000, 3)
+    del flush
+    return kern
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--periods-per-step", type=int, default=25,
+                    help="critical release periods per step: K steps time K x this many releases per phase")
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=sorted(CONFIGS))
+    ap.add_argument("--sub-configs", default="auto",
+                    help="comma-separated other co-run workloads reported as sub-lines ('auto': every other "
+                         "workload; 'none')")
     ap.add_argument("--reps", type=int, default=20, help="repetitions per kernel timing")
     ap.add_argument("--quantum-us", type=float, default=40.0)
     ap.add_argument("--depth", type=int, default=32)
     ap.add_argument("--inflight-us", type=float, default=-1.0,
                     help="normal work kept queued on the GPU (it bounds the wait of an unannounced critical "
-                         "release; 300 measured 2-6%% more best-effort throughput but slower critical kernels "
-                         "next to it); -1: 100")
+                         "release); -1: 100")
     ap.add_argument("--event-us", type=float, default=-1.0,
                     help="estimated normal work between completion events; -1: a third of the in-flight budget")
     ap.add_argument("--busy-policy", type=int, default=0,
-                    help="normal shards next to a running critical kernel: 0 paper rule, 1 none, 2 smallest")
+                    help="normal shards next to a running critical kernel in the 'elastic' phase: 0 paper rule, "
+                         "1 none, 2 smallest ('elastic_pause' always holds back)")
     ap.add_argument("--graphs", type=int, default=1, choices=(0, 1),
                     help="1: whole-request launches replay each task's captured HIP graph")
     ap.add_argument("--release-guard", type=int, default=-1, choices=(-1, 0, 1),
@@ -481,7 +853,9 @@ def main():
                          "buffers), each its own closed-loop task and stream; Sequential still runs one "
                          "request at a time.  0: the workload's default (3 for the two-task co-runs, 1 for "
                          "the four-task mix, whose three networks already give three streams)")
-    ap.add_argument("--phases", default="kernels,solo,sequential,multistream,multistream_cu,ib,elastic,elastic_pause")
+    ap.add_argument("--phases", default="kernels,config1,config2," + ",".join(MAIN_PHASES) + ",sub,cpu",
+                    help="kernels, config1 (single fp32 conv), config2 (ResNet-18 b1 per kernel), the co-run "
+                         "phases " + ", ".join(MAIN_PHASES) + ", sub (other workloads), cpu (oracle baseline)")
     ap.add_argument("--whole-when-clear", type=int, default=-1,
                     help="launch normal requests whole when they end before the next known critical "
                          "release (-1: with the release guard)")
@@ -503,7 +877,6 @@ def main():
 
     import torch
     from paper_2307_04339_amd import _lib as L
-    from paper_2307_04339_amd import models
     from paper_2307_04339_amd.ops import device_info
 
     cfg = CONFIGS[args.config]
@@ -511,89 +884,35 @@ def main():
     if args.profile_op:
         profile_op(args, cfg)
         return
+    pps = max(1, args.periods_per_step)
     dev = device_info()
     log(f"device {dev.arch.decode()} cus={dev.n_cu} config={args.config}")
-    cname, ckw = cfg["crit"]
-    crit_net = models.BUILDERS[cname](dtype=dtype, **ckw)
-    be_nets = [models.BUILDERS[n](dtype=dtype, **kw) for (n, kw) in cfg["be"]]
-    be_tasks = []  # every instance of every best-effort network
-    n_inst = args.be_instances if args.be_instances > 0 else cfg["be_instances"]
-    for first, (n, kw) in zip(be_nets, cfg["be"]):
-        be_tasks.append(first)
-        for _ in range(n_inst - 1):
-            be_tasks.append(models.BUILDERS[n](dtype=dtype, share=first, **kw))
-    crit_net.forward()
-    for n in be_tasks:
-        n.forward()
-    torch.cuda.synchronize()
     phases = set(args.phases.split(","))
-    flush = CacheFlush()
+    n_inst = args.be_instances if args.be_instances > 0 else cfg["be_instances"]
     result = {}
-
     kern = None
-    if "kernels" in phases:
-        log("timing kernels ...")
-        table = []
-        for n in be_nets + [crit_net]:
-            for k in time_layers(n, args.reps, flush):
-                k["net"] = n.name
-                table.append(k)
-        dom_net = be_nets[0]
-        dom = max((k for k in table if k["net"] == dom_net.name), key=lambda k: k["us"])
-        kern = roofline_of(dom, dtype)
-        kern["kernel"] = f"{dom_net.name}.{dom['name']}"
-        kern["launch_us"] = round(dom["us"], 2)
-        kern["flops_per_launch"] = dom["flops"]
-        kern["bytes_per_launch"] = dom["bytes"]
-        layer = next(l for l in dom_net.layers if l.name == dom["name"])
-        kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
-        kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
-        result["elastic_overhead"] = dict(kernel=kern["kernel"],
-                                          **shard_overhead(layer, args.reps, flush, dev.n_cu, L.load()))
-        log("index functions ...")
-        result["index_function"] = {"net": dom_net.name,
-                                    "layers": index_function_cost(dom_net, args.reps, flush, L)}
-        log("transformed kernels ...")
-        result["transformed_kernels"] = transformed_overhead(args.reps, flush)
-        result["kernels"] = [dict(net=k["net"], name=k["name"], us=round(k["us"], 2), tiles=k["tiles"],
-                                  **{kk: vv for kk, vv in roofline_of(k, dtype).items()
-                                     if kk in ("bound", "achieved", "unit", "frac")})
-                             for k in sorted(table, key=lambda k: -k["us"])[:12]]
-        result["be_solo_ms_per_request"] = {n.name: round(sum(k["us"] for k in table if k["net"] == n.name) / 1000, 3)
-                                            for n in be_nets}
-        result["crit_kernel_sum_ms"] = round(sum(k["us"] for k in table if k["net"] == crit_net.name) / 1000, 3)
-    del flush
-    torch.cuda.empty_cache()
+    if phases & ({"kernels"} | set(MAIN_PHASES)):
+        crit_net, be_nets, be_tasks = build_workload(cfg, n_inst)
+        torch.cuda.synchronize()
+        if "kernels" in phases:
+            log("timing kernels ...")
+            kern = kernel_phase(args, cfg, be_nets, crit_net, dev, L, result)
+            torch.cuda.empty_cache()
+    if "config1" in phases:
+        log("single fp32 elastic convolution ...")
+        result["config1"] = config1_phase(200, dev.n_cu, L.load(), launch_gap_us())
+    if "config2" in phases:
+        log("resnet18 b1 per kernel ...")
+        fl = CacheFlush()
+        result["config2"] = config2_phase(args.reps, fl)
+        del fl
+        torch.cuda.empty_cache()
 
-    guard = args.release_guard if args.release_guard >= 0 else int(cfg["arrival"] == "periodic")
-    warm = args.warm_critical if args.warm_critical >= 0 else guard
-    arm = args.arm_lead_us if args.arm_lead_us >= 0 else (500.0 if guard else 0.0)
-    whole = args.whole_when_clear if args.whole_when_clear >= 0 else guard
-    inflight_us = args.inflight_us if args.inflight_us >= 0 else 100.0
-    event_us = args.event_us if args.event_us >= 0 else inflight_us / 3.0
-    ccfg = dict(quantum_us=args.quantum_us, inflight_depth=args.depth, inflight_us=inflight_us, event_us=event_us,
-                busy_policy=args.busy_policy, profile_reps=3, graphs=args.graphs, release_guard=guard,
-                warm_critical=warm, arm_lead_us=arm, segments=args.segments, whole_when_clear=whole,
-                whole_margin=args.whole_margin)
-    runs = {}
-    for ph in ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause"):
-        if ph not in phases:
-            continue
-        log(f"phase {ph} ...")
-        policy = {"solo": "elastic", "elastic_pause": "elastic", "multistream_cu": "multistream"}.get(ph, ph)
-        pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else ccfg
-        if ph == "multistream_cu":
-            pcfg = dict(ccfg, be_cu_reserve=args.cu_reserve)
-        runs[ph] = run_phase(policy, crit_net, be_tasks, args.warmup, args.steps, cfg["period_ms"],
-                             cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
-        r = runs[ph]
-        log(f"  p50 {r['p50_ms']:.3f} ms  p99 {r['p99_ms']:.3f} ms  be {r['be_img_s']:.1f} img/s "
-            f"launches {r['launches']}")
-
-    # main line: Miriam with normal shards held back while a critical kernel runs (the paper's
-    # padding rule is reported beside it as "elastic")
-    main_name = next((n for n in ("elastic_pause", "elastic") if n in runs), None)
-    main_run = runs[main_name] if main_name else next(iter(runs.values()), None)
+    ccfg = coordinator_cfg(args, cfg)
+    main_name, main_run, summary, phases_out = None, None, {}, {}
+    if phases & set(MAIN_PHASES):
+        log(f"co-run {args.config} ...")
+        _, main_name, main_run, summary, phases_out = corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps)
     value = main_run["be_img_s"] if main_run else float("nan")
     out = {
         "metric": METRIC,
@@ -609,42 +928,56 @@ def main():
         "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": args.config,
-                   "critical": f"{cname} b{ckw['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
+                   "critical": f"{cfg['crit'][0]} b{cfg['crit'][1]['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
-                   "be_instances": n_inst,
+                   "be_instances": n_inst, "periods_per_step": pps,
+                   "releases_timed_per_phase": args.steps * pps,
+                   "main_line": "Miriam coordinator, hold-back rule (busy policy 1: no new normal shard while a "
+                                "critical kernel runs)" + (", with the known periodic release times (release "
+                                "guard, cache warming, armed gate, whole requests before the next release)"
+                                if ccfg["release_guard"] else ""),
                    "quantum_us": args.quantum_us, "inflight_depth": args.depth,
-                   "inflight_us": inflight_us, "event_us": round(event_us, 2),
-                   "busy_policy": 1 if main_name == "elastic_pause" else args.busy_policy,
-                   "graphs": args.graphs, "release_guard": guard, "warm_critical": warm,
-                   "arm_lead_us": arm, "segments": args.segments, "whole_when_clear": whole,
+                   "inflight_us": ccfg["inflight_us"], "event_us": round(ccfg["event_us"], 2),
+                   "busy_policy": 1 if main_name == "elastic_pause" else 0,
+                   "graphs": args.graphs, "release_guard": ccfg["release_guard"],
+                   "warm_critical": ccfg["warm_critical"], "arm_lead_us": ccfg["arm_lead_us"],
+                   "segments": args.segments, "whole_when_clear": ccfg["whole_when_clear"],
                    "cu_reserve_multistream_cu": args.cu_reserve},
     }
-    if "solo" in runs and main_run:
-        solo = runs["solo"]
-        out["critical"] = {
-            "policy": main_name,
-            "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
-            "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
-            "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
-        for other in ("elastic", "multistream", "multistream_cu", "ib", "sequential"):
-            if other in runs and other != main_name:
-                out["critical"][f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
-    for ph, r in runs.items():
-        out.setdefault("phases", {})[ph] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
-    if "sequential" in runs and main_run:
-        seq = runs["sequential"]
-        out["best_effort"] = {
-            "policy": main_name,
-            "elastic_img_s": round(main_run["be_img_s"], 2), "sequential_img_s": round(seq["be_img_s"], 2),
-            "speedup_vs_sequential": round(main_run["be_img_s"] / max(1e-9, seq["be_img_s"]), 3),
-            "sequential_p99_ms": round(seq["p99_ms"], 4)}
+    out.update(summary)
+    if phases_out:
+        out["phases"] = phases_out
     if kern:
         out["roofline"] = kern
-    out.update({k: v for k, v in result.items()})
-    if not args.no_cpu_baseline:
-        bname, bkw = cfg["be"][0]
+    out.update(result)
+    if phases & set(MAIN_PHASES):
+        del crit_net, be_nets, be_tasks
+        torch.cuda.empty_cache()
+
+    if "sub" in phases and args.sub_configs != "none":
+        subs = [c for c in sorted(CONFIGS) if c != args.config] if args.sub_configs == "auto" \
+            else [c for c in args.sub_configs.split(",") if c]
+        out["sub_configs"] = {}
+        for name in subs:
+            scfg = CONFIGS[name]
+            log(f"co-run {name} (sub-line) ...")
+            s_inst = scfg["be_instances"]
+            c_net, b_nets, b_tasks = build_workload(scfg, s_inst)
+            torch.cuda.synchronize()
+            s_ccfg = coordinator_cfg(args, scfg)
+            _, s_main, s_run, s_sum, s_ph = corun(args, scfg, set(SUB_PHASES), c_net, b_tasks, s_ccfg, pps)
+            out["sub_configs"][name] = dict(
+                value=round(s_run["be_img_s"], 3), unit="img/s", dtype=scfg["dtype"],
+                critical_task=f"{scfg['crit'][0]} b{scfg['crit'][1]['batch']} {scfg['arrival']} every "
+                              f"{scfg['period_ms']} ms",
+                best_effort_tasks=[f"{n} b{kw['batch']} closed-loop" for n, kw in scfg["be"]], be_instances=s_inst,
+                release_guard=s_ccfg["release_guard"], **s_sum, phases=s_ph)
+            del c_net, b_nets, b_tasks
+            torch.cuda.empty_cache()
+
+    if "cpu" in phases and not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(bname, dict(bkw, dtype=dtype))
+        out["cpu_baseline"] = cpu_baseline(dtype)
     print(json.dumps(out), flush=True)
 
 

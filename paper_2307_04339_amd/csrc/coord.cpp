@@ -265,7 +265,8 @@ struct HipBackend : Backend {
         return best;
     }
     double launch_gap_us(const miriam_op *op, int reps) override {
-        // extra time of n back-to-back one-tile launches over one, per launch
+        // time per launch of n back-to-back empty kernels: the gap one more kernel boundary adds
+        (void)op;
         const int n = 16;
         hipEvent_t e0, e1;
         if (hipEventCreate(&e0) != hipSuccess) return -1.0;
@@ -277,7 +278,7 @@ struct HipBackend : Backend {
         for (int r = 0; r < reps + 1; ++r) {
             (void)hipEventRecord(e0, prof);
             bool ok = true;
-            for (int i = 0; i < n && ok; ++i) ok = op_launch(op, 0, 1, 1, 256, prof) == MIRIAM_OK;
+            for (int i = 0; i < n && ok; ++i) ok = noop_launch(prof) == MIRIAM_OK;
             (void)hipEventRecord(e1, prof);
             if (!ok || hipEventSynchronize(e1) != hipSuccess) break;
             float ms = 0.0f;

@@ -85,6 +85,9 @@ struct WarmRange {
 // threads) on stream `st`; `sink` is a device word the kernel may write (never read back).
 int warm_launch(const WarmRange *table, int n, int grid, int *sink, hipStream_t st);
 
+// An empty one-wave kernel on `st` (launch-gap measurement).
+int noop_launch(hipStream_t st);
+
 // One-wave kernel on `st` that returns once *flag (coherent host memory, device address)
 // reaches `seq` or `limit_ticks` ticks of the device wall clock have passed.
 int gate_launch(const uint64_t *flag, uint64_t seq, uint64_t limit_ticks, hipStream_t st);

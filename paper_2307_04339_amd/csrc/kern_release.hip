@@ -47,6 +47,16 @@ __global__ __launch_bounds__(64) void gate_kernel(const uint64_t *flag, uint64_t
     }
 }
 
+// One empty wave: back-to-back launches of it measure the launch gap between two kernels of
+// one stream (the t_launch of the Eq. (5) launch term).
+__global__ __launch_bounds__(64) void noop_kernel() {}
+
+int noop_launch(hipStream_t st) {
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&noop_kernel), dim3(1), dim3(64), nullptr, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "empty kernel launch");
+    return MIRIAM_OK;
+}
+
 int warm_launch(const WarmRange *table, int n, int grid, int *sink, hipStream_t st) {
     if (n < 1 || grid < 1) return MIRIAM_OK;
     void *args[3] = {&table, &n, &sink};

@@ -320,8 +320,62 @@ __device__ __forceinline__ void st_row_vec(T *p, const float *v) {
     }
 }
 
+// Rows of up to kRowRegs vectors per lane (2048 16-bit or 1024 fp32 values) are read from
+// memory once and kept in registers for every pass; longer rows are read again per pass.
+// Either way each lane visits its elements j = lane V + i 64 V (+ e) in increasing i, so the
+// per-element operations, and the results, are the same.
+constexpr int kRowRegs = 4;
+
+template <class T, int V>
+__device__ void softmax_row_regs(const RowArgs &a, int64_t row, int lane) {
+    const T *xr = static_cast<const T *>(a.x) + row * a.ldx;
+    T *yr = static_cast<T *>(a.y) + row * a.ldy;
+    float v[kRowRegs][V];
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) ld_row_vec<T, V>(xr + j, v[i]);
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) m = fmaxf(m, a.scale * v[i][e]);
+        }
+    }
+    m = wave_max(m);
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                v[i][e] = expf(a.scale * v[i][e] - m);
+                s += v[i][e];
+            }
+        }
+    }
+    s = wave_sum(s);
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[i][e] = v[i][e] / s;
+            st_row_vec<T, V>(yr + j, v[i]);
+        }
+    }
+}
+
 template <class T, int V>
 __device__ void softmax_row(const RowArgs &a, int64_t row, int lane) {
+    if (a.n <= (int64_t)kRowRegs * kWave * V) {
+        softmax_row_regs<T, V>(a, row, lane);
+        return;
+    }
     const T *xr = static_cast<const T *>(a.x) + row * a.ldx;
     T *yr = static_cast<T *>(a.y) + row * a.ldy;
     float m = -INFINITY;
@@ -350,7 +404,62 @@ __device__ void softmax_row(const RowArgs &a, int64_t row, int lane) {
 }
 
 template <class T, int V>
+__device__ void layernorm_row_regs(const RowArgs &a, int64_t row, int lane) {
+    const T *xr = static_cast<const T *>(a.x) + row * a.ldx;
+    const T *rr = static_cast<const T *>(a.res) + row * a.ldx;
+    T *yr = static_cast<T *>(a.y) + row * a.ldy;
+    float v[kRowRegs][V];
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+            ld_row_vec<T, V>(xr + j, v[i]);
+            if (a.has_res) {
+                float r[V];
+                ld_row_vec<T, V>(rr + j, r);
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[i][e] += r[e];
+            }
+        }
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) s += v[i][e];
+        }
+    }
+    const float mean = wave_sum(s) / (float)a.n;
+    float q = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) q += (v[i][e] - mean) * (v[i][e] - mean);
+        }
+    }
+    const float var = wave_sum(q) / (float)a.n;
+    const float rstd = 1.0f / sqrtf(var + a.eps);
+#pragma unroll
+    for (int i = 0; i < kRowRegs; ++i) {
+        const int64_t j = (int64_t)lane * V + (int64_t)i * kWave * V;
+        if (j < a.n) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[i][e] = (v[i][e] - mean) * rstd * a.gamma[j + e] + a.beta[j + e];
+            st_row_vec<T, V>(yr + j, v[i]);
+        }
+    }
+}
+
+template <class T, int V>
 __device__ void layernorm_row(const RowArgs &a, int64_t row, int lane) {
+    if (a.n <= (int64_t)kRowRegs * kWave * V) {
+        layernorm_row_regs<T, V>(a, row, lane);
+        return;
+    }
     const T *xr = static_cast<const T *>(a.x) + row * a.ldx;
     const T *rr = static_cast<const T *>(a.res) + row * a.ldx;
     T *yr = static_cast<T *>(a.y) + row * a.ldy;
