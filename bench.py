@@ -25,6 +25,17 @@ import os
 import sys
 import time
 
+# Hardware queues of this process: one stream per coordinator task (the critical stream and up
+# to three normal streams) plus the profiling stream and the framework's own.  With HIP's
+# default of 4, kernel traces showed two normal streams sharing one queue (their kernels then
+# run in order); 8 gives every stream its own.  Read by the HIP runtime when it starts, so it is
+# raised to at least 8 before torch is imported (a larger setting in the environment is kept).
+try:
+    _hwq = int(os.environ.get("GPU_MAX_HW_QUEUES", "4"))
+except ValueError:
+    _hwq = 4
+os.environ["GPU_MAX_HW_QUEUES"] = str(min(32, max(8, _hwq)))
+
 import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -649,38 +660,46 @@ def cpu_baseline(dtype, seed=0):
 
 
 def profile_op(args, cfg):
-    """One layer's unsharded launch --reps times, then a plain device copy of 256 MiB
-    --reps times (its FETCH_SIZE / WRITE_SIZE calibrate the traffic counters)."""
+    """Each listed layer's unsharded launch --reps times back to back (layers in the order
+    given), then a plain device copy of 256 MiB --reps times, whose FETCH_SIZE / WRITE_SIZE
+    calibrate the traffic counters.  Prints one JSON line per layer and one for the copy."""
     import torch
     from paper_2307_04339_amd import models
-    net_name, layer_name = args.profile_op.split(".", 1)
-    kw = next((dict(k) for (n, k) in [cfg["crit"]] + cfg["be"] if n == net_name), None)
-    if kw is None:
-        raise SystemExit(f"{net_name} is not part of workload {args.config}")
-    net = models.BUILDERS[net_name](dtype=cfg["dtype"], **kw)
-    layer = next(l for l in net.layers if l.name == layer_name)
+    nets = {}
+    targets = []
+    for item in args.profile_op.split(","):
+        net_name, layer_name = item.split(".", 1)
+        kw = next((dict(k) for (n, k) in [cfg["crit"]] + cfg["be"] if n == net_name), None)
+        if kw is None:
+            raise SystemExit(f"{net_name} is not part of workload {args.config}")
+        if net_name not in nets:
+            nets[net_name] = models.BUILDERS[net_name](dtype=cfg["dtype"], **kw)
+            nets[net_name].forward()
+        targets.append((item, next(l for l in nets[net_name].layers if l.name == layer_name)))
     src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     src.fill_(1.0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.reps):
-        layer.op.run()
-    e1.record()
-    e1.synchronize()
-    us = 1000.0 * e0.elapsed_time(e1) / args.reps
+    for item, layer in targets:
+        e0.record()
+        for _ in range(args.reps):
+            layer.op.run()
+        e1.record()
+        e1.synchronize()
+        us = 1000.0 * e0.elapsed_time(e1) / args.reps
+        info = layer.op.info
+        print(json.dumps({"op": item, "reps": args.reps, "avg_us": round(us, 3), "tiles": layer.op.T,
+                          "tile": [info.tile_m, info.tile_n], "path": int(info.path), "grid": int(info.full_grid),
+                          "flops": info.flops, "bytes": info.bytes}), flush=True)
     e0.record()
     for _ in range(args.reps):
         dst.copy_(src)
     e1.record()
     e1.synchronize()
     cus = 1000.0 * e0.elapsed_time(e1) / args.reps
-    info = layer.op.info
-    print(json.dumps({"op": args.profile_op, "reps": args.reps, "avg_us": round(us, 3),
-                      "tiles": layer.op.T, "tile": [info.tile_m, info.tile_n],
-                      "flops": info.flops, "bytes": info.bytes,
-                      "copy_bytes_each_way": src.numel() * 4, "copy_avg_us": round(cus, 3)}), flush=True)
+    print(json.dumps({"op": "copy", "reps": args.reps, "copy_bytes_each_way": src.numel() * 4,
+                      "copy_avg_us": round(cus, 3)}), flush=True)
 
 
 # ------------------------------------------------------------------- main
@@ -864,9 +883,9 @@ def main():
     ap.add_argument("--cu-reserve", type=int, default=64,
                     help="multistream_cu phase: compute units left out of the normal streams' CU mask")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-op", default=None, metavar="NET.LAYER",
-                    help="only launch one layer (unsharded) --reps times, then a 256 MiB device copy "
-                         "--reps times as the counter calibration kernel (for rocprofv3 runs)")
+    ap.add_argument("--profile-op", default=None, metavar="NET.LAYER[,NET.LAYER...]",
+                    help="only launch the listed layers (unsharded) --reps times each, then a 256 MiB device "
+                         "copy --reps times as the counter calibration kernel (for rocprofv3 runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
@@ -927,7 +946,7 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": args.config,
+        "config": {"workload": args.config, "hw_queues": int(os.environ.get("GPU_MAX_HW_QUEUES", "4")),
                    "critical": f"{cfg['crit'][0]} b{cfg['crit'][1]['batch']} {cfg['arrival']} every {cfg['period_ms']} ms",
                    "best_effort": [f"{n} b{kw['batch']} closed-loop" for n, kw in cfg["be"]],
                    "be_instances": n_inst, "periods_per_step": pps,
