@@ -75,9 +75,20 @@ struct DmaKernel {
     static constexpr int STAGE = (TM + TN) * 128;        // bytes per stage
     static constexpr int LDC = TN + 4;
     static constexpr int C_BYTES = TM * LDC * 4;
-    static constexpr int LDS_BYTES = S * STAGE > C_BYTES ? S * STAGE : C_BYTES;
-    // register budget: two resident 4-wave workgroups per CU wherever their LDS fits
-    static constexpr int WAVES_PER_SIMD = (P == 4 && 2 * (LDS_BYTES + 16) <= 160 * 1024) ? 2 : 1;
+    // Split rings: where only two joint stages fit (128 x 128), the A and B operands get rings
+    // of their own in the same 80 KB, three A stages and two B stages.  The weights (B) are
+    // small and stay in L2; the input rows of the taps (A) also come from memory.  An A chunk
+    // is then issued two chunks ahead of its use and a B chunk one (measured on VGG-16 b8
+    // fp16: conv4_x 68 -> 58.5 us, conv2_2 55.4 -> 54.0 us, same bits).
+    static constexpr bool SR = S == 2 && (3 * TM + 2 * TN) * 128 <= 80 * 1024;
+    static constexpr int SA = SR ? 3 : S, SB = SR ? 2 : S;   // A and B stages
+    static constexpr int A_STAGE = TM * 128, B_STAGE = TN * 128;
+    static constexpr int RING_BYTES = SR ? SA * A_STAGE + SB * B_STAGE : S * STAGE;
+    static constexpr int LDS_BYTES = RING_BYTES > C_BYTES ? RING_BYTES : C_BYTES;
+    // register budget: two resident 4-wave workgroups per CU wherever their LDS fits (the split
+    // rings keep no other shared variable, so they may fill exactly half of the CU's LDS)
+    static constexpr int WAVES_PER_SIMD =
+        (P == 4 && 2 * (LDS_BYTES + (SR ? 0 : 16)) <= 160 * 1024) ? 2 : 1;
     static_assert(TM % (8 * P) == 0 && TN % (8 * P) == 0, "load instructions must divide evenly");
     static_assert((S - 2) * LPC < 64, "vmcnt range");
     static_assert(LW % SL == 0, "slots must divide logical waves");
@@ -90,6 +101,7 @@ template <class T, int TM, int TN, int MS, int P, bool UNI, bool MI = false>
 __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_SIMD)) void igemm_dma_kernel(
     IgemmArgs a, Shard sh) {
     typedef DmaKernel<T, TM, TN, MS, P> K_;
+    constexpr bool SR = K_::SR;
     typedef typename K_::MF MF;
     typedef typename MF::op_t op_t;
     typedef typename MF::acc_t acc_t;
@@ -138,9 +150,10 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         const int64_t m0 = (int64_t)mt * TM, n0 = (int64_t)nt * TN;
 
         // memory-based index function: the tile's rows of the host-computed table are staged
-        // in the ring's last stage, which the first DMA into it (after the main loop's first
-        // barrier) only overwrites once every wave has read its entries
-        const int4 *const tab = reinterpret_cast<const int4 *>(smem + (S - 1) * K_::STAGE);
+        // in the (A) ring's last stage, which the first DMA into it (after the main loop's
+        // first barrier) only overwrites once every wave has read its entries
+        const int4 *const tab =
+            reinterpret_cast<const int4 *>(smem + (SR ? (K_::SA - 1) * K_::A_STAGE : (S - 1) * K_::STAGE));
         if constexpr (MI) {
             const int4 *src = reinterpret_cast<const int4 *>(a.rowtab) + m0;
             for (int r = tid; r < TM; r += NT) const_cast<int4 *>(tab)[r] = src[r];
@@ -238,9 +251,17 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 }
             }
 
-            // issue chunk ch into stage st (all lanes issue every instruction)
-            auto issue = [&](int ch, int st) {
-                const uint32_t stage = lds_ring + (uint32_t)(st * K_::STAGE);
+            // LDS byte addresses of chunk ch's A and B stages
+            auto a_stage = [&](int ch) -> uint32_t {
+                return lds_ring + (uint32_t)(SR ? (ch % K_::SA) * K_::A_STAGE : (ch % S) * K_::STAGE);
+            };
+            auto b_stage = [&](int ch) -> uint32_t {
+                return lds_ring + (uint32_t)(SR ? K_::SA * K_::A_STAGE + (ch % K_::SB) * K_::B_STAGE
+                                                : (ch % S) * K_::STAGE + TM * 128);
+            };
+            // issue chunk ch of A (chunks in increasing order; all lanes issue every instruction)
+            auto issue_a = [&](int ch) {
+                const uint32_t stage = a_stage(ch);
                 if constexpr (UNI) {
                     if (retap) {
                         const int64_t toff = (((int64_t)ur * a.W + us) * a.ldx + uc) * (int64_t)sizeof(T);
@@ -257,11 +278,6 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                     for (int j = 0; j < NIA; ++j) {
                         lds_dma16(ap[j], stage + (uint32_t)((8 * (j * P + pw)) * 128));
                         ap[j] += astep[j];
-                    }
-#pragma unroll
-                    for (int j = 0; j < NIB; ++j) {
-                        lds_dma16(bp[j], stage + (uint32_t)((TM + 8 * (j * P + pw)) * 128));
-                        bp[j] += bstep[j];
                     }
                     uc += KT;
                     if (uc == C32) {
@@ -287,17 +303,32 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                         if (++ks[j] == KW32) { ks[j] = 0; ++kr[j]; }
                     }
                 }
+            };
+            // issue chunk ch of B (chunks in increasing order)
+            auto issue_b = [&](int ch) {
+                const uint32_t stage = b_stage(ch);
+                if constexpr (UNI) {
+#pragma unroll
+                    for (int j = 0; j < NIB; ++j) {
+                        lds_dma16(bp[j], stage + (uint32_t)((8 * (j * P + pw)) * 128));
+                        bp[j] += bstep[j];
+                    }
+                    (void)ch;
+                    return;
+                }
                 const int64_t k0 = (int64_t)(c0 + ch) * KT;
 #pragma unroll
                 for (int j = 0; j < NIB; ++j) {
                     const int64_t k = k0 + b_k0[j];
                     const T *src = (b_ok[j] && k < a.K) ? b_base[j] + k : zsrc;
-                    lds_dma16(src, stage + (uint32_t)((TM + 8 * (j * P + pw)) * 128));
+                    lds_dma16(src, stage + (uint32_t)((8 * (j * P + pw)) * 128));
                 }
             };
 
-            auto compute = [&](int st) {
-                const char *stage = smem + st * K_::STAGE;
+            auto compute = [&](int ch) {
+                const char *sta = smem + (SR ? (ch % K_::SA) * K_::A_STAGE : (ch % S) * K_::STAGE);
+                const char *stb = smem + (SR ? K_::SA * K_::A_STAGE + (ch % K_::SB) * K_::B_STAGE
+                                             : (ch % S) * K_::STAGE + TM * 128);
                 constexpr int NK = KT / KSTEP;
                 // read every operand of the chunk first, so LDS latency overlaps the MFMAs
                 op_t aop[NK][SL][BM], bop[NK][SL][BN];
@@ -313,13 +344,13 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                         for (int jn = 0; jn < BN; ++jn) {
                             const int row = wn * (TN / 2) + jn * MS + lane % MS;
                             bop[kk][s][jn] = *reinterpret_cast<const op_t *>(
-                                stage + (TM + row) * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
+                                stb + row * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
                         }
 #pragma unroll
                         for (int i = 0; i < BM; ++i) {
                             const int row = wm * (TM / 2) + i * MS + lane % MS;
                             aop[kk][s][i] = *reinterpret_cast<const op_t *>(
-                                stage + row * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
+                                sta + row * 128 + ((piece ^ ((row >> 1) & 7)) * 16) + within);
                         }
                     }
                 }
@@ -343,26 +374,51 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 }
             };
 
-#pragma unroll
-            for (int st = 0; st < S - 1; ++st)
-                if (st < nsl) issue(st, st);
-            for (int c = 0; c < nsl; ++c) {
-                // chunks issued after c and still allowed in flight: c+1 .. min(c+S-2, nsl-1)
-                const int pending = (nsl - 1 - c) < (S - 2) ? (nsl - 1 - c) : (S - 2);
-                if constexpr (S - 2 >= 2) {
-                    if (pending >= 2) wait_vmcnt<2 * LPC>();
-                    else if (pending == 1) wait_vmcnt<LPC>();
-                    else wait_vmcnt<0>();
-                } else if constexpr (S - 2 == 1) {
-                    if (pending >= 1) wait_vmcnt<LPC>();
-                    else wait_vmcnt<0>();
-                } else {
-                    (void)pending;
-                    wait_vmcnt<0>();
+            if constexpr (SR) {
+                // issue order: A(0), B(0), A(1), then per chunk c (after the barrier) B(c+1), A(c+2).
+                // At the top of chunk c the only load issued after B(c) is A(c+1), and A(c) was
+                // issued before B(c): waiting down to A(c+1)'s instructions completes both.
+                if (nsl > 0) {
+                    issue_a(0);
+                    issue_b(0);
                 }
-                __syncthreads();
-                if (c + S - 1 < nsl) issue(c + S - 1, (c + S - 1) % S);
-                compute(c % S);
+                if (nsl > 1) issue_a(1);
+                for (int c = 0; c < nsl; ++c) {
+                    if (c + 1 < nsl) wait_vmcnt<NIA>();
+                    else wait_vmcnt<0>();
+                    __syncthreads();
+                    if (c + 1 < nsl) issue_b(c + 1);
+                    if (c + 2 < nsl) issue_a(c + 2);
+                    compute(c);
+                }
+            } else {
+#pragma unroll
+                for (int st = 0; st < S - 1; ++st)
+                    if (st < nsl) {
+                        issue_a(st);
+                        issue_b(st);
+                    }
+                for (int c = 0; c < nsl; ++c) {
+                    // chunks issued after c and still allowed in flight: c+1 .. min(c+S-2, nsl-1)
+                    const int pending = (nsl - 1 - c) < (S - 2) ? (nsl - 1 - c) : (S - 2);
+                    if constexpr (S - 2 >= 2) {
+                        if (pending >= 2) wait_vmcnt<2 * LPC>();
+                        else if (pending == 1) wait_vmcnt<LPC>();
+                        else wait_vmcnt<0>();
+                    } else if constexpr (S - 2 == 1) {
+                        if (pending >= 1) wait_vmcnt<LPC>();
+                        else wait_vmcnt<0>();
+                    } else {
+                        (void)pending;
+                        wait_vmcnt<0>();
+                    }
+                    __syncthreads();
+                    if (c + S - 1 < nsl) {
+                        issue_a(c + S - 1);
+                        issue_b(c + S - 1);
+                    }
+                    compute(c);
+                }
             }
             __syncthreads();
 
@@ -468,17 +524,25 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             // The partials were written with agent-scope (device-coherent) stores; waiting for
             // them to complete before the arrival is counted orders them before the count, and
             // the reducer reads them back with agent-scope loads, so no cache-wide fence is needed.
-            __shared__ int s_last;
+            // the arrival flag: a shared word of its own, or with split rings the first word of the
+            // ring, free once the K loop has ended (the split-K path stages no epilogue there)
+            int *s_lastp;
+            if constexpr (SR) {
+                s_lastp = reinterpret_cast<int *>(smem_);
+            } else {
+                __shared__ int s_last;
+                s_lastp = &s_last;
+            }
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
                 const int prev = __hip_atomic_fetch_add(a.counters + otile, 1, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT);
-                s_last = prev == a.ksplit - 1;
-                if (s_last) __hip_atomic_store(a.counters + otile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                *s_lastp = prev == a.ksplit - 1;
+                if (*s_lastp) __hip_atomic_store(a.counters + otile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
-            if (s_last) {
+            if (*s_lastp) {
                 const float *base = a.work + (int64_t)otile * a.ksplit * (TM * TN);
                 constexpr int CVT = TN / VEC;
                 for (int idx = tid; idx < TM * CVT; idx += NT) {
