@@ -703,9 +703,9 @@ def profile_op(args, cfg):
 
 
 # ------------------------------------------------------------------- main
-PHASE_POLICY = {"solo": "elastic", "elastic_pause": "elastic", "multistream_cu": "multistream"}
+PHASE_POLICY = {"solo": "elastic", "elastic_pause": "elastic", "multistream_cu": "multistream", "elastic_cu": "elastic"}
 # co-run phases of the main workload and of the sub-line workloads
-MAIN_PHASES = ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_pause")
+MAIN_PHASES = ("solo", "sequential", "multistream", "multistream_cu", "ib", "elastic", "elastic_cu", "elastic_pause")
 SUB_PHASES = ("solo", "sequential", "elastic", "elastic_pause")
 
 
@@ -748,8 +748,11 @@ def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
         log(f"  phase {ph} ...")
         policy = PHASE_POLICY.get(ph, ph)
         pcfg = dict(ccfg, busy_policy=1) if ph == "elastic_pause" else dict(ccfg)
-        if ph == "multistream_cu":
-            pcfg = dict(ccfg, be_cu_reserve=args.cu_reserve)
+        if ph in ("multistream_cu", "elastic_cu"):
+            # normal streams masked off the top cu_reserve CUs: a spatial share for the critical
+            # stream (which keeps every CU, or only those with --crit-cu-exclusive) next to the
+            # paper's fill rule or plain multi-stream
+            pcfg = dict(ccfg, be_cu_reserve=args.cu_reserve, crit_cu_exclusive=args.crit_cu_exclusive)
         runs[ph] = run_phase(policy, crit_net, be_tasks, args.warmup * pps, args.steps * pps, cfg["period_ms"],
                              cfg["arrival"], seed=11, ccfg=pcfg, with_be=(ph != "solo"))
         r = runs[ph]
@@ -767,7 +770,7 @@ def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
                 "solo_p50_ms": round(solo["p50_ms"], 4), "solo_p99_ms": round(solo["p99_ms"], 4),
                 "corun_p50_ms": round(main_run["p50_ms"], 4), "corun_p99_ms": round(main_run["p99_ms"], 4),
                 "p99_overhead": round(main_run["p99_ms"] / solo["p99_ms"] - 1.0, 4)}
-        for other in ("elastic", "multistream", "multistream_cu", "ib", "sequential"):
+        for other in ("elastic", "elastic_cu", "multistream", "multistream_cu", "ib", "sequential"):
             if other in runs and other != main_name:
                 crit[f"{other}_p99_overhead"] = round(runs[other]["p99_ms"] / solo["p99_ms"] - 1.0, 4)
         summary["critical"] = crit
@@ -787,6 +790,15 @@ def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
         if "sequential" in runs:
             pr["speedup_vs_sequential"] = round(el["be_img_s"] / max(1e-9, runs["sequential"]["be_img_s"]), 3)
         summary["paper_rule"] = pr
+    if "elastic_cu" in runs and "solo" in runs:
+        el = runs["elastic_cu"]
+        pr = {"busy_policy": 0, "cu_reserve": args.cu_reserve, "crit_cu_exclusive": args.crit_cu_exclusive,
+              "p50_ms": round(el["p50_ms"], 4), "p99_ms": round(el["p99_ms"], 4),
+              "p99_overhead": round(el["p99_ms"] / runs["solo"]["p99_ms"] - 1.0, 4),
+              "be_img_s": round(el["be_img_s"], 2)}
+        if "sequential" in runs:
+            pr["speedup_vs_sequential"] = round(el["be_img_s"] / max(1e-9, runs["sequential"]["be_img_s"]), 3)
+        summary["paper_rule_cu_masked"] = pr
     phases_out = {ph: {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()} for ph, r in runs.items()}
     return runs, main_name, main_run, summary, phases_out
 
@@ -881,7 +893,9 @@ def main():
     ap.add_argument("--whole-margin", type=float, default=0.0,
                     help="factor on the estimate of whole-request launches (0: the library's 2.0)")
     ap.add_argument("--cu-reserve", type=int, default=64,
-                    help="multistream_cu phase: compute units left out of the normal streams' CU mask")
+                    help="multistream_cu / elastic_cu phases: compute units left out of the normal streams' CU mask")
+    ap.add_argument("--crit-cu-exclusive", type=int, default=1, choices=(0, 1),
+                    help="multistream_cu / elastic_cu phases: the critical stream gets only the reserved CUs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-op", default=None, metavar="NET.LAYER[,NET.LAYER...]",
                     help="only launch the listed layers (unsharded) --reps times each, then a 256 MiB device "

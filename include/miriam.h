@@ -366,6 +366,10 @@ typedef struct miriam_config {
     int32_t fake_fail_launch; /* FAKE backend only: the n-th launch (1-based, counting kernel launches
                                 and captured replays since miriam_init) fails with MIRIAM_EHIP, ending
                                 its request with that status; 0 = none (tests of the failure path) */
+    int32_t crit_cu_exclusive; /* HIP backend, with be_cu_reserve > 0: the critical stream is created
+                                with the complementary mask (the top be_cu_reserve CUs only), so
+                                the two classes never share a CU; 0 = the critical stream keeps
+                                every CU.  FAKE backend: ignored. */
 } miriam_config;
 
 typedef struct miriam_completion {

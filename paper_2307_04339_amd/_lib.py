@@ -84,6 +84,7 @@ class Config(ctypes.Structure):
         ("segments", ctypes.c_int32), ("event_us", ctypes.c_double),
         ("be_cu_reserve", ctypes.c_int32), ("whole_when_clear", ctypes.c_int32),
         ("whole_margin", ctypes.c_double), ("fake_fail_launch", ctypes.c_int32),
+        ("crit_cu_exclusive", ctypes.c_int32),
     ]
 
 

@@ -54,8 +54,9 @@ struct Captured {
 struct Backend {
     virtual ~Backend() {}
     // Create the streams: 0 critical, 1 .. n-1 normal; with cu_reserve > 0 the normal streams
-    // leave out the top cu_reserve of n_cu compute units.
-    virtual int start(int n_streams, int n_cu, int cu_reserve) = 0;
+    // leave out the top cu_reserve of n_cu compute units, and with crit_exclusive the critical
+    // stream has only those.
+    virtual int start(int n_streams, int n_cu, int cu_reserve, bool crit_exclusive) = 0;
     virtual int launch(const miriam_op *op, int64_t b, int64_t l, int grid, int block, int stream) = 0;
     virtual int record(int stream) = 0;       // event id >= 0, or < 0 error
     virtual int query(int ev) = 0;            // 1 done, 0 pending, < 0 error
@@ -115,14 +116,18 @@ struct HipBackend : Backend {
     uint64_t *gate_dev = nullptr;
     int wall_khz = 0;               // device wall-clock rate
 
-    int start(int n, int n_cu, int cu_reserve) override {
+    int start(int n, int n_cu, int cu_reserve, bool crit_exclusive) override {
         hipError_t e = hipGetDevice(&dev);
         if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-        std::vector<uint32_t> mask((size_t)(n_cu + 31) / 32, 0u);
-        for (int i = 0; i < n_cu - cu_reserve; ++i) mask[(size_t)i / 32] |= 1u << (i % 32);
+        std::vector<uint32_t> normal_mask((size_t)(n_cu + 31) / 32, 0u), crit_mask(normal_mask.size(), 0u);
+        for (int i = 0; i < n_cu; ++i) {
+            std::vector<uint32_t> &m = i < n_cu - cu_reserve ? normal_mask : crit_mask;
+            m[(size_t)i / 32] |= 1u << (i % 32);
+        }
         for (int i = 0; i < n; ++i) {
             hipStream_t s;
-            if (i > 0 && cu_reserve > 0) {
+            if (cu_reserve > 0 && (i > 0 || crit_exclusive)) {
+                const std::vector<uint32_t> &mask = i > 0 ? normal_mask : crit_mask;
                 e = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
                 if (e != hipSuccess) return hip_fail(e, "hipExtStreamCreateWithCUMask");
                 streams.push_back(s);
@@ -131,7 +136,7 @@ struct HipBackend : Backend {
                 e = hipExtStreamGetCUMask(s, (uint32_t)got.size(), got.data());
                 if (e != hipSuccess) return hip_fail(e, "hipExtStreamGetCUMask");
                 if (got != mask) {
-                    set_error("normal stream reports a different compute-unit mask than requested");
+                    set_error("stream reports a different compute-unit mask than requested");
                     return MIRIAM_ESTATE;
                 }
                 continue;
@@ -328,7 +333,7 @@ struct FakeBackend : Backend {
     std::vector<int64_t> ev_time;
     std::vector<int> free_ev;
 
-    int start(int n, int, int) override {
+    int start(int n, int, int, bool) override {
         busy_until.assign(n, 0);
         return MIRIAM_OK;
     }
@@ -1413,7 +1418,7 @@ int miriam_init(const miriam_config *cfg) {
         cfg->warm_critical < 0 || cfg->warm_critical > 1 || cfg->graph_chunk < 0 || !(cfg->arm_lead_us >= 0.0) ||
         cfg->segments < 0 || cfg->segments > 1 || !(cfg->event_us >= 0.0) || cfg->be_cu_reserve < 0 ||
         cfg->whole_when_clear < 0 || cfg->whole_when_clear > 1 || !(cfg->whole_margin >= 0.0) ||
-        cfg->fake_fail_launch < 0) {
+        cfg->fake_fail_launch < 0 || cfg->crit_cu_exclusive < 0 || cfg->crit_cu_exclusive > 1) {
         set_error("invalid coordinator configuration");
         return MIRIAM_EINVAL;
     }
@@ -1450,7 +1455,8 @@ int miriam_init(const miriam_config *cfg) {
         c->l_threads = 2048;
         c->be = f;
     }
-    int rc = c->be->start(c->n_streams, c->n_cu, cfg->backend == MIRIAM_BACKEND_HIP ? cfg->be_cu_reserve : 0);
+    int rc = c->be->start(c->n_streams, c->n_cu, cfg->backend == MIRIAM_BACKEND_HIP ? cfg->be_cu_reserve : 0,
+                          cfg->crit_cu_exclusive != 0);
     if (rc != MIRIAM_OK) {
         c->be->stop();
         delete c->be;

@@ -44,6 +44,7 @@ def default_config(**kw) -> L.Config:
     c.whole_when_clear = 0
     c.whole_margin = 0.0
     c.fake_fail_launch = 0
+    c.crit_cu_exclusive = 0
     for k, v in kw.items():
         if k == "policy" and isinstance(v, str):
             v = POLICY[v]

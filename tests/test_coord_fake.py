@@ -276,7 +276,8 @@ def test_bad_configs_rejected(L):
     lib = L.load()
     for bad in [dict(policy=5), dict(n_be_streams=0), dict(n_be_streams=9), dict(inflight_depth=0),
                 dict(top_frac=0.0), dict(quantum_us=0.0), dict(backend=3), dict(graphs=2), dict(graphs=-1),
-                dict(busy_policy=3), dict(be_cu_reserve=-1), dict(policy=4)]:
+                dict(busy_policy=3), dict(be_cu_reserve=-1), dict(policy=4), dict(crit_cu_exclusive=2),
+                dict(crit_cu_exclusive=-1)]:
         c = default_config(**dict(dict(backend="fake"), **bad))
         assert lib.miriam_init(ctypes.byref(c)) == L.EINVAL, bad
 

@@ -138,11 +138,11 @@ def test_release_gate_ends_on_flag_or_limit(limit_us, open_after_us):
     assert float(x.sum()) == 2048.0
 
 
-@pytest.mark.parametrize("policy", ["multistream", "elastic"])
-def test_cu_masked_normal_streams_match_eager(policy):
-    """Normal streams created with a compute-unit mask (64 CUs left to the critical stream):
-    every request completes with outputs bitwise equal to the eager forward pass, and a
-    reserve of every CU is rejected."""
+@pytest.mark.parametrize("policy,crit_excl", [("multistream", 0), ("elastic", 0), ("elastic", 1)])
+def test_cu_masked_normal_streams_match_eager(policy, crit_excl):
+    """Normal streams created with a compute-unit mask (64 CUs left to the critical stream, which
+    with crit_excl has only those): every request completes with outputs bitwise equal to the
+    eager forward pass, and a reserve of every CU is rejected."""
     from paper_2307_04339_amd import models
     from paper_2307_04339_amd import _lib as L
     from paper_2307_04339_amd.runtime import Coordinator
@@ -156,7 +156,7 @@ def test_cu_masked_normal_streams_match_eager(policy):
     torch.cuda.synchronize()
     ref = {n.name: [bits(l.t["y"]) for l in n.layers] for n in (crit, be)}
     co = Coordinator(policy=policy, be_cu_reserve=64, profile_reps=1, n_be_streams=1, inflight_depth=2,
-                     quantum_us=20.0)
+                     quantum_us=20.0, crit_cu_exclusive=crit_excl)
     try:
         ct = co.task(crit.ops())
         bt = co.task(be.ops())
