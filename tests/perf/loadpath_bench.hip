@@ -1,0 +1,187 @@
+// Load-path microbenchmark for the contraction kernels' operand stream on gfx950.
+//
+// Part 1, raw rates: every wave of a 4-wave workgroup streams 1 KB per instruction
+// (global_load_lds_dwordx4 into LDS, or global_load_dwordx4 into registers) from an L2-resident
+// 64 KB block or from a large buffer; bytes per clock per CU at one and two workgroups per CU.
+// Part 2, the pipelined implicit GEMM's operand stream without arithmetic: per 128 x 128 tile
+// and 64-element K chunk, 128 input rows of 128 B (pixel stride 256 B, the nine 3x3 tap
+// shifts: VGG-16 b8 conv2_2) and 128 weight rows of 128 B (row stride 2304 B), by LDS DMA into
+// a 3-stage A ring and a 2-stage B ring, with the kernel's vmcnt wait and barrier per chunk or
+// free-running; the same byte count from contiguous 1 KB blocks for comparison.
+//
+// Every address is inside its buffer by construction (see the bounds noted at each index).
+// Build and run:  hipcc --offload-arch=gfx950 -O3 -o /tmp/loadpath tests/perf/loadpath_bench.hip && /tmp/loadpath
+#include <hip/hip_runtime.h>
+#include <cstdint>
+#include <cstdio>
+
+#define CHECK(x)                                                                         \
+    do {                                                                                 \
+        hipError_t e_ = (x);                                                             \
+        if (e_ != hipSuccess) {                                                          \
+            printf("HIP error %s at line %d\n", hipGetErrorString(e_), __LINE__);        \
+            return 1;                                                                    \
+        }                                                                                \
+    } while (0)
+
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ uint32_t lds_addr(char *p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)p;
+}
+
+// ---- part 1: raw rates.  Wave w of the workgroup, instruction j of iteration i reads the 1 KB
+// block ((i * 8 + j) * 4 + w) masked to the span (a power of two >= 64 KB), offset by 64 KB per
+// workgroup when per_wg; LDS target: 8 KB per wave (32 KB per workgroup).
+template <bool DMA>
+__global__ __launch_bounds__(256) void raw_kernel(const char *src, uint64_t span_mask, int iters, int per_wg, int *sink) {
+    __shared__ __attribute__((aligned(1024))) char lds[32768];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
+    const uint32_t base = lds_addr(lds);
+    const uint64_t off = per_wg ? (uint64_t)blockIdx.x * 65536 : 0;
+    uint32_t acc = 0;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint64_t o = (off + (uint64_t)((i * 8 + j) * 4 + wave) * 1024) & span_mask;  // o + 1 KB <= span
+            const char *p = src + o + lane * 16;
+            if constexpr (DMA) {
+                dma16(p, base + wave * 8192 + j * 1024);
+            } else {
+                const uint4 v = *reinterpret_cast<const uint4 *>(p);
+                acc ^= v.x ^ v.y ^ v.z ^ v.w;
+            }
+        }
+        if constexpr (DMA) wait_vm<8>();  // one batch of 8 instructions in flight behind the newest
+    }
+    wait_vm<0>();
+    __syncthreads();
+    if constexpr (DMA) acc ^= *reinterpret_cast<const uint32_t *>(lds + threadIdx.x * 4);
+    if (acc == 0x12345678u) sink[0] = (int)acc;
+}
+
+// ---- part 2: the operand stream of a 128 x 128 implicit-GEMM tile
+constexpr int kPix = 8 * 112 * 112;  // input pixels, 256 B each
+constexpr int kK = 1152;             // weight row length (elements): 2304 B rows, 128 rows
+
+// PAT 0: the convolution's rows; 1: contiguous 1 KB per instruction
+template <int PAT, bool BAR>
+__global__ __launch_bounds__(256) void conv_kernel(const char *X, const char *W, int tiles, int *sink) {
+    __shared__ __attribute__((aligned(1024))) char lds[81920];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
+    const int lrow = lane >> 3, slot = lane & 7;
+    const uint32_t base = lds_addr(lds);
+    for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+        const int m0 = (t * 128) % (kPix - 128 - 2 * 112 - 2);  // m0 + 127 + 226 < kPix
+        for (int c = 0; c < 18; ++c) {
+            const int tap = c >> 1, half = c & 1;
+            const int shift = (tap / 3) * 112 + (tap % 3);  // <= 226
+            const uint32_t sa = base + (c % 3) * 16384, sb = base + 49152 + (c % 2) * 16384;  // < 80 KB
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 8 * (j * 4 + wave) + lrow;  // < 128
+                const char *pb = PAT == 0 ? W + (int64_t)row * (kK * 2) + c * 128 + slot * 16  // <= 294912 B
+                                          : W + (int64_t)((c * 16 + j * 4 + wave) % 256) * 1024 + lane * 16;  // < 256 KB
+                dma16(pb, sb + (8 * (j * 4 + wave)) * 128);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 8 * (j * 4 + wave) + lrow;
+                const char *pa = PAT == 0 ? X + (int64_t)(m0 + row + shift) * 256 + half * 128 + slot * 16
+                                          : X + (int64_t)(m0 * 2 + (c * 16 + j * 4 + wave) * 64) * 16 + lane * 16;
+                dma16(pa, sa + (8 * (j * 4 + wave)) * 128);
+            }
+            if (BAR) {
+                wait_vm<4>();
+                __syncthreads();
+            } else {
+                wait_vm<16>();
+            }
+        }
+    }
+    wait_vm<0>();
+    __syncthreads();
+    if (lds[threadIdx.x] == 123 && lds[threadIdx.x + 1] == 45) sink[0] = 1;
+}
+
+static int cus = 0;
+
+template <class F>
+static int best_ms(F launch, float *out) {
+    hipEvent_t a, b;
+    CHECK(hipEventCreate(&a));
+    CHECK(hipEventCreate(&b));
+    launch();
+    CHECK(hipDeviceSynchronize());
+    float best = 1e30f;
+    for (int r = 0; r < 5; ++r) {
+        CHECK(hipEventRecord(a));
+        launch();
+        CHECK(hipEventRecord(b));
+        CHECK(hipEventSynchronize(b));
+        float ms = 0;
+        CHECK(hipEventElapsedTime(&ms, a, b));
+        if (ms < best) best = ms;
+    }
+    CHECK(hipEventDestroy(a));
+    CHECK(hipEventDestroy(b));
+    *out = best;
+    return 0;
+}
+
+static void report(const char *name, int grid, double bytes, float ms) {
+    printf("%-44s grid %5d  %9.1f us  %8.1f GB/s  %5.1f B/clk/CU\n", name, grid, ms * 1e3, bytes / (ms * 1e-3) / 1e9,
+           bytes / (ms * 1e-3) / 2.4e9 / cus);
+}
+
+int main() {
+    CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
+    const uint64_t big = 1ull << 30;
+    char *src, *X, *W;
+    int *sink;
+    CHECK(hipMalloc(&src, big));
+    CHECK(hipMemset(src, 1, big));
+    CHECK(hipMalloc(&X, (size_t)kPix * 256));
+    CHECK(hipMemset(X, 1, (size_t)kPix * 256));
+    CHECK(hipMalloc(&W, (size_t)1 << 20));
+    CHECK(hipMemset(W, 1, (size_t)1 << 20));
+    CHECK(hipMalloc(&sink, 64));
+    printf("CUs %d; rates at 2.4 GHz\n", cus);
+    float ms;
+    for (int k = 1; k <= 2; ++k) {
+        const int grid = cus * k, it = 2000;
+        printf("-- part 1: %d workgroup(s) of 4 waves per CU\n", k);
+        const double b_hot = (double)grid * 256 * 16 * 8 * it, b_big = b_hot / 4;
+        if (best_ms([&] { hipLaunchKernelGGL(raw_kernel<true>, dim3(grid), dim3(256), 0, 0, src, 65535ull, it, 0, sink); }, &ms)) return 1;
+        report("LDS DMA, L2-resident 64 KB", grid, b_hot, ms);
+        if (best_ms([&] { hipLaunchKernelGGL(raw_kernel<false>, dim3(grid), dim3(256), 0, 0, src, 65535ull, it, 0, sink); }, &ms)) return 1;
+        report("load to VGPR, L2-resident 64 KB", grid, b_hot, ms);
+        if (best_ms([&] { hipLaunchKernelGGL(raw_kernel<true>, dim3(grid), dim3(256), 0, 0, src, big - 1, it / 4, 1, sink); }, &ms)) return 1;
+        report("LDS DMA, 16 MB per workgroup of 1 GB", grid, b_big, ms);
+        if (best_ms([&] { hipLaunchKernelGGL(raw_kernel<false>, dim3(grid), dim3(256), 0, 0, src, big - 1, it / 4, 1, sink); }, &ms)) return 1;
+        report("load to VGPR, 16 MB per workgroup of 1 GB", grid, b_big, ms);
+    }
+    for (int k = 1; k <= 2; ++k) {
+        const int grid = cus * k;
+        printf("-- part 2: %d workgroup(s) per CU, 128x128 tiles of 18 K chunks (32 KB each)\n", k);
+        for (int tiles : {grid, 784}) {
+            const double bytes = (double)tiles * 18 * 32768;
+            char name[64];
+            snprintf(name, sizeof(name), "conv rows, barrier per chunk, %d tiles", tiles);
+            if (best_ms([&] { hipLaunchKernelGGL((conv_kernel<0, true>), dim3(grid), dim3(256), 0, 0, X, W, tiles, sink); }, &ms)) return 1;
+            report(name, grid, bytes, ms);
+            snprintf(name, sizeof(name), "conv rows, free running, %d tiles", tiles);
+            if (best_ms([&] { hipLaunchKernelGGL((conv_kernel<0, false>), dim3(grid), dim3(256), 0, 0, X, W, tiles, sink); }, &ms)) return 1;
+            report(name, grid, bytes, ms);
+            snprintf(name, sizeof(name), "contiguous 1 KB, barrier per chunk, %d tiles", tiles);
+            if (best_ms([&] { hipLaunchKernelGGL((conv_kernel<1, true>), dim3(grid), dim3(256), 0, 0, X, W, tiles, sink); }, &ms)) return 1;
+            report(name, grid, bytes, ms);
+        }
+    }
+    return 0;
+}
