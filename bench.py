@@ -201,7 +201,10 @@ def transformed_overhead(reps, flush):
     """Kernels elasticised by the source-to-source transformer: median time of the plain launch
     and of the elastic form unsharded (grid = the plain grid) and as 4 shards, cold caches.
     Workloads: bias + ReLU over 8 x 112 x 112 x 64 fp32, 2x2 max pooling of the same tensor,
-    and a 1024^3 fp32 product with 16 x 16 shared-memory tiles."""
+    a 1024^3 fp32 product with 16 x 16 shared-memory tiles, a direct 3x3 convolution with bias
+    and ReLU (1 x 56 x 56 x 64 -> 64, the single fp32 convolution's shape), a depthwise 3x3
+    convolution with bias and ReLU6 (16 x 56 x 56 x 144, a MobileNetV2 b16 layer), and row
+    softmax and LayerNorm over the encoder's shapes (4 heads x 128 x 128 scores; 128 x 768)."""
     import torch
     from paper_2307_04339_amd.transform import lib as TL
     T = TL.load()
@@ -214,6 +217,19 @@ def transformed_overhead(reps, flush):
     B = torch.rand((1024, 1024), device="cuda", generator=g)
     C = torch.empty((1024, 1024), device="cuda")
     n = x.numel()
+    xc = torch.rand((1, 56, 56, 64), device="cuda", generator=g) * 2 - 1
+    wc = torch.rand((64, 3, 3, 64), device="cuda", generator=g) * 2 - 1
+    yc = torch.empty((1, 56, 56, 64), device="cuda")
+    xd = torch.rand((16, 56, 56, 144), device="cuda", generator=g) * 2 - 1
+    wd = torch.rand((144, 3, 3), device="cuda", generator=g) * 2 - 1
+    bd = torch.rand(144, device="cuda", generator=g) * 2 - 1
+    yd = torch.empty_like(xd)
+    xs = torch.randn((4 * 128, 128), device="cuda", generator=g)
+    ys = torch.empty_like(xs)
+    xl = torch.randn((128, 768), device="cuda", generator=g)
+    gl = torch.rand(768, device="cuda", generator=g) + 0.5
+    bl_ = torch.rand(768, device="cuda", generator=g) - 0.5
+    yl = torch.empty_like(xl)
     cases = {
         "bias_relu": ((n + 255) // 256, 256,
                       lambda G, bl: T.plain_bias_relu_plain_launch(x.data_ptr(), bvec.data_ptr(), y.data_ptr(), n, 64,
@@ -230,6 +246,31 @@ def transformed_overhead(reps, flush):
                                                                      1024, 1024, 1024, G, 1, None),
                        lambda G, b0, l, gr, bl: T.plain_tiled_gemm_elastic_launch(
                            A.data_ptr(), B.data_ptr(), C.data_ptr(), 1024, 1024, 1024, G, 1, b0, l, gr, bl, None)),
+        "conv3x3_relu": ((yc.numel() + 255) // 256, 256,
+                         lambda G, bl: T.plain_conv3x3_relu_plain_launch(
+                             xc.data_ptr(), wc.data_ptr(), bvec.data_ptr(), yc.data_ptr(), 1, 56, 56, 64, 64, 1, G, 1,
+                             None),
+                         lambda G, b0, l, gr, bl: T.plain_conv3x3_relu_elastic_launch(
+                             xc.data_ptr(), wc.data_ptr(), bvec.data_ptr(), yc.data_ptr(), 1, 56, 56, 64, 64, 1, G, 1,
+                             b0, l, gr, bl, None)),
+        "dwconv3x3_relu6": ((yd.numel() + 255) // 256, 256,
+                            lambda G, bl: T.plain_dwconv3x3_relu6_plain_launch(
+                                xd.data_ptr(), wd.data_ptr(), bd.data_ptr(), yd.data_ptr(), 16, 56, 56, 144, 1, G, 1,
+                                None),
+                            lambda G, b0, l, gr, bl: T.plain_dwconv3x3_relu6_elastic_launch(
+                                xd.data_ptr(), wd.data_ptr(), bd.data_ptr(), yd.data_ptr(), 16, 56, 56, 144, 1, G, 1,
+                                b0, l, gr, bl, None)),
+        "softmax_rows": (4 * 128, 256,
+                         lambda G, bl: T.plain_softmax_rows_plain_launch(xs.data_ptr(), ys.data_ptr(), 4 * 128, 128,
+                                                                         G, 1, None),
+                         lambda G, b0, l, gr, bl: T.plain_softmax_rows_elastic_launch(
+                             xs.data_ptr(), ys.data_ptr(), 4 * 128, 128, G, 1, b0, l, gr, bl, None)),
+        "layernorm_rows": (128, 128,
+                           lambda G, bl: T.plain_layernorm_rows_plain_launch(
+                               xl.data_ptr(), gl.data_ptr(), bl_.data_ptr(), yl.data_ptr(), 128, 768, 1e-5, G, 1, None),
+                           lambda G, b0, l, gr, bl: T.plain_layernorm_rows_elastic_launch(
+                               xl.data_ptr(), gl.data_ptr(), bl_.data_ptr(), yl.data_ptr(), 128, 768, 1e-5, G, 1, b0, l,
+                               gr, bl, None)),
     }
 
     def med(fn):

@@ -71,3 +71,120 @@ __global__ void plain_transpose16(const float *in, float *out, int rows, int col
     const int oc = blockIdx.y * 16 + threadIdx.x, orow = blockIdx.x * 16 + threadIdx.y;
     if (orow < cols && oc < rows) out[(long long)orow * rows + oc] = tile[threadIdx.x][threadIdx.y];
 }
+
+// Direct 3x3 convolution, NHWC input [n, h, w, c], weights [k, 3, 3, c], zero padding 1, stride
+// s, plus bias and ReLU; one output element per thread, taps row-major and channels innermost.
+// elastic: block 256
+__global__ void plain_conv3x3_relu(const float *x, const float *wt, const float *b, float *y, int n, int h, int w,
+                                   int c, int k, int s) {
+    const int ho = (h + 2 - 3) / s + 1, wo = (w + 2 - 3) / s + 1;
+    const long long total = (long long)n * ho * wo * k;
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int oc = (int)(i % k), q = (int)((i / k) % wo), p = (int)((i / ((long long)k * wo)) % ho);
+    const int img = (int)(i / ((long long)k * wo * ho));
+    float acc = 0.0f;
+    for (int r = 0; r < 3; ++r) {
+        const int hi = p * s - 1 + r;
+        if (hi < 0 || hi >= h) continue;
+        for (int t = 0; t < 3; ++t) {
+            const int wi = q * s - 1 + t;
+            if (wi < 0 || wi >= w) continue;
+            const float *xp = x + (((long long)img * h + hi) * w + wi) * c;
+            const float *wp = wt + ((long long)(oc * 3 + r) * 3 + t) * c;
+            for (int ch = 0; ch < c; ++ch) acc = fmaf(xp[ch], wp[ch], acc);
+        }
+    }
+    const float v = acc + b[oc];
+    y[i] = v > 0.0f ? v : 0.0f;
+}
+
+// Depthwise 3x3 convolution (MobileNet), NHWC [n, h, w, c], weights [c, 3, 3], zero padding 1,
+// stride s, plus bias and ReLU6; one output element per thread.
+// elastic: block 256
+__global__ void plain_dwconv3x3_relu6(const float *x, const float *wt, const float *b, float *y, int n, int h, int w,
+                                      int c, int s) {
+    const int ho = (h + 2 - 3) / s + 1, wo = (w + 2 - 3) / s + 1;
+    const long long total = (long long)n * ho * wo * c;
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int ch = (int)(i % c), q = (int)((i / c) % wo), p = (int)((i / ((long long)c * wo)) % ho);
+    const int img = (int)(i / ((long long)c * wo * ho));
+    float acc = 0.0f;
+    for (int r = 0; r < 3; ++r) {
+        const int hi = p * s - 1 + r;
+        if (hi < 0 || hi >= h) continue;
+        for (int t = 0; t < 3; ++t) {
+            const int wi = q * s - 1 + t;
+            if (wi < 0 || wi >= w) continue;
+            acc = fmaf(x[(((long long)img * h + hi) * w + wi) * c + ch], wt[(ch * 3 + r) * 3 + t], acc);
+        }
+    }
+    const float v = acc + b[ch];
+    y[i] = fminf(fmaxf(v, 0.0f), 6.0f);
+}
+
+// Softmax of each row of a rows x n matrix (attention scores), one 256-thread block per row:
+// the row maximum and the sum of exponentials are reduced in shared memory, so the elastic
+// form keeps the 256-thread block.
+// elastic: block 256
+__global__ void plain_softmax_rows(const float *x, float *y, int rows, int n) {
+    __shared__ float red[256];
+    const int row = blockIdx.x;
+    if (row >= rows) return;
+    const float *xr = x + (long long)row * n;
+    float m = -INFINITY;
+    for (int j = threadIdx.x; j < n; j += 256) m = fmaxf(m, xr[j]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int d = 128; d > 0; d >>= 1) {
+        if (threadIdx.x < d) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + d]);
+        __syncthreads();
+    }
+    m = red[0];
+    __syncthreads();
+    float sum = 0.0f;
+    for (int j = threadIdx.x; j < n; j += 256) sum += expf(xr[j] - m);
+    red[threadIdx.x] = sum;
+    __syncthreads();
+    for (int d = 128; d > 0; d >>= 1) {
+        if (threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
+        __syncthreads();
+    }
+    const float inv = 1.0f / red[0];
+    for (int j = threadIdx.x; j < n; j += 256) y[(long long)row * n + j] = expf(xr[j] - m) * inv;
+}
+
+// LayerNorm of each row of a rows x n matrix (transformer), one 128-thread block per row: mean
+// and variance reduced in shared memory, then y = (x - mean) / sqrt(var + eps) * g + b.
+// elastic: block 128
+__global__ void plain_layernorm_rows(const float *x, const float *g, const float *b, float *y, int rows, int n,
+                                     float eps) {
+    __shared__ float red[128];
+    const int row = blockIdx.x;
+    if (row >= rows) return;
+    const float *xr = x + (long long)row * n;
+    float s = 0.0f;
+    for (int j = threadIdx.x; j < n; j += 128) s += xr[j];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int d = 64; d > 0; d >>= 1) {
+        if (threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
+        __syncthreads();
+    }
+    const float mean = red[0] / (float)n;
+    __syncthreads();
+    float v = 0.0f;
+    for (int j = threadIdx.x; j < n; j += 128) {
+        const float d = xr[j] - mean;
+        v += d * d;
+    }
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int d = 64; d > 0; d >>= 1) {
+        if (threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
+        __syncthreads();
+    }
+    const float rstd = 1.0f / sqrtf(red[0] / (float)n + eps);
+    for (int j = threadIdx.x; j < n; j += 128) y[(long long)row * n + j] = (xr[j] - mean) * rstd * g[j] + b[j];
+}

@@ -17,7 +17,12 @@ def _plain():
 def test_parse_plain_kernels():
     ks = {k.name: k for k in elastify.parse(_plain())}
     assert set(ks) == {"plain_bias_relu", "plain_maxpool2", "plain_tiled_gemm", "plain_shift_add2d",
-                       "plain_transpose16"}
+                       "plain_transpose16", "plain_conv3x3_relu", "plain_dwconv3x3_relu6", "plain_softmax_rows",
+                       "plain_layernorm_rows"}
+    for name in ("plain_conv3x3_relu", "plain_dwconv3x3_relu6"):
+        assert (ks[name].block, ks[name].block_elastic) == (256, True)
+    for name, blk in (("plain_softmax_rows", 256), ("plain_layernorm_rows", 128)):
+        assert (ks[name].block, ks[name].block_elastic, len(ks[name].shared_decls)) == (blk, False, 1)
     assert (ks["plain_shift_add2d"].bx, ks["plain_shift_add2d"].by, ks["plain_shift_add2d"].block_elastic) == (32, 8, True)
     assert (ks["plain_transpose16"].bx, ks["plain_transpose16"].by, ks["plain_transpose16"].block_elastic) == (16, 16, False)
     assert (ks["plain_bias_relu"].block, ks["plain_bias_relu"].block_elastic) == (256, True)

@@ -6,7 +6,12 @@ two-tap convolution, in float64, rounded once to float32).
 
 Inputs: seeded U[-1, 1] float32 tensors (bias + ReLU over 1000 x 37, max pooling of a
 2 x 18 x 22 x 24 image, a 100 x 70 by 70 x 90 product; on 2-D grids and blocks a shifted
-sum over a 45 x 70 image and the transpose of a 50 x 37 matrix)."""
+sum over a 45 x 70 image and the transpose of a 50 x 37 matrix).  Network kernels written
+plainly: a direct 3x3 convolution with bias and ReLU (2 x 9 x 11 x 13 -> 10 channels, strides 1
+and 2) and a depthwise 3x3 convolution with bias and ReLU6 (2 x 10 x 13 x 24, inputs in [-4, 4]
+so the clamp at 6 is reached), against the oracle's convolution and epilogue; row softmax
+(37 x 300, N(0, 3)) and LayerNorm (29 x 200) with shared-memory reductions, which keep their
+block, against the oracle's row operators."""
 import numpy as np
 import pytest
 import torch
@@ -151,3 +156,86 @@ def test_transpose16_keeps_its_2d_block(T):
     # the transpose as the exact product I x^T
     ref = orc.gemm_nt(np.eye(Cc), x64.astype(np.float64))
     assert np.array_equal(y.cpu().numpy(), _f32(ref))
+
+
+# Network kernels written plainly (one output element per thread, or one block per row with
+# shared-memory reductions), elasticised by the same transformer.
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_conv3x3_relu(T, stride):
+    rng = np.random.default_rng(10 + stride)
+    N, H, W, C, K = 2, 9, 11, 13, 10
+    x64 = rng.uniform(-1, 1, (N, H, W, C)).astype(np.float32)
+    w64 = rng.uniform(-1, 1, (K, 3, 3, C)).astype(np.float32)
+    b64 = rng.uniform(-1, 1, K).astype(np.float32)
+    x, w, b = _dev(x64), _dev(w64), _dev(b64)
+    Ho, Wo = (H - 1) // stride + 1, (W - 1) // stride + 1
+    y = torch.empty((N, Ho, Wo, K), dtype=torch.float32, device="cuda")
+    G = (N * Ho * Wo * K + 255) // 256
+    _check_elastic(lambda G: T.plain_conv3x3_relu_plain_launch(_p(x), _p(w), _p(b), _p(y), N, H, W, C, K, stride,
+                                                               G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_conv3x3_relu_elastic_launch(_p(x), _p(w), _p(b), _p(y), N, H, W, C,
+                                                                               K, stride, G, 1, b0, l, g, bl, None),
+                   y, G, [64, 128, 256], seed=11)
+    from oracle import oracle as orc
+    ref = orc.conv2d(x64.astype(np.float64), w64.astype(np.float64), stride=stride, pad=1,
+                     bias=b64.astype(np.float64), act="relu")
+    # 117 fp32 fused multiply-adds per output against the fp64 sum
+    assert _rel(y.cpu().numpy(), ref) <= 1e-5
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_dwconv3x3_relu6(T, stride):
+    rng = np.random.default_rng(20 + stride)
+    N, H, W, C = 2, 10, 13, 24
+    # scaled so that some outputs pass 6 and the clamp is exercised
+    x64 = rng.uniform(-4, 4, (N, H, W, C)).astype(np.float32)
+    w64 = rng.uniform(-1, 1, (C, 3, 3)).astype(np.float32)
+    b64 = rng.uniform(-1, 1, C).astype(np.float32)
+    x, w, b = _dev(x64), _dev(w64), _dev(b64)
+    Ho, Wo = (H - 1) // stride + 1, (W - 1) // stride + 1
+    y = torch.empty((N, Ho, Wo, C), dtype=torch.float32, device="cuda")
+    G = (N * Ho * Wo * C + 255) // 256
+    _check_elastic(lambda G: T.plain_dwconv3x3_relu6_plain_launch(_p(x), _p(w), _p(b), _p(y), N, H, W, C, stride,
+                                                                  G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_dwconv3x3_relu6_elastic_launch(_p(x), _p(w), _p(b), _p(y), N, H, W,
+                                                                                  C, stride, G, 1, b0, l, g, bl, None),
+                   y, G, [64, 128, 256], seed=21)
+    from oracle import oracle as orc
+    ref = orc.conv2d(x64.astype(np.float64), w64.astype(np.float64).reshape(C, 3, 3, 1), stride=stride, pad=1,
+                     groups=C, bias=b64.astype(np.float64), act="relu6")
+    got = y.cpu().numpy()
+    assert (ref >= 6.0).any() and (ref <= 0.0).any()
+    assert _rel(got, ref) <= 1e-5
+
+
+def test_softmax_rows_keeps_its_block(T):
+    rng = np.random.default_rng(30)
+    rows, n = 37, 300  # the row is longer than the block: each thread reduces two strided values
+    x64 = rng.normal(0, 3, (rows, n)).astype(np.float32)
+    x = _dev(x64)
+    y = torch.empty((rows, n), dtype=torch.float32, device="cuda")
+    _check_elastic(lambda G: T.plain_softmax_rows_plain_launch(_p(x), _p(y), rows, n, G, 1, None),
+                   lambda G, b0, l, g, bl: T.plain_softmax_rows_elastic_launch(_p(x), _p(y), rows, n, G, 1, b0, l, g,
+                                                                               bl, None),
+                   y, rows, [256], seed=31)
+    from oracle import oracle as orc
+    ref = orc.softmax_rows(x64.astype(np.float64), 1.0)
+    assert _rel(y.cpu().numpy(), ref) <= 1e-5
+
+
+def test_layernorm_rows_keeps_its_block(T):
+    rng = np.random.default_rng(40)
+    rows, n, eps = 29, 200, 1e-5
+    x64 = rng.normal(0.5, 2, (rows, n)).astype(np.float32)
+    g64 = rng.uniform(0.5, 1.5, n).astype(np.float32)
+    b64 = rng.uniform(-1, 1, n).astype(np.float32)
+    x, g, b = _dev(x64), _dev(g64), _dev(b64)
+    y = torch.empty((rows, n), dtype=torch.float32, device="cuda")
+    _check_elastic(lambda G: T.plain_layernorm_rows_plain_launch(_p(x), _p(g), _p(b), _p(y), rows, n, eps, G, 1, None),
+                   lambda G, b0, l, gr, bl: T.plain_layernorm_rows_elastic_launch(_p(x), _p(g), _p(b), _p(y), rows, n,
+                                                                                  eps, G, 1, b0, l, gr, bl, None),
+                   y, rows, [128], seed=41)
+    from oracle import oracle as orc
+    ref = orc.layernorm_rows(x64.astype(np.float64), g64.astype(np.float64), b64.astype(np.float64), eps)
+    assert _rel(y.cpu().numpy(), ref) <= 1e-5
