@@ -844,6 +844,41 @@ def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
     return runs, main_name, main_run, summary, phases_out
 
 
+def vendor_context(layer, reps, flush, ours_us):
+    """The dominant convolution's shape through the vendor libraries, for context: torch's
+    conv2d on channels-last tensors and on NCHW copies (MIOpen; convolution only, without the
+    fused BN and activation) and the equivalent dense product (M = N*Ho*Wo, N = K, K = KH*KW*C; hipBLASLt via
+    torch.matmul).  Same eviction read before each launch and HIP events as the per-layer times."""
+    import torch
+    import torch.nn.functional as F
+    t = layer.t
+    x, w = t["x"], t["w"]
+    stride, pad = layer.params["stride"], layer.params["pad"]
+    N, H, W, C = x.shape
+    K, KH, KW, _ = w.shape
+    xc = x.permute(0, 3, 1, 2)  # NCHW view of the NHWC tensor: channels-last memory
+    wc = w.permute(0, 3, 1, 2).contiguous(memory_format=torch.channels_last)
+    y = F.conv2d(xc, wc, stride=stride, padding=pad)
+    torch.cuda.synchronize()
+    conv_us, _ = _median_us(lambda: F.conv2d(xc, wc, stride=stride, padding=pad), reps, flush)
+    xn, wn = xc.contiguous(), w.permute(0, 3, 1, 2).contiguous()  # NCHW copies
+    F.conv2d(xn, wn, stride=stride, padding=pad)
+    torch.cuda.synchronize()
+    conv_nchw_us, _ = _median_us(lambda: F.conv2d(xn, wn, stride=stride, padding=pad), reps, flush)
+    del xn, wn
+    Ho, Wo = y.shape[2], y.shape[3]
+    M, Kd = N * Ho * Wo, KH * KW * C
+    A = (torch.rand(M, Kd, device="cuda") * 2 - 1).to(x.dtype)
+    B = (torch.rand(K, Kd, device="cuda") * 0.1).to(x.dtype)
+    gemm_us, _ = _median_us(lambda: A @ B.t(), reps, flush)
+    del A, B, y
+    return {"ours_us": round(ours_us, 2), "miopen_conv2d_us": round(conv_us, 2),
+            "miopen_conv2d_nchw_us": round(conv_nchw_us, 2),
+            "hipblaslt_gemm_us": round(gemm_us, 2), "gemm_shape": [M, K, Kd],
+            "note": "torch conv2d (MIOpen; channels-last, and NCHW copies) without the fused BN and activation, and the "
+                    "equivalent dense GEMM through torch.matmul (hipBLASLt); cold caches, HIP events"}
+
+
 def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
     """Per-kernel timing of the workload's networks; the dominant kernel's roofline, shard
     overhead (with its Eq. (5) decomposition), index functions and transformed kernels."""
@@ -864,6 +899,9 @@ def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
     layer = next(l for l in dom_net.layers if l.name == dom["name"])
     kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
     kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
+    if layer.kind == "conv":
+        log("  vendor context ...")
+        result["vendor_context"] = {"kernel": kern["kernel"], **vendor_context(layer, args.reps, flush, dom["us"])}
     gap = launch_gap_us()
     result["launch_gap_us"] = round(gap, 3)
     log("  shard overhead ...")
