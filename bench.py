@@ -902,6 +902,19 @@ def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
     if layer.kind == "conv":
         log("  vendor context ...")
         result["vendor_context"] = {"kernel": kern["kernel"], **vendor_context(layer, args.reps, flush, dom["us"])}
+        # every convolution of the dominant network, same comparison
+        per = []
+        for k in table:
+            if k["net"] != dom_net.name:
+                continue
+            l = next(x for x in dom_net.layers if x.name == k["name"])
+            if l.kind != "conv":
+                continue
+            v = vendor_context(l, args.reps, flush, k["us"])
+            per.append(dict(name=l.name, ours_us=v["ours_us"], miopen_us=min(v["miopen_conv2d_us"],
+                                                                               v["miopen_conv2d_nchw_us"]),
+                            hipblaslt_gemm_us=v["hipblaslt_gemm_us"]))
+        result["vendor_context"]["layers"] = per
     gap = launch_gap_us()
     result["launch_gap_us"] = round(gap, 3)
     log("  shard overhead ...")
