@@ -8,6 +8,8 @@
 // shifts: VGG-16 b8 conv2_2) and 128 weight rows of 128 B (row stride 2304 B), by LDS DMA into
 // a 3-stage A ring and a 2-stage B ring, with the kernel's vmcnt wait and barrier per chunk or
 // free-running; the same byte count from contiguous 1 KB blocks for comparison.
+// Part 3, streaming reads of a 3 GiB buffer (the practical HBM read rate).  Part 4, a small-batch
+// FC layer's weight stream in the skinny kernel's load pattern and row-contiguous.
 //
 // Every address is inside its buffer by construction (see the bounds noted at each index).
 // Build and run:  hipcc --offload-arch=gfx950 -O3 -o /tmp/loadpath tests/perf/loadpath_bench.hip && /tmp/loadpath
@@ -109,6 +111,69 @@ __global__ __launch_bounds__(256) void conv_kernel(const char *X, const char *W,
     if (lds[threadIdx.x] == 123 && lds[threadIdx.x + 1] == 45) sink[0] = 1;
 }
 
+// ---- part 3: streaming reads from HBM.  Workgroup g reads the contiguous region
+// [g * per_wg, (g + 1) * per_wg) of a buffer larger than every cache, 16 B per lane per load,
+// U loads in flight per lane; per_wg is a multiple of 256 * 16 * U bytes.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+template <int U>
+__global__ __launch_bounds__(256) void stream_kernel(const u32x4 *src, long long per_wg_vec, int *sink) {
+    const u32x4 *p = src + (long long)blockIdx.x * per_wg_vec + threadIdx.x;
+    uint32_t acc = 0;
+    for (long long i = 0; i < per_wg_vec; i += 256 * U) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + i + u * 256);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    if (acc == 0x12345678u) sink[0] = (int)acc;
+}
+
+// ---- part 4: the weight stream of a small-batch FC layer (VGG-16 fc6: 4096 rows of 25088
+// fp16 values, 50176 B apart).  1024 workgroups of 4 waves; workgroup g covers rows
+// 16 (g % 256) .. +15 and K slice g / 256 (of 4), wave w the slice's quarter w (1568 values).
+// ROWPAT 1 (the skinny kernel's MFMA-operand pattern): a load instruction reads 64 B of each of
+// the 16 rows (lane l: row l % 16, 16 B at 8 (l / 16) values into a 32-value step), 4 steps per
+// group, two groups in flight.  ROWPAT 0: an instruction reads 1 KB of one row (512 values),
+// cycling over the 16 rows, 8 instructions in flight.  Offsets stay inside the buffer: the
+// last 1 KB instruction of a quarter may run past it into the next quarter of the same row,
+// and the last quarter of a row stops at the row's end (clamped).
+constexpr long long kFcRow = 25088, kFcQ = 1568;
+template <int ROWPAT>
+__global__ __launch_bounds__(256) void fc_stream_kernel(const unsigned short *W, int *sink) {
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const long long n0 = (long long)(blockIdx.x % 256) * 16, slice = blockIdx.x / 256;
+    const long long kb = slice * (kFcRow / 4) + wave * kFcQ;
+    uint32_t acc = 0;
+    if constexpr (ROWPAT == 1) {
+        const int row = lane % 16, grp = lane / 16;
+        const unsigned short *wr = W + (n0 + row) * kFcRow;
+        for (long long k0 = kb; k0 < kb + kFcQ; k0 += 128) {
+            u32x4 v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const long long k = k0 + j * 32 + grp * 8;  // k + 8 <= kb + kFcQ + 96 <= kFcRow
+                v[j] = k + 8 <= kFcRow ? *reinterpret_cast<const u32x4 *>(wr + k) : u32x4{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+        }
+    } else {
+        for (long long c = 0; c < kFcQ; c += 512) {
+            u32x4 v[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                long long k = kb + c + lane * 8;
+                if (k + 8 > kFcRow) k = kFcRow - 8;
+                v[r] = *reinterpret_cast<const u32x4 *>(W + (n0 + r) * kFcRow + k);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc ^= v[r].x ^ v[r].y ^ v[r].z ^ v[r].w;
+        }
+    }
+    if (acc == 0x12345678u) sink[0] = (int)acc;
+}
+
 static int cus = 0;
 
 template <class F>
@@ -182,6 +247,36 @@ int main() {
             if (best_ms([&] { hipLaunchKernelGGL((conv_kernel<1, true>), dim3(grid), dim3(256), 0, 0, X, W, tiles, sink); }, &ms)) return 1;
             report(name, grid, bytes, ms);
         }
+    }
+    {
+        const size_t bytes = (size_t)3 << 30;  // 3 GiB: beyond the L2s and the 256 MB Infinity Cache
+        char *big3;
+        CHECK(hipMalloc(&big3, bytes));
+        CHECK(hipMemset(big3, 1, bytes));
+        printf("-- part 3: streaming reads of 3 GiB (nontemporal 16-byte loads)\n");
+        for (int k : {1, 2, 4, 8}) {
+            const int grid = cus * k;
+            const long long per_vec = (long long)(bytes / 16 / grid) / (256 * 8) * (256 * 8);
+            const double rb = (double)per_vec * 16 * grid;
+            if (best_ms([&] { hipLaunchKernelGGL(stream_kernel<8>, dim3(grid), dim3(256), 0, 0,
+                                                 reinterpret_cast<const u32x4 *>(big3), per_vec, sink); }, &ms)) return 1;
+            char name[64];
+            snprintf(name, sizeof(name), "stream, %d workgroups per CU, 8 loads in flight", k);
+            printf("%-44s grid %5d  %9.1f us  %8.1f GB/s\n", name, grid, ms * 1e3, rb / (ms * 1e-3) / 1e9);
+        }
+        CHECK(hipFree(big3));
+    }
+    {
+        const size_t wbytes = (size_t)4096 * kFcRow * 2;
+        unsigned short *Wf;
+        CHECK(hipMalloc(&Wf, wbytes));
+        CHECK(hipMemset(Wf, 1, wbytes));
+        printf("-- part 4: VGG-16 fc6 weight stream (205 MB), 1024 workgroups\n");
+        if (best_ms([&] { hipLaunchKernelGGL(fc_stream_kernel<1>, dim3(1024), dim3(256), 0, 0, Wf, sink); }, &ms)) return 1;
+        printf("%-44s  %9.1f us  %8.1f GB/s\n", "16 rows x 64 B per instruction", ms * 1e3, wbytes / (ms * 1e-3) / 1e9);
+        if (best_ms([&] { hipLaunchKernelGGL(fc_stream_kernel<0>, dim3(1024), dim3(256), 0, 0, Wf, sink); }, &ms)) return 1;
+        printf("%-44s  %9.1f us  %8.1f GB/s\n", "1 row x 1 KB per instruction", ms * 1e3, wbytes / (ms * 1e-3) / 1e9);
+        CHECK(hipFree(Wf));
     }
     return 0;
 }
