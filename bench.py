@@ -380,8 +380,8 @@ def shard_overhead(layer, reps, flush, n_cu, lib, gap_us):
 def config1_phase(reps, n_cu, lib, gap_us):
     """The single elastic fp32 convolution: x 1x56x56x64 and w 64x64x3x3 ~ U[-1, 1] (seeds 0 and
     1), bias ~ U[-1, 1] (seed 2), stride 1, pad 1, ReLU.  Its 1.75 MB working set stays in the
-    caches, so launches are timed warm, back to back: the mean of 200 launches between two
-    events, and the median of single launches between events.  Then every plan n in {1, 2, 4, 8}
+    caches, so launches are timed warm after 50 warm-up launches: the mean of 1000 launches
+    back to back between two events, and the median of 1000 single launches between events.  Then every plan n in {1, 2, 4, 8}
     x block {64, 128, 256} x forward / reverse shard order (persistent grids), each checked
     bitwise against the unsharded output."""
     import torch
@@ -398,7 +398,7 @@ def config1_phase(reps, n_cu, lib, gap_us):
         op.launch(0, T, full, 256)
     torch.cuda.synchronize()
     ref = y.clone()
-    nb = 200
+    nb = 1000
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(nb):
@@ -406,7 +406,7 @@ def config1_phase(reps, n_cu, lib, gap_us):
     e1.record()
     e1.synchronize()
     mean_b2b = 1000.0 * e0.elapsed_time(e1) / nb
-    med_single, _ = _median_us(lambda: op.launch(0, T, full, 256), reps)
+    med_single, _ = _median_us(lambda: op.launch(0, T, full, 256), max(reps, nb))
     flops = op.info.flops
     out = {"workload": "conv 1x56x56x64 * 64x64x3x3 fp32, bias + ReLU", "tiles": T,
            "tile": [op.info.tile_m, op.info.tile_n], "flops": flops,

@@ -9,7 +9,8 @@
 // a 3-stage A ring and a 2-stage B ring, with the kernel's vmcnt wait and barrier per chunk or
 // free-running; the same byte count from contiguous 1 KB blocks for comparison.
 // Part 3, streaming reads of a 3 GiB buffer (the practical HBM read rate).  Part 4, a small-batch
-// FC layer's weight stream in the skinny kernel's load pattern and row-contiguous.
+// FC layer's weight stream in the skinny kernel's load pattern and row-contiguous.  Part 5, the
+// MFMA peak from registers (fp16, bf16, fp32).
 //
 // Every address is inside its buffer by construction (see the bounds noted at each index).
 // Build and run:  hipcc --offload-arch=gfx950 -O3 -o /tmp/loadpath tests/perf/loadpath_bench.hip && /tmp/loadpath
@@ -174,6 +175,40 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const unsigned short *W,
     if (acc == 0x12345678u) sink[0] = (int)acc;
 }
 
+// ---- part 5: the MFMA peak from registers: each wave runs 8 independent accumulator chains of
+// v_mfma_f32_32x32x16_{f16,bf16} (32768 FLOP each) or v_mfma_f32_32x32x2f32 (4096 FLOP), no memory.
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+template <int KIND>
+__global__ __launch_bounds__(256) void mfma_kernel(int iters, float *sink) {
+    f32x16_t acc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+        for (int e = 0; e < 16; ++e) acc[c][e] = 0.0f;
+    const float x = (float)(threadIdx.x & 7) * 0.001f;
+    f16x8_t a16, b16;
+    bf16x8_t a16b, b16b;
+    for (int e = 0; e < 8; ++e) {
+        a16[e] = (_Float16)x;
+        b16[e] = (_Float16)(x + 0.5f);
+        a16b[e] = (__bf16)x;
+        b16b[e] = (__bf16)(x + 0.5f);
+    }
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            if constexpr (KIND == 0) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a16, b16, acc[c], 0, 0, 0);
+            else if constexpr (KIND == 1) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a16b, b16b, acc[c], 0, 0, 0);
+            else acc[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(x, x + 0.5f, acc[c], 0, 0, 0);
+        }
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][15];
+    if (s == 1234.5f) sink[0] = s;
+}
+
 static int cus = 0;
 
 template <class F>
@@ -277,6 +312,26 @@ int main() {
         if (best_ms([&] { hipLaunchKernelGGL(fc_stream_kernel<0>, dim3(1024), dim3(256), 0, 0, Wf, sink); }, &ms)) return 1;
         printf("%-44s  %9.1f us  %8.1f GB/s\n", "1 row x 1 KB per instruction", ms * 1e3, wbytes / (ms * 1e-3) / 1e9);
         CHECK(hipFree(Wf));
+    }
+    {
+        float *fs;
+        CHECK(hipMalloc(&fs, 64));
+        printf("-- part 5: MFMA from registers, 8 chains per wave, 2 workgroups of 4 waves per CU\n");
+        const int grid = cus * 2, it = 4000;
+        const char *names[3] = {"v_mfma_f32_32x32x16_f16", "v_mfma_f32_32x32x16_bf16", "v_mfma_f32_32x32x2f32"};
+        const double flop_per[3] = {32768.0, 32768.0, 4096.0};
+        const double peak[3] = {2500.0, 2500.0, 157.3};
+        for (int kind = 0; kind < 3; ++kind) {
+            int rc = 0;
+            if (kind == 0) rc = best_ms([&] { hipLaunchKernelGGL(mfma_kernel<0>, dim3(grid), dim3(256), 0, 0, it, fs); }, &ms);
+            if (kind == 1) rc = best_ms([&] { hipLaunchKernelGGL(mfma_kernel<1>, dim3(grid), dim3(256), 0, 0, it, fs); }, &ms);
+            if (kind == 2) rc = best_ms([&] { hipLaunchKernelGGL(mfma_kernel<2>, dim3(grid), dim3(256), 0, 0, it, fs); }, &ms);
+            if (rc) return 1;
+            const double tf = (double)grid * 4 * it * 8 * flop_per[kind] / (ms * 1e-3) / 1e12;
+            printf("%-44s  %9.1f us  %8.1f TFLOP/s  %5.1f %% of %.1f\n", names[kind], ms * 1e3, tf, 100.0 * tf / peak[kind],
+                   peak[kind]);
+        }
+        CHECK(hipFree(fs));
     }
     return 0;
 }
