@@ -45,6 +45,32 @@ __device__ __forceinline__ void lds_dma16(const void *src, uint32_t lds_addr) {
                  : "memory", "m0");
 }
 
+// Buffer resource over `bytes` bytes from `base` (raw buffer: stride 0, 32-bit offsets in
+// range [0, bytes)).  A load whose per-lane offset is at or past `bytes` returns zeros, which
+// the kernels use for padding taps and rows or columns past the operand's end.
+typedef int32_t rsrc_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    rsrc_t r;
+    r[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)b);
+    r[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(b >> 32) & 0xffffu));
+    r[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
+    r[3] = 0x00020000;  // 32-bit data format, no swizzle: plain byte offsets
+    return r;
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // past every buffer here (spans are < 2^31 bytes)
+
+// One 16-byte-per-lane buffer -> LDS load: lane i reads bytes [voff + soff, + 16) of the buffer
+// (zeros when voff is out of range) into LDS bytes [lds + 16 i, + 16).  Ordered like lds_dma16.
+__device__ __forceinline__ void buf_dma16(uint32_t voff, rsrc_t rsrc, uint32_t soff, uint32_t lds_addr) {
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr);
+    const uint32_t so = __builtin_amdgcn_readfirstlane(soff);
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %3 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "s"(lds), "s"(so)
+                 : "memory", "m0");
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -128,6 +154,7 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
     const int64_t G = gridDim.x;
     const int64_t rank = wg_rank(blockIdx.x, G);
     const int32_t C32 = (int32_t)a.C, KW32 = a.KW, KH32 = a.KH, H32 = (int32_t)a.H, W32 = (int32_t)a.W;
+    const int32_t ldx32 = (int32_t)a.ldx;
     // this lane's place in every load instruction: row offset in the 8-row group, slot
     const int lrow = lane >> 3, slot = lane & 7;
 
@@ -163,7 +190,9 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         const T *a_base[NIA];
         int32_t a_h0[NIA], a_w0[NIA];
         int32_t a_kr0[NIA], a_ks0[NIA], a_kc0[NIA];
-        uint64_t a_org[NIA];  // UNI: byte address of tap (0, 0), channel 0 + this lane's piece
+        // UNI: element offset from Xb of tap (0, 0), channel 0 + this lane's piece (negative for
+        // rows whose first tap lies in the padding)
+        int32_t a_row0[NIA];
         bool a_ok[NIA];
 #pragma unroll
         for (int j = 0; j < NIA; ++j) {
@@ -188,8 +217,8 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             // logical 16-byte piece of this slot, in the slice's first chunk
             const int32_t k = (int32_t)(slice * (uint32_t)a.cps) * KT + ((slot ^ ((row >> 1) & 7)) * VEC);
             if constexpr (UNI) {
-                const int64_t off = ((int64_t)a_h0[j] * a.W + a_w0[j]) * a.ldx + (slot ^ ((row >> 1) & 7)) * VEC;
-                a_org[j] = (uint64_t)(uintptr_t)a_base[j] + (uint64_t)(off * (int64_t)sizeof(T));
+                a_row0[j] = (int32_t)((a_base[j] - Xb) + ((int64_t)a_h0[j] * a.W + a_w0[j]) * a.ldx +
+                                      (slot ^ ((row >> 1) & 7)) * VEC);
             } else {
                 a_kc0[j] = k % C32;
                 const int32_t tap = k / C32;
@@ -200,6 +229,7 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         const T *b_base[NIB];
         int32_t b_k0[NIB];
         bool b_ok[NIB];
+        uint32_t b_off[NIB];  // UNI: byte offset from Wb of this lane's piece of K chunk 0 (or out of range)
 #pragma unroll
         for (int j = 0; j < NIB; ++j) {
             const int row = 8 * (j * P + pw) + lrow;
@@ -207,6 +237,14 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             b_ok[j] = n < a.Nc;
             b_base[j] = Wb + (b_ok[j] ? n : 0) * a.ldw;
             b_k0[j] = (slot ^ ((row >> 1) & 7)) * VEC;
+            b_off[j] = b_ok[j] ? (uint32_t)((n * a.ldw + b_k0[j]) * (int64_t)sizeof(T)) : kOutOfRange;
+        }
+        // UNI: the operands as buffers (spans below 2^31 bytes, checked at creation), so padding
+        // and rows past M or N read zeros from out-of-range offsets
+        rsrc_t rs_a, rs_b;
+        if constexpr (UNI) {
+            rs_a = make_rsrc(Xb, a.x_bytes);
+            rs_b = make_rsrc(Wb, a.w_bytes);
         }
 
         const int c0 = (int)slice * a.cps;
@@ -233,22 +271,19 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                     kc[j] = a_kc0[j];
                 }
             }
-            // UNI: the chunk's tap (ur, us) and channel base uc are wave-uniform; per-lane
-            // pointers and steps (elements per chunk: KT, or 0 for zero-block lanes)
+            // UNI: the chunk's tap (ur, us) and channel base uc are wave-uniform
             int32_t ur = 0, us = 0, uc = 0;
             bool retap = true;
-            const T *ap[NIA], *bp[NIB];
-            int32_t astep[NIA], bstep[NIB];
+            // UNI: this tap's byte offset per A instruction, fixed across the tap's chunks (the
+            // chunk's channel base goes in the uniform offset); the next B chunk's byte offset
+            uint32_t voff_a[NIA];
+            uint32_t kb_bytes = 0;
             if constexpr (UNI) {
                 const int32_t k0 = c0 * KT, tap = k0 / C32;
                 uc = k0 - tap * C32;
                 ur = tap / KW32;
                 us = tap - ur * KW32;
-#pragma unroll
-                for (int j = 0; j < NIB; ++j) {
-                    bp[j] = b_ok[j] ? b_base[j] + k0 + b_k0[j] : zsrc;
-                    bstep[j] = b_ok[j] ? KT : 0;
-                }
+                kb_bytes = (uint32_t)k0 * (uint32_t)sizeof(T);
             }
 
             // LDS byte addresses of chunk ch's A and B stages
@@ -264,21 +299,18 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 const uint32_t stage = a_stage(ch);
                 if constexpr (UNI) {
                     if (retap) {
-                        const int64_t toff = (((int64_t)ur * a.W + us) * a.ldx + uc) * (int64_t)sizeof(T);
+                        const int32_t toff = (ur * W32 + us) * ldx32;
 #pragma unroll
                         for (int j = 0; j < NIA; ++j) {
                             const uint32_t h = (uint32_t)(a_h0[j] + ur), w = (uint32_t)(a_w0[j] + us);
                             const bool ok = a_ok[j] && h < (uint32_t)H32 && w < (uint32_t)W32;
-                            ap[j] = ok ? reinterpret_cast<const T *>((uintptr_t)(a_org[j] + (uint64_t)toff)) : zsrc;
-                            astep[j] = ok ? KT : 0;
+                            voff_a[j] = ok ? (uint32_t)(a_row0[j] + toff) * (uint32_t)sizeof(T) : kOutOfRange;
                         }
                         retap = false;
                     }
+                    const uint32_t soff = (uint32_t)uc * (uint32_t)sizeof(T);
 #pragma unroll
-                    for (int j = 0; j < NIA; ++j) {
-                        lds_dma16(ap[j], stage + (uint32_t)((8 * (j * P + pw)) * 128));
-                        ap[j] += astep[j];
-                    }
+                    for (int j = 0; j < NIA; ++j) buf_dma16(voff_a[j], rs_a, soff, stage + (uint32_t)((8 * (j * P + pw)) * 128));
                     uc += KT;
                     if (uc == C32) {
                         uc = 0;
@@ -309,10 +341,8 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 const uint32_t stage = b_stage(ch);
                 if constexpr (UNI) {
 #pragma unroll
-                    for (int j = 0; j < NIB; ++j) {
-                        lds_dma16(bp[j], stage + (uint32_t)((8 * (j * P + pw)) * 128));
-                        bp[j] += bstep[j];
-                    }
+                    for (int j = 0; j < NIB; ++j) buf_dma16(b_off[j], rs_b, kb_bytes, stage + (uint32_t)((8 * (j * P + pw)) * 128));
+                    kb_bytes += (uint32_t)KT * (uint32_t)sizeof(T);
                     (void)ch;
                     return;
                 }

@@ -83,6 +83,9 @@ struct IgemmArgs {
     // memory-based index function: per output row m < mT * TM, (image, p * stride - pad,
     // q * stride - pad, m < M) as 4 int32; null = computed in the kernel
     const int32_t *rowtab;
+    // bytes addressable from one batch entry's x / w base (chunk-uniform decode only: the
+    // operands are read as buffers of this size, below 2^31 bytes)
+    uint32_t x_bytes, w_bytes;
     Epilogue epi;
 };
 

@@ -426,7 +426,18 @@ static int create_igemm(miriam_op *op) {
         if (nmaj) op->lay = (a_vec && b_vec) ? LAY_VEC_NB : LAY_SCALAR_NB;
         else op->lay = (a_vec && b_vec) ? LAY_VEC : LAY_SCALAR;
         // every 128-byte K chunk inside one filter tap: per-lane pointers advance per chunk
-        if (op->lay == LAY_VEC && a.C % (128 / es) == 0) op->lay = LAY_VEC_UNI;
+        // the chunk-uniform decode reads its operands as buffers with 32-bit offsets: spans in
+        // bytes from a batch entry's base, below 2^31 (zeros past the end come from the range check)
+        {
+            const int64_t x_span = (d.kind == MIRIAM_OP_CONV2D ? d.n * a.img_x : (a.M - 1) * a.ldx + a.K) * es;
+            const int64_t w_span = ((a.Nc - 1) * a.ldw + a.K) * es;
+            if (op->lay == LAY_VEC && a.C % (128 / es) == 0 && x_span < ((int64_t)1 << 31) &&
+                w_span < ((int64_t)1 << 31)) {
+                op->lay = LAY_VEC_UNI;
+                a.x_bytes = (uint32_t)x_span;
+                a.w_bytes = (uint32_t)w_span;
+            }
+        }
         if (!memidx && get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
             return einval("no kernel for this dtype / layout");
         if (memidx) {
