@@ -303,7 +303,8 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
 #pragma unroll
                         for (int j = 0; j < NIA; ++j) {
                             const uint32_t h = (uint32_t)(a_h0[j] + ur), w = (uint32_t)(a_w0[j] + us);
-                            const bool ok = a_ok[j] && h < (uint32_t)H32 && w < (uint32_t)W32;
+                            // bitwise &: one mask and one select, no branch per lane group
+                            const bool ok = a_ok[j] & (h < (uint32_t)H32) & (w < (uint32_t)W32);
                             voff_a[j] = ok ? (uint32_t)(a_row0[j] + toff) * (uint32_t)sizeof(T) : kOutOfRange;
                         }
                         retap = false;
