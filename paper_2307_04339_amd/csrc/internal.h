@@ -27,7 +27,8 @@ int igemm_mi_kernels_f16(int cfg, bool uni, const void *out[3], int *lds);
 int igemm_mi_kernels_bf16(int cfg, bool uni, const void *out[3], int *lds);
 int pix_kernels(int dtype, int kind, bool vec, const void *out[3]);
 int row_kernels(int dtype, int kind, bool vec, const void *out[3]);
-int skinny_kernels(int dtype, const void *out[3]);
+int skinny_kernels(int dtype, int cg, const void *out[3]);  // cg: 16-column groups per tile (1 or 2)
+int skinny_group(int cg);                                   // K per wave group of that kernel
 // resident-weight direct convolution: (3x3, stride 1, C in {8,16,32,64}), (3x3, stride 2, C = 8),
 // (1x1, stride 1, C in {16,24,32,64})
 int rw_kernels(int dtype, int64_t ks, int64_t stride, int64_t c, const void *out[3], int *lds);

@@ -58,10 +58,19 @@ static int tile_m_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 ? 64 
 static int tile_n_of(int cfg) { return cfg == CFG_32 ? 32 : (cfg == CFG_64 || cfg == CFG_128x64 ? 64 : 128); }
 constexpr int TILE_SKINNY = 5;  // descriptor tile code of the split-K skinny kernel
 
-// Fill the per-physical-block residency of the op's kernels.  Without a device
-// the figures stay 0 ("unknown"); the error state of the runtime is cleared.
 static int device_cus();
 
+// Column groups of 16 per skinny tile: two (one activation load per two weight loads) when
+// the op still has about four tiles per CU at 32 columns with slices of 1024 K values or more
+// (VGG-16 fc6, 8 x 4096 x 25088: 51.1 -> 48.7 us); one otherwise, where wider tiles left too
+// few tiles (fc7 15.0 / 15.1 us, fc8 10.5 / 11.1, ResNet-18 fc 6.6 / 8.0).
+static int skinny_cols(int64_t M, int64_t Nc, int64_t K) {
+    (void)M;
+    return cdiv(Nc, 32) * std::max<int64_t>(2, K / 1024) >= 4 * (int64_t)device_cus() ? 2 : 1;
+}
+
+// Fill the per-physical-block residency of the op's kernels.  Without a device
+// the figures stay 0 ("unknown"); the error state of the runtime is cleared.
 static void query_occupancy(miriam_op *op) {
     op->full_grid = op->T;
     int dev = 0;
@@ -285,7 +294,13 @@ static int create_igemm(miriam_op *op) {
     a.vec_store = (a.ldy % V == 0) && (a.sy0 % V == 0) && (a.sy1 % V == 0) && aligned16(d.y) &&
                   (!(d.flags & MIRIAM_EPI_RESIDUAL) || aligned16(d.residual));
     // fully connected layers at small batch: split-K skinny kernel
-    const bool skinny_ok = d.kind == MIRIAM_OP_GEMM && d.dtype != MIRIAM_F32 && a.M <= 16 && a_vec && b_vec;
+    // (its operands are read with 32-bit byte offsets: the M activation rows and a tile's
+    // weight rows must span less than 2^31 bytes)
+    const int skinny_cg = skinny_cols(a.M, a.Nc, a.K);
+    const int64_t es_in = esize(d.dtype);
+    const bool skinny_ok = d.kind == MIRIAM_OP_GEMM && d.dtype != MIRIAM_F32 && a.M <= 16 && a_vec && b_vec &&
+                           ((a.M - 1) * a.ldx + a.K) * es_in < ((int64_t)1 << 31) &&
+                           ((16 * skinny_cg - 1) * a.ldw + a.K) * es_in < ((int64_t)1 << 31);
     // direct 3x3 / stride-1 convolution with the input patch in LDS: C a whole number of
     // 128-byte chunks, aligned rows.  The library picks it for layers with at most 64 output
     // channels (one n tile) when it gives 1.5 tiles per CU and the 32-pixel tile columns waste
@@ -353,23 +368,27 @@ static int create_igemm(miriam_op *op) {
     } else if (cfg == TILE_SKINNY) {
         if (!skinny_ok) return einval("skinny tile needs an fp16/bf16 GEMM with m <= 16 and 16-byte rows");
         op->family = FAM_SKINNY;
+        const int cg = skinny_cg;
+        const int64_t group = skinny_group(cg);
         a.mT = 1;
-        a.nT = cdiv(a.Nc, 16);
-        // K slices: each slice keeps at least one 128-element group per logical wave.  The
-        // library choice splits until the op has about four tiles per CU, so a shard of a
-        // quarter of the op still gives every CU a tile (more slices measured slower
-        // unsharded: VGG-16 fc6 at eight tiles per CU 73 us against 59 us), and keeps slices of
-        // about 1024 K values or more beyond two slices (VGG-16 fc8, 4096 -> 1000: 12.0 us at
-        // 8 slices, 9.9 us at 4)
-        const int64_t max_ks = std::max<int64_t>(1, cdiv(a.K, 128) / 4);
+        a.nT = cdiv(a.Nc, 16 * cg);
+        // K slices: each slice keeps at least one group per logical wave.  The library choice
+        // splits until the op has about four tiles per CU, so a shard of a quarter of the op
+        // still gives every CU a tile (more slices measured slower unsharded: VGG-16 fc6 at
+        // eight tiles per CU 73 us against 59 us), and keeps slices of about 1024 K values or
+        // more beyond two slices (VGG-16 fc8, 4096 -> 1000: 12.0 us at 8 slices, 9.9 us at 4)
+        const int64_t max_ks = std::max<int64_t>(1, cdiv(a.K, group) / 4);
         int64_t ks = d.ksplit > 1 ? std::min<int64_t>(d.ksplit, max_ks)
                      : d.ksplit == 1 ? 1
                                      : std::min<int64_t>(std::min<int64_t>(max_ks, cdiv(4 * (int64_t)device_cus(), a.nT)),
                                                          std::max<int64_t>(2, a.K / 1024));
         ks = std::max<int64_t>(1, ks);
+        // slice length as the kernel derives it (whole numbers of 4 groups); count only the
+        // slices that hold K values
+        ks = cdiv(a.K, cdiv(a.K, ks * 4 * group) * 4 * group);
         a.ksplit = 1;
         if (ks > 1) {
-            const size_t wbytes = (size_t)a.nT * (size_t)ks * 16 * 16 * sizeof(float);
+            const size_t wbytes = (size_t)a.nT * (size_t)ks * 16 * 16 * cg * sizeof(float);
             const size_t cbytes = (size_t)a.nT * sizeof(int32_t);
             const int wr = alloc_workspace(op, wbytes, cbytes, d.ksplit > 1);
             if (wr < 0) return wr;
@@ -381,10 +400,11 @@ static int create_igemm(miriam_op *op) {
         }
         op->T = a.nT * a.ksplit;
         op->cfg = cfg;
-        op->tile_m = op->tile_n = 16;
+        op->tile_m = 16;
+        op->tile_n = 16 * cg;
         op->lay = LAY_VEC;
-        op->lds_bytes = 4 * 16 * 17 * 4;
-        if (skinny_kernels(d.dtype, op->kern) != 0) return einval("no skinny kernel for this dtype");
+        op->lds_bytes = 4 * 16 * (16 * cg + 1) * 4;
+        if (skinny_kernels(d.dtype, cg, op->kern) != 0) return einval("no skinny kernel for this dtype");
     } else {
         if (cfg < CFG_32 || cfg > CFG_256x128 || cfg == TILE_SKINNY) return einval("unknown tile configuration");
         a.mT = cdiv(a.M, tile_m_of(cfg));

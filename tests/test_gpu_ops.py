@@ -80,10 +80,11 @@ def test_gemm_matches_oracle(ops, orc, dtype, case):
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("M,N,K,ksplit", [(4, 300, 4096, 4), (8, 1000, 8192, 0), (2, 64, 3328, 3),
-                                          (16, 200, 2048, 2)])
+                                          (16, 200, 2048, 2), (4, 2048, 16384, 0), (5, 2040, 16392, 0)])
 def test_skinny_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, M, N, K, ksplit):
     # K slices reduced in fixed order by the last-arriving slice; library choice (0) splits
-    # until the op has about four tiles per CU
+    # until the op has about four tiles per CU.  The two large cases take 32-column tiles (two
+    # column groups sharing each activation load; the second with ragged N and a K tail).
     seed = (M * 7 + N * 3 + K) % 991
     x, x64 = rand((M, K), dtype, seed)
     w, w64 = rand((N, K), dtype, seed + 1, -0.05, 0.05)
@@ -91,7 +92,8 @@ def test_skinny_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, M, N, K, 
     y = empty((M, N), dtype)
     op = ops.gemm(x, w, y, bias=f32_dev(b64), act="relu", tile=5, ksplit=ksplit)
     assert op.info.ksplit > 1
-    assert op.T == op.info.ksplit * ((N + 15) // 16)
+    assert op.info.tile_n == (32 if K >= 16384 else 16)
+    assert op.T == op.info.ksplit * ((N + op.info.tile_n - 1) // op.info.tile_n)
     op.run()
     torch.cuda.synchronize()
     ref = orc.linear(x64, w64, bias=b64, act="relu")

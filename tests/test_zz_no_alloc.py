@@ -103,7 +103,7 @@ def test_noalloc_rejects_what_does_not_fit():
     d = L.OpDesc()
     d.kind, d.dtype = L.OP_GEMM, L.F16
     d.m, d.nn, d.kk = 16, 4096, K
-    d.tile, d.ksplit = 5, 512  # 256 output tiles x 512 slices x 1 KiB of partials: beyond the scratch
+    d.tile, d.ksplit = 5, 512  # 512 slices of every output tile: 128 MiB of partials, beyond the scratch
     d.x, d.wt, d.y = x.data_ptr(), w.data_ptr(), y.data_ptr()
     rc, h = _create(L, d, True)
     assert rc == L.ERANGE, rc
