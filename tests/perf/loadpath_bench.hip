@@ -135,10 +135,10 @@ __global__ __launch_bounds__(256) void stream_kernel(const u32x4 *src, long long
 // 16 (g % 256) .. +15 and K slice g / 256 (of 4), wave w the slice's quarter w (1568 values).
 // ROWPAT 1 (the skinny kernel's MFMA-operand pattern): a load instruction reads 64 B of each of
 // the 16 rows (lane l: row l % 16, 16 B at 8 (l / 16) values into a 32-value step), 4 steps per
-// group, two groups in flight.  ROWPAT 0: an instruction reads 1 KB of one row (512 values),
-// cycling over the 16 rows, 8 instructions in flight.  Offsets stay inside the buffer: the
-// last 1 KB instruction of a quarter may run past it into the next quarter of the same row,
-// and the last quarter of a row stops at the row's end (clamped).
+// group, one group loaded and consumed at a time.  ROWPAT 0: an instruction reads 1 KB of one
+// row (512 values), cycling over the 16 rows, 16 instructions in flight.  Offsets stay inside
+// the buffer: the last 1 KB instruction of a quarter may run past it into the next quarter of
+// the same row, and the last quarter of a row stops at the row's end (clamped).
 constexpr long long kFcRow = 25088, kFcQ = 1568;
 template <int ROWPAT>
 __global__ __launch_bounds__(256) void fc_stream_kernel(const unsigned short *W, int *sink) {
