@@ -101,7 +101,6 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
     const T *__restrict__ Wt = static_cast<const T *>(a.w);
     T *__restrict__ Y = static_cast<T *>(a.y);
     const T *__restrict__ R = static_cast<const T *>(a.res);
-    const T *const zsrc = reinterpret_cast<const T *>(g_zero_src);
     const int64_t G = gridDim.x;
     const int64_t rank = wg_rank(blockIdx.x, G);
     const int64_t end = sh.begin + sh.len;
@@ -164,28 +163,40 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
         }
     };
 
-    // DMA of the patch of tile `c` into buffer `buf`: instruction j writes slots 64j .. 64j+63
+    // DMA of the patch of tile `c` into buffer `buf`: instruction j writes slots 64j .. 64j+63.
+    // The slot a lane fills is the same in every tile, so its decode (patch row and column,
+    // 16-byte piece, whether the slot holds data) is done once and kept packed in one register
+    // per instruction: bits [0, 7) column, [7, 11) row, [11, 15) piece, bit 15 set for a data
+    // slot.  Per tile a lane then only adds the tile's origin, checks the image bounds and
+    // forms a 32-bit byte offset into the image (the library admits the kernel only for images
+    // of less than 2^31 bytes); pixels outside the image and padding slots take an offset past
+    // the buffer, which reads zeros.
+    static_assert(K_::PW < 128 && K_::PH <= 16 && SP <= 16, "packed patch geometry");
+    uint32_t geo[NJ];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) {
+        const int j = jj * P + pw;
+        const int q = j * kWave + lane;
+        const int pr = q / SP, sl = q - (q / SP) * SP;
+        const int prow = pr / PW, pcol = pr - (pr / PW) * PW;
+        const bool ok = j < NINS && pr < K_::PPIX && sl < NP;
+        geo[jj] = ok ? ((uint32_t)pcol | ((uint32_t)prow << 7) | ((uint32_t)sl << 11) | (1u << 15)) : 0u;
+    }
+    const uint32_t img_bytes = (uint32_t)(a.img_x * (int64_t)sizeof(T));
     auto issue_patch = [&](Cursor c, int buf) {
         const uint32_t tx = c.tx, ty = c.ty, img = c.img;
         const int32_t iy0 = (int32_t)ty * K_::TH * ST - a.pad, ix0 = (int32_t)tx * TW * ST - a.pad;
-        const T *xb = X + (int64_t)img * a.img_x;
+        const rsrc_t rs = make_rsrc(X + (int64_t)img * a.img_x, img_bytes);
         const uint32_t base = lds0 + (uint32_t)(buf * BUF);
-        // the lane index passes through an empty asm so this lane's slot decode is recomputed
-        // at each call instead of being hoisted out of the tile loop, where its results would
-        // sit in registers next to the resident weights
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) {
             const int j = jj * P + pw;
             if (j < NINS) {
-                const int q = j * kWave + ln;
-                const int pr = q / SP, sl = q - (q / SP) * SP;
-                const int prow = pr / PW, pcol = pr - (pr / PW) * PW;
-                const int32_t iy = iy0 + prow, ix = ix0 + pcol;
-                const bool ok = pr < K_::PPIX && sl < NP && (uint32_t)iy < (uint32_t)H32 && (uint32_t)ix < (uint32_t)W32;
-                const int32_t off = (iy * W32 + ix) * ldx32 + sl * VEC;
-                lds_dma16(ok ? xb + off : zsrc, base + (uint32_t)(j * kWave * 16));
+                const uint32_t g = geo[jj];
+                const int32_t iy = iy0 + (int32_t)((g >> 7) & 15u), ix = ix0 + (int32_t)(g & 127u);
+                const bool ok = (g >> 15) != 0u && (uint32_t)iy < (uint32_t)H32 && (uint32_t)ix < (uint32_t)W32;
+                const uint32_t off = (uint32_t)((iy * W32 + ix) * ldx32 + (int32_t)((g >> 11) & 15u) * VEC) * (uint32_t)sizeof(T);
+                buf_dma16(ok ? off : kOutOfRange, rs, 0u, base + (uint32_t)(j * kWave * 16));
             }
         }
     };
@@ -252,10 +263,9 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
                     abase[sl][i] = patch + (y * ST * PW + xl * ST) * PS + (NP == 1 ? 0 : hx * 16);
                 }
             }
-            // one 8-channel tap per operand half (C = 8, 3x3): halves take taps 2s and 2s+1
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                op_t av[SL][2];
+            // operands of k-step s for every block; one 8-channel tap per operand half (C = 8,
+            // 3x3): halves take taps 2s and 2s+1
+            auto fetch = [&](int s, op_t (&av)[SL][2]) {
 #pragma unroll
                 for (int sl = 0; sl < SL; ++sl)
 #pragma unroll
@@ -276,20 +286,25 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
                             av[sl][i] = v;
                         }
                     }
+            };
+            // Software pipeline in program order: the operand reads of step s + LA are issued
+            // before the MFMAs of step s, and a scheduling fence after each step keeps the
+            // compiler from sinking the reads next to their use (it otherwise waited on every
+            // read and ran each block's MFMAs as one dependent chain).  Within a step the
+            // blocks' MFMAs are independent.
+            constexpr int LA = SL == 1 ? 2 : 1;
+            op_t opnd[LA + 1][SL][2];
+#pragma unroll
+            for (int s = 0; s < LA && s < NS; ++s) fetch(s, opnd[s]);
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                if (s + LA < NS) fetch(s + LA, opnd[(s + LA) % (LA + 1)]);
 #pragma unroll
                 for (int sl = 0; sl < SL; ++sl)
 #pragma unroll
                     for (int i = 0; i < 2; ++i)
-                        acc[sl][i] = MF::run(av[sl][i], bw[s], s == 0 ? acc_t{} : acc[sl][i]);
-            }
-            // schedule: operand reads run two k-steps ahead of the MFMAs that use them
-            constexpr int RD = 2 * SL;
-            __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
-            if constexpr (NS > 1) __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                __builtin_amdgcn_sched_group_barrier(0x008, RD, 0);
-                if (s + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+                        acc[sl][i] = MF::run(opnd[s % (LA + 1)][sl][i], bw[s], s == 0 ? acc_t{} : acc[sl][i]);
+                __builtin_amdgcn_sched_barrier(0);
             }
             // ---- epilogue, stage 1: v = acc * sc + sh per channel; without a residual the
             // activation and the one rounding happen here and the tile is staged in the output

@@ -323,7 +323,7 @@ static int create_igemm(miriam_op *op) {
                           (d.kh == 1 && d.kw == 1 && d.stride == 1 && d.pad == 0 &&
                            (d.c == 16 || d.c == 24 || d.c == 32 || d.c == 64));
     const bool rw_ok = d.kind == MIRIAM_OP_CONV2D && d.dtype != MIRIAM_F32 && rw_shape && a_vec && b_vec &&
-                       d.ksplit <= 1 && a.img_x < (int64_t)INT32_MAX;
+                       d.ksplit <= 1 && a.img_x * esize(d.dtype) < ((int64_t)1 << 31);
     const int64_t rw_T = d.n * halo_ty * halo_tx * cdiv(a.Nc, 64);
     int cfg = d.tile;
     // the memory-based index function is served by the pipelined kernel only
@@ -336,7 +336,7 @@ static int create_igemm(miriam_op *op) {
     if (memidx && (cfg == CFG_RW || cfg == CFG_HALO || cfg == TILE_SKINNY))
         return einval("memory-based index function: tiles 1..4 only (pipelined contraction kernel)");
     if (cfg == CFG_RW) {
-        if (!rw_ok) return einval("tile 8 (resident-weight direct conv) needs an fp16/bf16 conv that is 3x3 stride 1 with C in {8,16,32,64} and at most 64 output channels, 3x3 stride 2 with C = 8 and at most 64 output channels, or 1x1 stride 1 pad 0 with C in {16,24,32,64}; 16-byte rows; no split K");
+        if (!rw_ok) return einval("tile 8 (resident-weight direct conv) needs an fp16/bf16 conv that is 3x3 stride 1 with C in {8,16,32,64} and at most 64 output channels, 3x3 stride 2 with C = 8 and at most 64 output channels, or 1x1 stride 1 pad 0 with C in {16,24,32,64}; 16-byte rows; images under 2 GiB; no split K");
         a.tX = halo_tx;
         a.tY = halo_ty;
         a.mT = halo_ty * halo_tx;
