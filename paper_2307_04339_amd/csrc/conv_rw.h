@@ -369,6 +369,30 @@ __global__ __launch_bounds__(kWave * P, (RwKernel<T, C, P, KS, ST>::WAVES_PER_SI
             with_act(a.epi.act, stage2_res);
             continue;
         }
+        if (a.y_bytes != 0u) {
+            // whole 16-byte pieces and an output of less than 2^31 bytes: buffer stores with
+            // 32-bit offsets, pieces outside the output written to an offset past the buffer
+            // (dropped), no branch per piece
+            static_assert((TM * RV) % NT == 0 && RV == 8 && TW == 32, "stage 2 piece decode");
+            const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(Y, (short)0, (int)a.y_bytes, 0x00020000);
+            // (unsigned arithmetic: the offset of a piece outside the output may wrap; it is
+            // replaced before use)
+            const uint32_t orow0 = ((uint32_t)img * (uint32_t)Ho32 + (uint32_t)oy0) * (uint32_t)Wo32 + (uint32_t)ox0;
+            const uint32_t ldyb = (uint32_t)a.ldy * (uint32_t)sizeof(T);
+#pragma unroll
+            for (int it = 0; it < TM * RV / NT; ++it) {
+                const int idx = tid + it * NT;
+                const int row = idx >> 3, cv = idx & 7;
+                const int32_t oy = oy0 + (row >> 5), ox = ox0 + (row & 31);
+                const uint32_t n = 64u * ntile + (uint32_t)(cv * VEC);
+                const bool ok = oy < Ho32 && ox < Wo32 && n < (uint32_t)a.Nc;
+                const uint32_t off = (orow0 + (uint32_t)(row >> 5) * (uint32_t)Wo32 + (uint32_t)(row & 31)) * ldyb +
+                                     n * (uint32_t)sizeof(T);
+                const u32x4 v = *reinterpret_cast<const u32x4 *>(Ys + row * LDY + cv * VEC);
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, (int)(ok ? off : kOutOfRange), 0, 0);
+            }
+            continue;
+        }
 #pragma unroll 1
         for (int idx = tid; idx < TM * RV; idx += NT) {
             const int row = idx / RV, cv = idx - (idx / RV) * RV;

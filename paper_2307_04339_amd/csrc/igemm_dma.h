@@ -147,6 +147,8 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
     const T *__restrict__ X = static_cast<const T *>(a.x);
     const T *__restrict__ Wt = static_cast<const T *>(a.w);
     T *__restrict__ Y = static_cast<T *>(a.y);
+    // output as a buffer (used when a.y_bytes != 0: whole 16-byte pieces, span below 2^31 bytes)
+    const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(Y, (short)0, (int)a.y_bytes, 0x00020000);
     const T *__restrict__ R = static_cast<const T *>(a.res);
     const T *const zsrc = reinterpret_cast<const T *>(g_zero_src);
     const uint32_t HoWo32 = (uint32_t)(a.Ho * a.Wo), Wo32 = (uint32_t)a.Wo;
@@ -522,8 +524,19 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                     const int row = (lam >> 1) * SUBR + r;
                     const int col = FULL ? cv * VEC : (lam & 1) * SUBC + cv * VEC;
                     const int64_t m = m0 + row, n = n0 + col;
-                    if (m >= a.M) continue;
                     const float *cr = Cs + row * LDC + col;
+                    if (!RES && a.y_bytes != 0u) {
+                        // whole 16-byte pieces and an output of less than 2^31 bytes: a buffer
+                        // store with a 32-bit offset (wrapping for rows past M, which are
+                        // replaced by an offset past the buffer, so the store is dropped)
+                        Vec16<T> o;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        const uint32_t off = ((uint32_t)yoff + (uint32_t)m * (uint32_t)a.ldy + (uint32_t)n) * (uint32_t)sizeof(T);
+                        __builtin_amdgcn_raw_buffer_store_b128(o.u, ry, (int)(m < a.M && n < a.Nc ? off : kOutOfRange), 0, 0);
+                        continue;
+                    }
+                    if (m >= a.M) continue;
                     const int64_t off = yoff + m * a.ldy + n;
                     if (a.vec_store && n + VEC <= a.Nc) {
                         Vec16<T> o;

@@ -86,6 +86,7 @@ struct IgemmArgs {
     // bytes addressable from one batch entry's x / w base (chunk-uniform decode only: the
     // operands are read as buffers of this size, below 2^31 bytes)
     uint32_t x_bytes, w_bytes;
+    uint32_t y_bytes;  // resident-weight kernel: output span in bytes when below 2^31 and 16-byte stores apply, else 0
     Epilogue epi;
 };
 

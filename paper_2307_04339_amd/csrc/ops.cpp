@@ -297,10 +297,9 @@ static int create_igemm(miriam_op *op) {
     // (its operands are read with 32-bit byte offsets: the M activation rows and a tile's
     // weight rows must span less than 2^31 bytes)
     const int skinny_cg = skinny_cols(a.M, a.Nc, a.K);
-    const int64_t es_in = esize(d.dtype);
     const bool skinny_ok = d.kind == MIRIAM_OP_GEMM && d.dtype != MIRIAM_F32 && a.M <= 16 && a_vec && b_vec &&
-                           ((a.M - 1) * a.ldx + a.K) * es_in < ((int64_t)1 << 31) &&
-                           ((16 * skinny_cg - 1) * a.ldw + a.K) * es_in < ((int64_t)1 << 31);
+                           ((a.M - 1) * a.ldx + a.K) * es < ((int64_t)1 << 31) &&
+                           ((16 * skinny_cg - 1) * a.ldw + a.K) * es < ((int64_t)1 << 31);
     // direct 3x3 / stride-1 convolution with the input patch in LDS: C a whole number of
     // 128-byte chunks, aligned rows.  The library picks it for layers with at most 64 output
     // channels (one n tile) when it gives 1.5 tiles per CU and the 32-pixel tile columns waste
@@ -343,6 +342,11 @@ static int create_igemm(miriam_op *op) {
         a.nT = cdiv(a.Nc, 64);
         a.ksplit = 1;
         a.cps = 1;
+        {
+            // whole 16-byte output pieces within 2^31 bytes: the kernel's buffer-store epilogue
+            const int64_t y_span = d.n * a.Ho * a.Wo * a.ldy * (int64_t)esize(d.dtype);
+            a.y_bytes = (a.vec_store && a.Nc % vec_elems(d.dtype) == 0 && y_span < ((int64_t)1 << 31)) ? (uint32_t)y_span : 0u;
+        }
         op->T = d.n * a.mT * a.nT;
         op->cfg = cfg;
         op->tile_m = 128;
@@ -457,6 +461,11 @@ static int create_igemm(miriam_op *op) {
                 a.x_bytes = (uint32_t)x_span;
                 a.w_bytes = (uint32_t)w_span;
             }
+            // the epilogue stores whole 16-byte pieces as buffer stores with 32-bit offsets
+            // when there is one batch entry and the output spans less than 2^31 bytes
+            const int64_t y_span = a.M * a.ldy * es;
+            if (batch == 1 && a.vec_store && a.Nc % (16 / es) == 0 && y_span < ((int64_t)1 << 31))
+                a.y_bytes = (uint32_t)y_span;
         }
         if (!memidx && get_igemm_table(d.dtype, cfg, op->lay, op->kern, &op->lds_bytes) != 0)
             return einval("no kernel for this dtype / layout");
