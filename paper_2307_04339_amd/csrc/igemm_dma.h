@@ -58,7 +58,10 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     r[3] = 0x00020000;  // 32-bit data format, no swizzle: plain byte offsets
     return r;
 }
-constexpr uint32_t kOutOfRange = 0x80000000u;  // past every buffer here (spans are < 2^31 bytes)
+constexpr uint32_t kOutOfRange = 0x80000000u;
+// cache policy of a buffer access with agent-scope coherence (sc1): what relaxed agent-scope
+// atomic loads and stores compile to, here 16 bytes wide
+constexpr int kAgentCoherent = 16;  // past every buffer here (spans are < 2^31 bytes)
 
 // One 16-byte-per-lane buffer -> LDS load: lane i reads bytes [voff + soff, + 16) of the buffer
 // (zeros when voff is out of range) into LDS bytes [lds + 16 i, + 16).  Ordered like lds_dma16.
@@ -252,6 +255,90 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
         const int c0 = (int)slice * a.cps;
         const int nsl = c0 >= nch ? 0 : ((nch - c0) < a.cps ? (nch - c0) : a.cps);  // chunks of this slice
         float *const part = a.ksplit > 1 ? a.work + (int64_t)t * (TM * TN) : nullptr;
+
+        // ---- epilogue of round rd: stage 1, accumulators * sc + sh (bias, BN) -> LDS as fp32
+        auto epilogue = [&](int rd, acc_t (&acc)[SL][BM][BN]) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                const int lam = (rd * SL + s) * P + pw;
+                const int wm = lam >> 1, wn = lam & 1;
+                trace_wave(sh, t, lam, pw, rd * SL + s);
+#pragma unroll
+                for (int jn = 0; jn < BN; ++jn) {
+                    const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                    const int64_t n = n0 + col;
+                    float sc, shf;
+                    chan_affine(a.epi, n < a.Nc ? n : 0, sc, shf);
+#pragma unroll
+                    for (int i = 0; i < BM; ++i) {
+                        float *const cb = Cs + (wm * (TM / 2) + i * MS + (lane / MS) * 4) * LDC + col;
+#pragma unroll
+                        for (int e = 0; e < MF::NACC; ++e) {
+                            const int rr = (e / 4) * (4 * (kWave / MS)) + (e % 4);
+                            cb[rr * LDC] = acc[s][i][jn][e] * sc + shf;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            // ---- stage 2: + residual, activation, one rounding, coalesced row stores.
+            // When this pass holds both column halves of its rows (always for 4-wave blocks),
+            // consecutive threads cover whole output rows of the tile, so every store
+            // instruction writes full rows (TN * sizeof(T) contiguous bytes each) rather
+            // than half rows whose other halves arrive later.
+            auto stage2 = [&](auto actc, auto resc) {
+                constexpr int ACT = decltype(actc)::value;
+                constexpr bool RES = decltype(resc)::value != 0;
+                constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
+                constexpr bool FULL = (SL * P) % 2 == 0;
+                constexpr int RV = FULL ? 2 * CV : CV;  // vectors per stored row segment
+                constexpr int ROWS = FULL ? (SL * P / 2) * SUBR : SL * P * SUBR;
+                const int lam0 = rd * SL * P;
+                for (int idx = tid; idx < ROWS * RV; idx += NT) {
+                    const int rr2 = idx / RV, cv = idx - (idx / RV) * RV;
+                    // FULL: row block (lam0 / 2 + rr2 / SUBR) and both halves; else sub-tile lam0 + rr2 / SUBR
+                    const int blk = rr2 / SUBR, r = rr2 - blk * SUBR;
+                    const int lam = FULL ? lam0 + 2 * blk : lam0 + blk;
+                    const int row = (lam >> 1) * SUBR + r;
+                    const int col = FULL ? cv * VEC : (lam & 1) * SUBC + cv * VEC;
+                    const int64_t m = m0 + row, n = n0 + col;
+                    const float *cr = Cs + row * LDC + col;
+                    if (!RES && a.y_bytes != 0u) {
+                        // whole 16-byte pieces and an output of less than 2^31 bytes: a buffer
+                        // store with a 32-bit offset (wrapping for rows past M, which are
+                        // replaced by an offset past the buffer, so the store is dropped)
+                        Vec16<T> o;
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        const uint32_t off = ((uint32_t)yoff + (uint32_t)m * (uint32_t)a.ldy + (uint32_t)n) * (uint32_t)sizeof(T);
+                        __builtin_amdgcn_raw_buffer_store_b128(o.u, ry, (int)(m < a.M && n < a.Nc ? off : kOutOfRange), 0, 0);
+                        continue;
+                    }
+                    if (m >= a.M) continue;
+                    const int64_t off = yoff + m * a.ldy + n;
+                    if (a.vec_store && n + VEC <= a.Nc) {
+                        Vec16<T> o;
+                        if constexpr (RES) {
+                            const Vec16<T> rv = ld_vec(R + off);
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e)
+                                o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e] + TypeOps<T>::to_f(rv.e[e])));
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
+                        }
+                        st_vec(Y + off, o);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (n + e < a.Nc) st_f(Y + off + e, act_c<ACT>(RES ? cr[e] + ld_f(R + off + e) : cr[e]));
+                    }
+                }
+            };
+            if (has_res) with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<1>{}); });
+            else with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<0>{}); });
+            __syncthreads();
+        };
 
         for (int rd = 0; rd < ROUNDS; ++rd) {
             acc_t acc[SL][BM][BN];
@@ -456,110 +543,35 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
             __syncthreads();
 
             if (a.ksplit > 1) {
-                // split K: store this slice's raw partial tile; the reduction follows the rounds
+                // split K: store this slice's raw partial tile; the reduction follows the rounds.
+                // Layout: fragment (logical wave, i, jn), then quarter q of the lane's NACC
+                // accumulators, then lane: each 16-byte agent-scope (device-coherent) store
+                // instruction writes 1 KB contiguous; the reducing slice reads every slice back
+                // in the same layout.
+                const __amdgpu_buffer_rsrc_t rp =
+                    __builtin_amdgcn_make_buffer_rsrc(part, (short)0, (int)(TM * TN * sizeof(float)), 0x00020000);
 #pragma unroll
                 for (int s = 0; s < SL; ++s) {
                     const int lam = (rd * SL + s) * P + pw;
-                    const int wm = lam >> 1, wn = lam & 1;
                     trace_wave(sh, t, lam, pw, rd * SL + s);
 #pragma unroll
                     for (int i = 0; i < BM; ++i)
 #pragma unroll
                         for (int jn = 0; jn < BN; ++jn) {
-                            const int col = wn * (TN / 2) + jn * MS + lane % MS;
+                            const int f = (lam * BM + i) * BN + jn;
 #pragma unroll
-                            for (int e = 0; e < MF::NACC; ++e) {
-                                const int rr = (e / 4) * (4 * (kWave / MS)) + (lane / MS) * 4 + (e % 4);
-                                const int row = wm * (TM / 2) + i * MS + rr;
-                                __hip_atomic_store(part + row * TN + col, acc[s][i][jn][e], __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT);
+                            for (int q = 0; q < MF::NACC / 4; ++q) {
+                                const f32x4 v = {acc[s][i][jn][4 * q], acc[s][i][jn][4 * q + 1], acc[s][i][jn][4 * q + 2],
+                                                 acc[s][i][jn][4 * q + 3]};
+                                const uint32_t fo = (uint32_t)((f * (MF::NACC / 4) + q) * kWave + lane) * 16u;
+                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rp, (int)fo, 0,
+                                                                       kAgentCoherent);
                             }
                         }
                 }
                 continue;
             }
-
-            // ---- epilogue, stage 1: accumulators * sc + sh (bias, BN) -> LDS as fp32
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const int lam = (rd * SL + s) * P + pw;
-                const int wm = lam >> 1, wn = lam & 1;
-                trace_wave(sh, t, lam, pw, rd * SL + s);
-#pragma unroll
-                for (int jn = 0; jn < BN; ++jn) {
-                    const int col = wn * (TN / 2) + jn * MS + lane % MS;
-                    const int64_t n = n0 + col;
-                    float sc, shf;
-                    chan_affine(a.epi, n < a.Nc ? n : 0, sc, shf);
-#pragma unroll
-                    for (int i = 0; i < BM; ++i) {
-                        float *const cb = Cs + (wm * (TM / 2) + i * MS + (lane / MS) * 4) * LDC + col;
-#pragma unroll
-                        for (int e = 0; e < MF::NACC; ++e) {
-                            const int rr = (e / 4) * (4 * (kWave / MS)) + (e % 4);
-                            cb[rr * LDC] = acc[s][i][jn][e] * sc + shf;
-                        }
-                    }
-                }
-            }
-            __syncthreads();
-            // ---- stage 2: + residual, activation, one rounding, coalesced row stores.
-            // When this pass holds both column halves of its rows (always for 4-wave blocks),
-            // consecutive threads cover whole output rows of the tile, so every store
-            // instruction writes full rows (TN * sizeof(T) contiguous bytes each) rather
-            // than half rows whose other halves arrive later.
-            auto stage2 = [&](auto actc, auto resc) {
-                constexpr int ACT = decltype(actc)::value;
-                constexpr bool RES = decltype(resc)::value != 0;
-                constexpr int SUBR = TM / 2, SUBC = TN / 2, CV = SUBC / VEC;
-                constexpr bool FULL = (SL * P) % 2 == 0;
-                constexpr int RV = FULL ? 2 * CV : CV;  // vectors per stored row segment
-                constexpr int ROWS = FULL ? (SL * P / 2) * SUBR : SL * P * SUBR;
-                const int lam0 = rd * SL * P;
-                for (int idx = tid; idx < ROWS * RV; idx += NT) {
-                    const int rr2 = idx / RV, cv = idx - (idx / RV) * RV;
-                    // FULL: row block (lam0 / 2 + rr2 / SUBR) and both halves; else sub-tile lam0 + rr2 / SUBR
-                    const int blk = rr2 / SUBR, r = rr2 - blk * SUBR;
-                    const int lam = FULL ? lam0 + 2 * blk : lam0 + blk;
-                    const int row = (lam >> 1) * SUBR + r;
-                    const int col = FULL ? cv * VEC : (lam & 1) * SUBC + cv * VEC;
-                    const int64_t m = m0 + row, n = n0 + col;
-                    const float *cr = Cs + row * LDC + col;
-                    if (!RES && a.y_bytes != 0u) {
-                        // whole 16-byte pieces and an output of less than 2^31 bytes: a buffer
-                        // store with a 32-bit offset (wrapping for rows past M, which are
-                        // replaced by an offset past the buffer, so the store is dropped)
-                        Vec16<T> o;
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
-                        const uint32_t off = ((uint32_t)yoff + (uint32_t)m * (uint32_t)a.ldy + (uint32_t)n) * (uint32_t)sizeof(T);
-                        __builtin_amdgcn_raw_buffer_store_b128(o.u, ry, (int)(m < a.M && n < a.Nc ? off : kOutOfRange), 0, 0);
-                        continue;
-                    }
-                    if (m >= a.M) continue;
-                    const int64_t off = yoff + m * a.ldy + n;
-                    if (a.vec_store && n + VEC <= a.Nc) {
-                        Vec16<T> o;
-                        if constexpr (RES) {
-                            const Vec16<T> rv = ld_vec(R + off);
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e)
-                                o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e] + TypeOps<T>::to_f(rv.e[e])));
-                        } else {
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e) o.e[e] = TypeOps<T>::from_f(act_c<ACT>(cr[e]));
-                        }
-                        st_vec(Y + off, o);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            if (n + e < a.Nc) st_f(Y + off + e, act_c<ACT>(RES ? cr[e] + ld_f(R + off + e) : cr[e]));
-                    }
-                }
-            };
-            if (has_res) with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<1>{}); });
-            else with_act(a.epi.act, [&](auto actc) { stage2(actc, ActTag<0>{}); });
-            __syncthreads();
+            epilogue(rd, acc);
         }
 
         if (a.ksplit > 1) {
@@ -586,46 +598,55 @@ __global__ __launch_bounds__(kWave * P, (DmaKernel<T, TM, TN, MS, P>::WAVES_PER_
                 if (*s_lastp) __hip_atomic_store(a.counters + otile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             __syncthreads();
-            if (*s_lastp) {
-                const float *base = a.work + (int64_t)otile * a.ksplit * (TM * TN);
-                constexpr int CVT = TN / VEC;
-                for (int idx = tid; idx < TM * CVT; idx += NT) {
-                    const int row = idx / CVT, col = (idx - (idx / CVT) * CVT) * VEC;
-                    const int64_t m = m0 + row, n = n0 + col;
-                    if (m >= a.M) continue;
-                    float v[VEC];
+            const bool last = *s_lastp;
+            // the epilogue's staging may overwrite the flag's word
+            __syncthreads();
+            if (last) {
+                // each round's accumulators = the slices' partials added in slice order, read in
+                // the fragment layout they were written in; then the regular epilogue
+                const float *const base = a.work + (int64_t)otile * a.ksplit * (TM * TN);
+                const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float *>(base), (short)0, (int)((int64_t)a.ksplit * TM * TN * sizeof(float)), 0x00020000);
+                for (int rd = 0; rd < ROUNDS; ++rd) {
+                    acc_t acc[SL][BM][BN];
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e)
-                        v[e] = __hip_atomic_load(base + row * TN + col + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    for (int sl = 1; sl < a.ksplit; ++sl)
+                    for (int s = 0; s < SL; ++s) {
+                        const int lam = (rd * SL + s) * P + pw;
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            v[e] += __hip_atomic_load(base + (int64_t)sl * (TM * TN) + row * TN + col + e,
-                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const int64_t off = yoff + m * a.ldy + n;
-                    if (a.vec_store && n + VEC <= a.Nc) {
-                        Vec16<T> rv = (a.epi.flags & EPI_RES) ? ld_vec(R + off) : zero_vec<T>();
-                        Vec16<T> o;
+                        for (int i = 0; i < BM; ++i)
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) {
-                            float sc, shf;
-                            chan_affine(a.epi, n + e, sc, shf);
-                            o.e[e] = TypeOps<T>::from_f(epilogue_post(a.epi, v[e] * sc + shf, TypeOps<T>::to_f(rv.e[e])));
-                        }
-                        st_vec(Y + off, o);
-                    } else {
+                            for (int jn = 0; jn < BN; ++jn) {
+                                const int f = (lam * BM + i) * BN + jn;
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e)
-                            if (n + e < a.Nc) {
-                                const float res = (a.epi.flags & EPI_RES) ? ld_f(R + off + e) : 0.0f;
-                                float sc, shf;
-                                chan_affine(a.epi, n + e, sc, shf);
-                                st_f(Y + off + e, epilogue_post(a.epi, v[e] * sc + shf, res));
+                                for (int q = 0; q < MF::NACC / 4; ++q) {
+                                    const uint32_t fo = (uint32_t)((f * (MF::NACC / 4) + q) * kWave + lane) * 16u;
+                                    auto ld = [&](int sl) {
+                                        return __builtin_bit_cast(
+                                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                       rb, (int)(fo + (uint32_t)sl * (TM * TN * 4u)), 0, kAgentCoherent));
+                                    };
+                                    f32x4 v;
+                                    if (a.ksplit <= 4) {
+                                        // all four loads in flight (slices past ksplit re-read
+                                        // the last one and are not added)
+                                        f32x4 w[4];
+#pragma unroll
+                                        for (int sl = 0; sl < 4; ++sl) w[sl] = ld(sl < a.ksplit ? sl : a.ksplit - 1);
+                                        v = w[0];
+#pragma unroll
+                                        for (int sl = 1; sl < 4; ++sl) v = sl < a.ksplit ? v + w[sl] : v;
+                                    } else {
+                                        v = ld(0);
+                                        for (int sl = 1; sl < a.ksplit; ++sl) v = v + ld(sl);
+                                    }
+#pragma unroll
+                                    for (int e = 0; e < 4; ++e) acc[s][i][jn][4 * q + e] = v[e];
+                                }
                             }
                     }
+                    epilogue(rd, acc);
                 }
             }
-            __syncthreads();
         }
     }
 }

@@ -417,15 +417,26 @@ static int create_igemm(miriam_op *op) {
         a.ksplit = 1;
         a.cps = (int32_t)cdiv(a.K, d.dtype == MIRIAM_F32 ? 32 : 64);  // K chunks of one 128-byte row
         // split K over workgroups with a fixed-order reduction (pipelined kernel only) when
-        // the caller asks for it, or by the library's choice for ops with at most a quarter of
-        // a tile per CU and at least 32 K chunks (a slice keeps 16 or more): ResNet-18 b1
-        // layer 4 as a 49 x 512 x 4608 product 21.0 -> 14.3 us with 4 slices; ops with more
-        // tiles measured slower split (encoder b1 QKV 9.9 -> 14.3 us with 2)
+        // the caller asks for it, or by the library's choice: the most slices, up to 4, that
+        // keep every slice of every tile resident at once (two workgroups per CU), with 8 or
+        // more K chunks per slice when the op fills at most half the CUs and 32 or more when
+        // it fills up to all of them.  A slice's latency-bound chunk loop is that much shorter;
+        // the partial tiles cost one device-coherent write and read each (1 KB per store
+        // instruction).  Measured (unsplit -> split): ResNet-18 b1 layer 3 14.5 -> 11.2 us and
+        // layer 4 21.6 -> 12.5 us at 4 slices; encoder b1 FFN2 (96 32x32 tiles) 16.9 -> 12.7 us
+        // at 4; VGG-16 b8 conv5_x (200 64x64 tiles, 72 chunks) 27.8 -> 24.0 us at 2.  Lost:
+        // encoder b4 FFN2 (192 64x64 tiles, 48 chunks) 22.2 -> 24.0 us at 2; ops whose slices
+        // would not all be resident (conv4_2, 392 tiles: 49.7 -> 62.5 us at 2).
         const int64_t nch = a.cps;
         const bool vec_layout = (a_vec && b_vec && !nmaj);
         int64_t want_ks = d.ksplit;
-        if (d.ksplit == 0 && vec_layout && op->T * 4 <= (int64_t)device_cus() && nch >= 32)
-            want_ks = std::min<int64_t>(4, nch / 16);
+        if (d.ksplit == 0 && vec_layout) {
+            const int64_t slots = 2 * (int64_t)device_cus();
+            const int64_t min_chunks = op->T * 2 <= (int64_t)device_cus() ? 8 : 32;
+            want_ks = 1;
+            for (int64_t k = 2; k <= 4; ++k)
+                if (op->T * k <= slots && nch / k >= min_chunks) want_ks = k;
+        }
         if (want_ks > 1 && vec_layout) {
             int64_t ks = std::min<int64_t>(want_ks, nch);
             if (ks > 1) {

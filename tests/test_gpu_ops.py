@@ -288,6 +288,41 @@ def test_launch_errors_do_not_launch(ops):
     assert torch.isnan(y.float()).all()  # nothing ran
 
 
+@pytest.mark.parametrize("case", ["vgg_conv5", "resnet_l3_res", "encoder_ffn2"])
+def test_library_split_k_matches_oracle_and_is_elastic(ops, orc, case):
+    # the library's own split-K choice on the pipelined kernel (slices reduced in fixed order by
+    # the last to arrive, partials in fragment layout with 16-byte device-coherent accesses):
+    # VGG-16 b8 conv5_x (200 tiles, 2 slices), a ResNet-18 b1 layer-3 convolution with a
+    # residual, the encoder b1 FFN2 product; checked against the oracle in full and bitwise
+    # across shard plans
+    dtype = "f16"
+    if case == "encoder_ffn2":
+        M, N, K = 128, 768, 3072
+        x, x64 = rand((M, K), "bf16", 61)
+        w, w64 = rand((N, K), "bf16", 62, -0.03, 0.03)
+        b64 = np.random.default_rng(63).uniform(-1, 1, N).astype(np.float32).astype(np.float64)
+        y = empty((M, N), "bf16")
+        op = ops.gemm(x, w, y, bias=f32_dev(b64), act="gelu")
+        ref = orc.linear(x64, w64, bias=b64, act="gelu")
+        dtype = "bf16"
+    else:
+        n, h, c, k, res = (8, 14, 512, 512, False) if case == "vgg_conv5" else (1, 14, 256, 256, True)
+        x, x64 = rand((n, h, h, c), dtype, 64)
+        w, w64 = rand((k, 3, 3, c), dtype, 65, -0.02, 0.02)
+        b64 = np.random.default_rng(66).uniform(-1, 1, k).astype(np.float32).astype(np.float64)
+        r, r64 = rand((n, h, h, k), dtype, 67) if res else (None, None)
+        y = empty((n, h, h, k), dtype)
+        op = ops.conv2d(x, w, y, stride=1, pad=1, bias=f32_dev(b64), residual=r, act="relu")
+        ref = orc.conv2d(x64, w64, stride=1, pad=1, bias=b64, residual=r64, act="relu")
+    assert op.info.ksplit > 1, case
+    op.run()
+    torch.cuda.synchronize()
+    err = rel_err(to_f64(y), ref)
+    print(f"library split K {case}: ksplit={op.info.ksplit} T={op.T} tile={op.info.tile_m}x{op.info.tile_n} rel={err:.3e}")
+    assert err <= RTOL[dtype], err
+    _elastic_bitwise(op, y, orc, plans=(1, 2, 3, 8))
+
+
 @pytest.mark.parametrize("tile,shape", [(5, (8, 300, 4096)), (2, None)])
 def test_split_k_counters_reset_after_abandoned_pass(ops, orc, tile, shape):
     # a pass that covers only part of a split-K op's tile space leaves arrival counts behind;
