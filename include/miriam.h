@@ -144,8 +144,11 @@ typedef struct miriam_op_info {
     int32_t path;             /* miriam_kernel_path: which kernel family serves the op */
     int32_t ksplit;           /* K slices per output tile (1 = no split); num_tiles counts slices */
     int32_t full_grid;        /* grid of the op's whole-tile-space (unsharded) launch: num_tiles (one
-                                 workgroup per tile), or for kernels that keep operands resident
-                                 across tiles the workgroups that fit the device at once */
+                                 workgroup per tile); for kernels that keep operands resident
+                                 across tiles the workgroups that fit the device at once; for the
+                                 global->LDS pipelined contraction (paths 2 and 3) with one to two
+                                 rounds of resident workgroups' worth of tiles, half the tiles (two
+                                 per workgroup) */
 } miriam_op_info;
 
 /* Kernel family behind an op (diagnostic; results do not depend on it beyond rounding

@@ -90,6 +90,15 @@ static void query_occupancy(miriam_op *op) {
     // as fit the device at once (one per tile when that is fewer)
     if (op->family == FAM_IGEMM && op->lay == LAY_RW && op->max_wg_per_cu[2] > 0)
         op->full_grid = std::min<int64_t>(op->T, (int64_t)device_cus() * op->max_wg_per_cu[2]);
+    // the pipelined contraction with more tiles than resident workgroups, but at most twice as
+    // many: half as many workgroups, two tiles each, none waiting for a second dispatch (VGG-16
+    // b8 fp16, 128x128 tiles on 512 resident slots, cold caches: conv2_2's 784 tiles 50.8 ->
+    // 49.1 us, conv2_1 34.3 -> 33.1 us, same bits; a grid of the 512 slots, 54.5 us, gives the
+    // second tiles to whole dies, since consecutive ranks share a die)
+    if (op->family == FAM_IGEMM && (op->lay == LAY_VEC || op->lay == LAY_VEC_UNI) && op->max_wg_per_cu[2] > 0) {
+        const int64_t slots = (int64_t)device_cus() * op->max_wg_per_cu[2];
+        if (op->T > slots && op->T <= 2 * slots) op->full_grid = cdiv(op->T, 2);
+    }
 }
 
 static Epilogue make_epi(const miriam_op_desc &d, int64_t C) {

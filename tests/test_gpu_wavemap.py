@@ -146,3 +146,27 @@ def test_residency_figures_match_lds_budget(ops, L):
             assert m * block <= 2048, (name, block, m)
             if op.info.lds_bytes > 0:
                 assert m * op.info.lds_bytes <= LDS_PER_CU, (name, block, m, op.info.lds_bytes)
+
+
+def test_full_grid_of_pipelined_contraction(ops, L):
+    """The unsharded grid of the pipelined contraction: one workgroup per tile up to one round of
+    resident workgroups, half as many workgroups (two tiles each) for one to two rounds, one per
+    tile beyond; the two-tiles-per-workgroup launch gives the bits of the one-per-tile launch."""
+    from gpu_util import bits
+    n_cu = ops.device_info().n_cu
+    for n, hw, c, k, tile in [(8, 112, 128, 128, 0), (8, 56, 256, 256, 0), (8, 56, 64, 64, 1)]:
+        op = _conv(ops, "f16", n, hw, hw, c, k, tile=tile)
+        info = op.info
+        assert info.path in (L.PATH_DMA, L.PATH_DMA_UNIFORM), (n, hw, c, k, info.path)
+        T, slots = op.T, n_cu * info.max_wg_per_cu[2]
+        want = (T + 1) // 2 if slots < T <= 2 * slots else T
+        assert info.full_grid == want, (T, slots, info.full_grid)
+        y = op._keep[2]
+        op.run()
+        torch.cuda.synchronize()
+        ref = bits(y)
+        y.fill_(float("nan"))
+        op.launch(0, T, T, 256)
+        torch.cuda.synchronize()
+        assert bits(y) == ref, (T, info.full_grid)
+        print(f"full grid: {n}x{hw}x{hw}x{c}->{k}: T={T} slots={slots} grid={info.full_grid}")
