@@ -130,9 +130,10 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(workload, kernel, tile, path):
+def measured_traffic(workload, kernel, tile, path, grid):
     """HBM bytes per launch of `kernel` from the committed counter summary, or None when
-    there is none for this workload / kernel path / tile or the kernel sources changed since."""
+    there is none for this workload / kernel path / tile / unsharded grid (where recorded) or
+    the kernel sources changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             entries = json.load(f)["entries"]
@@ -140,7 +141,7 @@ def measured_traffic(workload, kernel, tile, path):
         return None
     e = entries.get(f"{workload}:{kernel}")
     if (not e or list(e.get("tile", [])) != list(tile) or e.get("path") != path
-            or e.get("source_sha256") != kernel_source_hash()):
+            or e.get("grid", grid) != grid or e.get("source_sha256") != kernel_source_hash()):
         return None
     fetch = e["fetch_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_fetch_kib"] * 1024.0)
     write = e["write_kib"] * 1024.0 * e["copy_bytes"] / (e["copy_write_kib"] * 1024.0)
@@ -902,7 +903,8 @@ def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
     kern["bytes_per_launch"] = dom["bytes"]
     layer = next(l for l in dom_net.layers if l.name == dom["name"])
     kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
-    kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path)
+    kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path,
+                                       int(layer.op.info.full_grid))
     if layer.kind == "conv":
         log("  vendor context ...")
         result["vendor_context"] = {"kernel": kern["kernel"], **vendor_context(layer, args.reps, flush, dom["us"])}
