@@ -846,7 +846,7 @@ def corun(args, cfg, phases, crit_net, be_tasks, ccfg, pps):
 
 
 def vendor_context(layer, reps, flush, ours_us):
-    """The dominant convolution's shape through the vendor libraries, for context: torch's
+    """A convolution's shape through the vendor libraries, for context: torch's
     conv2d on channels-last tensors and on NCHW copies (MIOpen; convolution only, without the
     fused BN and activation) and the equivalent dense product (M = N*Ho*Wo, N = K, K = KH*KW*C; hipBLASLt via
     torch.matmul).  Same eviction read before each launch and HIP events as the per-layer times."""
@@ -905,9 +905,16 @@ def kernel_phase(args, cfg, be_nets, crit_net, dev, L, result):
     kern["tile"] = [layer.op.info.tile_m, layer.op.info.tile_n]
     kern["traffic"] = measured_traffic(args.config, kern["kernel"], kern["tile"], layer.op.info.path,
                                        int(layer.op.info.full_grid))
-    if layer.kind == "conv":
+    # the vendor libraries on the longest convolution of the dominant network (the dominant
+    # kernel itself when it is one)
+    convs = [k for k in table if k["net"] == dom_net.name
+             and next(x for x in dom_net.layers if x.name == k["name"]).kind == "conv"]
+    vdom = max(convs, key=lambda k: k["us"]) if convs else None
+    if vdom is not None:
+        vlayer = next(x for x in dom_net.layers if x.name == vdom["name"])
         log("  vendor context ...")
-        result["vendor_context"] = {"kernel": kern["kernel"], **vendor_context(layer, args.reps, flush, dom["us"])}
+        result["vendor_context"] = {"kernel": f"{dom_net.name}.{vdom['name']}",
+                                    **vendor_context(vlayer, args.reps, flush, vdom["us"])}
         # every convolution of the dominant network, same comparison
         per = []
         for k in table:
