@@ -114,10 +114,12 @@ typedef struct miriam_op_desc {
                            per output tile (partials reduced in fixed order; the op then owns a device
                            workspace and arrival counters, every pass over the op must cover its whole
                            tile space, and passes over one op must not overlap in time).  The library
-                           choice splits small-batch FC layers (tile 5) up to about four tiles per
-                           CU, and implicit-GEMM ops with at most a quarter of a tile per CU and at
-                           least 32 K chunks into up to 4 slices; the workspace is allocated here,
-                           at creation */
+                           choice splits small-batch FC layers (tile 5) into the fewest slices that
+                           give every CU a tile (twice as many for slices of 8192 K values or more;
+                           slices of about 1024 K values or more), and implicit-GEMM ops into the
+                           most slices, up to 4, whose workgroups are all resident at once (two per
+                           CU) with 8 or more K chunks each (32 or more when the op fills more than
+                           half of the CUs); the workspace is allocated here, at creation */
     int32_t tile;       /* contractions: 0 = library choice, 1 = 32x32, 2 = 64x64, 3 = 128x128, 4 = 128x64,
                            5 = 16-column split-K (GEMM, fp16/bf16, m <= 16), 6 = 256x128,
                            7 = direct 3x3 stride-1 conv: 4x32 output pixels x 64 channels, the tile's

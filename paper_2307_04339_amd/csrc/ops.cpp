@@ -386,15 +386,19 @@ static int create_igemm(miriam_op *op) {
         a.mT = 1;
         a.nT = cdiv(a.Nc, 16 * cg);
         // K slices: each slice keeps at least one group per logical wave.  The library choice
-        // splits until the op has about four tiles per CU, so a shard of a quarter of the op
-        // still gives every CU a tile (more slices measured slower unsharded: VGG-16 fc6 at
-        // eight tiles per CU 73 us against 59 us), and keeps slices of about 1024 K values or
-        // more beyond two slices (VGG-16 fc8, 4096 -> 1000: 12.0 us at 8 slices, 9.9 us at 4)
+        // takes the fewest slices that give every CU a tile, twice as many when those slices
+        // would still hold 8192 K values or more (two tiles per CU, each streaming a long
+        // slice), and keeps slices of about 1024 K values or more.  Measured unsharded (cold
+        // caches, VGG-16 b8 fp16): fc6 (25088 -> 4096, 128 32-column tiles) 46.9 / 50.4 / 42.9 /
+        // 51.0 / 46.8 / 48.0 us at 2 / 3 / 4 / 5 / 6 / 8 slices; fc7 (4096 -> 4096, 256 tiles)
+        // 13.1 / 14.0 / 15.1 us at 1 / 2 / 4; fc8 (4096 -> 1000, 63 tiles) 10.8 / 10.3 / 10.4 /
+        // 12.3 us at 2 / 3 / 4 / 8; the MobileNetV2 b16 classifier (1280 -> 1000) 8.8 / 9.4 us
+        // at 1 / 2.
         const int64_t max_ks = std::max<int64_t>(1, cdiv(a.K, group) / 4);
-        int64_t ks = d.ksplit > 1 ? std::min<int64_t>(d.ksplit, max_ks)
-                     : d.ksplit == 1 ? 1
-                                     : std::min<int64_t>(std::min<int64_t>(max_ks, cdiv(4 * (int64_t)device_cus(), a.nT)),
-                                                         std::max<int64_t>(2, a.K / 1024));
+        int64_t lib_ks = cdiv((int64_t)device_cus(), a.nT);
+        if (a.K / lib_ks >= 8192) lib_ks *= 2;
+        lib_ks = std::min<int64_t>(std::min<int64_t>(lib_ks, max_ks), std::max<int64_t>(1, a.K / 1024));
+        int64_t ks = d.ksplit > 1 ? std::min<int64_t>(d.ksplit, max_ks) : d.ksplit == 1 ? 1 : lib_ks;
         ks = std::max<int64_t>(1, ks);
         // slice length as the kernel derives it (whole numbers of 4 groups); count only the
         // slices that hold K values

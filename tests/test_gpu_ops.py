@@ -82,8 +82,8 @@ def test_gemm_matches_oracle(ops, orc, dtype, case):
 @pytest.mark.parametrize("M,N,K,ksplit", [(4, 300, 4096, 4), (8, 1000, 8192, 0), (2, 64, 3328, 3),
                                           (16, 200, 2048, 2), (4, 2048, 16384, 0), (5, 2040, 16392, 0)])
 def test_skinny_split_k_matches_oracle_and_is_elastic(ops, orc, dtype, M, N, K, ksplit):
-    # K slices reduced in fixed order by the last-arriving slice; library choice (0) splits
-    # until the op has about four tiles per CU.  The two large cases take 32-column tiles (two
+    # K slices reduced in fixed order by the last-arriving slice; library choice (0): the
+    # fewest slices that give every CU a tile.  The two large cases take 32-column tiles (two
     # column groups sharing each activation load; the second with ragged N and a K tail).
     seed = (M * 7 + N * 3 + K) % 991
     x, x64 = rand((M, K), dtype, seed)
