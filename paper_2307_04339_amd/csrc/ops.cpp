@@ -142,12 +142,18 @@ static int device_cus() {
 // workloads: 128x128 when N > 64 and it still gives 1.5 tiles per compute unit (its
 // operands cost the fewest bytes per flop); otherwise the largest of 128x64, 64x64,
 // 32x32 that gives three quarters of a tile per compute unit (a smaller tile beats a
-// larger one once the larger leaves CUs idle).  256x128 never won: too few tiles.
-static int choose_cfg(int64_t batch, int64_t M, int64_t N) {
+// larger one once the larger leaves CUs idle), or 1.1 tiles per compute unit when K is at
+// most four 128-byte chunks: such a tile is mostly its epilogue, and more tiles in flight
+// hide it (MobileNetV2 b16 / b32 1x1 projections and expansions, bf16, with 0.77-0.88 larger
+// tiles per CU: 9.0 -> 8.2, 10.6 -> 9.7, 10.9 -> 9.9, 11.3 -> 10.2 us; with 1.15 per CU the
+// larger tile still wins, 8.5 against 10.7 us; the encoder's K = 768 products keep 64x64 at
+// three quarters of a tile per CU).  256x128 never won: too few tiles.
+static int choose_cfg(int64_t batch, int64_t M, int64_t N, int64_t k_chunks) {
     const int64_t cus = device_cus();
+    const int64_t fill = k_chunks <= 4 ? cus * 11 / 10 : cus * 3 / 4;
     if (N > 64 && batch * cdiv(M, 128) * cdiv(N, 128) >= cus * 3 / 2) return CFG_128;
-    if (batch * cdiv(M, 128) * cdiv(N, 64) >= cus * 3 / 4) return CFG_128x64;
-    if (batch * cdiv(M, 64) * cdiv(N, 64) >= cus * 3 / 4) return CFG_64;
+    if (batch * cdiv(M, 128) * cdiv(N, 64) >= fill) return CFG_128x64;
+    if (batch * cdiv(M, 64) * cdiv(N, 64) >= fill) return CFG_64;
     return CFG_32;
 }
 
@@ -340,7 +346,7 @@ static int create_igemm(miriam_op *op) {
     if (cfg == 0 && !memidx && halo_ok && a.Nc <= 64 && halo_T >= (int64_t)device_cus() * 3 / 2 &&
         halo_tx * 32 * 4 <= a.Wo * 5)
         cfg = CFG_HALO;
-    if (cfg == 0) cfg = (skinny_ok && !memidx) ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc);
+    if (cfg == 0) cfg = (skinny_ok && !memidx) ? TILE_SKINNY : choose_cfg(batch, a.M, a.Nc, cdiv(a.K * es, 128));
     if (memidx && (cfg == CFG_RW || cfg == CFG_HALO || cfg == TILE_SKINNY))
         return einval("memory-based index function: tiles 1..4 only (pipelined contraction kernel)");
     if (cfg == CFG_RW) {
