@@ -25,9 +25,14 @@ static int pix_table_k(int kind, bool vec, const void *out[3]) {
     case PIX_AVG: pix_table_v<T, PIX_AVG>(vec, out); return 0;
     case PIX_EW: pix_table_v<T, PIX_EW>(vec, out); return 0;
     case PIX_DW3:
-        if (!vec) return -1;
-        pix_table<T, 16 / sizeof(T), PIX_DW3>(out);
-        return 0;
+        // 16-bit types only
+        if constexpr (sizeof(T) != 2) {
+            return -1;
+        } else {
+            if (!vec) return -1;
+            pix_table<T, 16 / sizeof(T), PIX_DW3>(out);
+            return 0;
+        }
     default: return -1;
     }
 }

@@ -580,12 +580,15 @@ static int create_pix(miriam_op *op) {
     a.x = d.x; a.w = d.wt; a.y = d.y; a.res = d.residual;
     a.epi = make_epi(d, a.C);
     // 3x3 depthwise with 16-byte channel vectors: strips of kDwStrip output pixels per item
-    // (a third of the input loads per output), where the strips still give three tiles per CU;
-    // measured on MobileNetV2 b16: 56x56x144 25.4 -> 22.0 us, 112x112x32 23.0 -> 21.8 us, while
-    // stride 2 (112 -> 56, C = 96: 21.4 -> 22.2 us) and the smaller layers, left with fewer
-    // tiles than CUs, got slower
-    if (kind == PIX_DW && vec && a.KH == 3 && a.KW == 3 && a.stride == 1 &&
-        cdiv(a.N * a.Ho * cdiv(a.Wo, kDwStrip) * (a.C / v), 256) >= 3 * (int64_t)device_cus())
+    // (a third of the input loads per output), where the strips still give three quarters of a
+    // tile per CU; measured on MobileNetV2 (bf16, cold caches): b16 56x56x144 22.2 -> 19.2 us,
+    // 112x112x32 21.8 -> 18.9 us, 28x28x192 12.8 -> 11.2 us; b32 14x14x576 15.1 -> 11.8 us,
+    // 14x14x384 12.8 -> 11.1 us; with fewer tiles (b16 14x14x384 at 0.66 per CU, 7x7x960 at
+    // 0.4) the per-pixel kernel stays faster (9.0 against 9.4, 7.9 against 8.9 us), as does
+    // stride 2 (112 -> 56, C = 96: 21.4 against 22.2 us)
+    // (16-bit types only: fp32 keeps the per-pixel kernel)
+    if (kind == PIX_DW && vec && d.dtype != MIRIAM_F32 && a.KH == 3 && a.KW == 3 && a.stride == 1 &&
+        cdiv(a.N * a.Ho * cdiv(a.Wo, kDwStrip) * (a.C / v), 256) >= 3 * (int64_t)device_cus() / 4)
         kind = PIX_DW3;
     a.Ws = kind == PIX_DW3 ? cdiv(a.Wo, kDwStrip) : a.Wo;
     a.items = a.N * a.Ho * a.Ws * (a.C / v);
